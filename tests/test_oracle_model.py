@@ -1,0 +1,116 @@
+"""Pins for the oracle decoder: a third-party Llama, brute force, Lemma 1, causality."""
+import numpy as np
+import pytest
+from hypothesis import given, settings, strategies as st
+
+import oracle
+from tests import hf_llama
+from tests.oracle_fixtures import small_model, context
+
+
+def close_to(a, ref, rel):
+    """max|a - ref| <= rel * max|ref|. The transformers Llama keeps RMSNorm and the
+    rotary angles in fp32 even in an fp64 model, so agreement is ~1e-6 relative."""
+    err = np.abs(np.asarray(a) - np.asarray(ref)).max()
+    assert err <= rel * np.abs(ref).max(), (err, np.abs(ref).max())
+
+
+def test_full_prefill_matches_transformers_llama():
+    dims, w, V = small_model(seed=1)
+    toks = context(1, [20], 5, V)
+    h, k, v = oracle.full_prefill(toks, 0, w, dims)
+    ref_h, ref_k, ref_v = hf_llama.prefill(hf_llama.build(w, dims, V), toks)
+    close_to(h, ref_h, 1e-5)
+    close_to(k, ref_k, 1e-5)
+    close_to(v, ref_v, 1e-5)
+
+
+def test_full_prefill_at_offset_matches_transformers_llama():
+    dims, w, V = small_model(seed=2, hq=6, hkv=2, hd=16, D=48)
+    toks = context(2, [13], 0, V)
+    h, k, v = oracle.full_prefill(toks, 37, w, dims)
+    ref_h, ref_k, ref_v = hf_llama.prefill(hf_llama.build(w, dims, V), toks, pos0=37)
+    close_to(h, ref_h, 1e-5)
+    close_to(k, ref_k, 1e-5)
+    close_to(v, ref_v, 1e-5)
+
+
+def brute_attention(q, qp, k, v, kp):
+    nq, hq, hd = q.shape
+    g = hq // k.shape[1]
+    out = np.zeros_like(q)
+    for j in range(nq):
+        for h in range(hq):
+            keys = [t for t in range(k.shape[0]) if kp[t] <= qp[j]]
+            s = [sum(q[j, h, e] * k[t, h // g, e] for e in range(hd)) / np.sqrt(hd) for t in keys]
+            mx = max(s)
+            p = [np.exp(x - mx) for x in s]
+            z = sum(p)
+            for e in range(hd):
+                out[j, h, e] = sum(pi * v[t, h // g, e] for pi, t in zip(p, keys)) / z
+    return out
+
+
+def test_attention_brute_force_gqa_sparse_rows():
+    rng = np.random.default_rng(3)
+    q = rng.standard_normal((5, 4, 4))
+    k = rng.standard_normal((9, 2, 4))
+    v = rng.standard_normal((9, 2, 4))
+    qp = np.array([0, 2, 3, 7, 8])          # sparse, sorted query positions
+    kp = np.arange(9)
+    np.testing.assert_allclose(oracle.attention(q, qp, k, v, kp), brute_attention(q, qp, k, v, kp),
+                               rtol=0, atol=1e-12)
+
+
+def test_first_unit_cache_is_a_causal_prefix_of_full_prefill():
+    dims, w, V = small_model(seed=4)
+    lens = [7, 5]
+    toks = context(4, lens, 3, V)
+    _, kf, vf = oracle.full_prefill(toks, 0, w, dims)
+    kc, vc = oracle.cache_units(toks, lens, w, dims)
+    np.testing.assert_allclose(kc[0], kf[:, :7], rtol=0, atol=1e-12)
+    np.testing.assert_allclose(vc[0], vf[:, :7], rtol=0, atol=1e-12)
+    # the second unit was cached out of context: its deeper-layer states differ
+    assert np.abs(vc[1][1] - vf[1, 7:12]).max() > 1e-3
+
+
+@settings(max_examples=60, deadline=None)
+@given(seed=st.integers(0, 10_000), n=st.integers(1, 12), d=st.sampled_from([2, 4, 8, 16]),
+       dk=st.floats(0.0, 2.0), dv=st.floats(0.0, 2.0))
+def test_lemma1_attention_perturbation_bound(seed, n, d, dk, dv):
+    """Lemma 1 (App. B): ||y - y*|| <= Vmax ||q|| / sqrt(d) * max||dk_i|| + max||dv_i||.
+
+    The constant is the one in the lemma's statement; the proof's last line halves it,
+    which a two-token example violates (see test_lemma1_halved_constant_is_violated).
+    """
+    rng = np.random.default_rng(seed)
+    q = rng.standard_normal((1, 1, d))
+    ks = rng.standard_normal((n, 1, d))
+    vs = rng.standard_normal((n, 1, d))
+    kp = ks + dk * rng.standard_normal((n, 1, d)) / np.sqrt(d)
+    vp = vs + dv * rng.standard_normal((n, 1, d)) / np.sqrt(d)
+    pos = np.arange(n)
+    qpos = np.array([n - 1])
+    y = oracle.attention(q, qpos, kp, vp, pos)[0, 0]
+    ys = oracle.attention(q, qpos, ks, vs, pos)[0, 0]
+    vmax = np.linalg.norm(vs[:, 0], axis=1).max()
+    bound = (vmax * np.linalg.norm(q) / np.sqrt(d) * np.linalg.norm((kp - ks)[:, 0], axis=1).max()
+             + np.linalg.norm((vp - vs)[:, 0], axis=1).max())
+    assert np.linalg.norm(y - ys) <= bound * (1 + 1e-6) + 1e-12
+
+
+def test_lemma1_halved_constant_is_violated():
+    """Two tokens with values +-Vmax and a small symmetric logit shift: the error is
+    Vmax ||q|| eps / sqrt(d), twice the bound with the halved constant."""
+    d, eps = 4, 1e-3
+    q = np.zeros((1, 1, d)); q[0, 0, 0] = 2.0
+    ks = np.zeros((2, 1, d))
+    vs = np.zeros((2, 1, d)); vs[0, 0, 1] = 1.0; vs[1, 0, 1] = -1.0
+    kp = ks.copy(); kp[0, 0, 0] = eps; kp[1, 0, 0] = -eps
+    pos = np.arange(2)
+    y = oracle.attention(q, [1], kp, vs, pos)[0, 0]
+    ys = oracle.attention(q, [1], ks, vs, pos)[0, 0]
+    err = np.linalg.norm(y - ys)
+    halved = 1.0 * 2.0 / (2 * np.sqrt(d)) * eps
+    assert err > 1.9 * halved
+    assert err <= 2.0 / np.sqrt(d) * eps * (1 + 1e-6)
