@@ -1,0 +1,232 @@
+"""Benchmark of the reuse prefill on one MI355X.
+
+One step = one akvs_reuse_prefill call over the whole 3B-class workload (28-layer
+decoder of width 3072, 24/8 heads of 128, FFN 8192; 20 memory units of U{192..256}
+tokens + a 64-token query, ~4.5K tokens; refresh 20 %, check layer 1), with token ids,
+weights and unit caches already resident in HBM. The unit caches are built beforehand
+by the library's own full prefill of each unit at position 0 (not timed).
+
+Prints one JSON line: reuse-prefill tokens/s, the full-prefill baseline on the same
+tokens and the speedup, the roofline figure of the dominant kernel (the bf16 MFMA GEMM,
+timed with HIP events on its launch stream during the timed steps) and the CPU oracle
+timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+MFMA_BF16_PEAK_TFLOPS = 2500.0   # MI355X dense bf16
+HBM_PEAK_GBS = 8000.0
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=10)
+    p.add_argument("--warmup", type=int, default=3)
+    p.add_argument("--workload", default="3b")
+    p.add_argument("--refresh", default="1/5")
+    p.add_argument("--check-layer", type=int, default=1)
+    p.add_argument("--seed", type=int, default=0)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-sample-layers", default="prefix,probe",
+                   help="oracle layers timed for the CPU baseline")
+    return p.parse_args()
+
+
+def gemm_flops(shape, rows_full, t_ctx, m_rows, c):
+    """Algorithmic GEMM flops of one reuse-prefill step.
+
+    Per computed row and layer: 2 * (D*(Hq+2Hkv)*hd + Hq*hd*D + 2F*D + F*D); the prefix
+    layers compute every row, the check layer adds the K/V projection of every unit
+    token, and the layers from the check layer on compute the M recomputed rows."""
+    D, F = shape.d_model, shape.ffn_dim
+    hqw = shape.n_q_heads * shape.head_dim
+    kvw = shape.n_kv_heads * shape.head_dim
+    per_row = 2.0 * (D * (hqw + 2 * kvw) + hqw * D + 2 * F * D + F * D)
+    return (c * rows_full * per_row + 2.0 * t_ctx * D * 2 * kvw
+            + (shape.n_layers - c) * m_rows * per_row)
+
+
+def full_gemm_flops(shape, n):
+    D, F = shape.d_model, shape.ffn_dim
+    hqw = shape.n_q_heads * shape.head_dim
+    kvw = shape.n_kv_heads * shape.head_dim
+    return shape.n_layers * n * 2.0 * (D * (hqw + 2 * kvw) + hqw * D + 2 * F * D + F * D)
+
+
+def cpu_baseline(wl, refresh, c, seed, m_rows):
+    """The oracle, as it stands, on a bounded sample: one prefix layer over all T rows and
+    one layer from the check layer on (M recomputed rows + the unit correction) at the
+    full width and length of the workload, scaled to the L-layer step. Inputs are fresh
+    seeded draws of the same shapes."""
+    import numpy as np
+    import oracle
+    import synthetic
+
+    shape = wl.shape
+    dims = oracle.dims_from(shape.with_layers(1))
+    w = synthetic.make_weights(shape, seed=seed, n_layers=1, embed=False)
+    lw = oracle.split_layer(w["layers"][0], dims)
+    T, tc = wl.n_tokens, wl.n_ctx
+    rng = np.random.default_rng(seed + 5)
+    h = rng.standard_normal((T, shape.d_model)) * 0.02
+    pos = np.arange(T)
+    t0 = time.perf_counter()
+    oracle.decoder_layer(h, pos, lw, dims)
+    t_prefix = time.perf_counter() - t0
+    rows = np.sort(np.concatenate([rng.choice(tc, size=m_rows - wl.query_len, replace=False),
+                                   np.arange(tc, T)]))
+    kc = rng.standard_normal((tc, shape.n_kv_heads, shape.head_dim))
+    vc = rng.standard_normal((tc, shape.n_kv_heads, shape.head_dim))
+    starts = oracle.chunk_starts(wl.chunk_lens)
+    t0 = time.perf_counter()
+    q, kf, vf = oracle.model.project_qkv(h[rows], rows, lw, dims)
+    k_corr = np.empty((T, shape.n_kv_heads, shape.head_dim))
+    v_corr = np.empty_like(k_corr)
+    for s, n in zip(starts, wl.chunk_lens):
+        reuse = oracle.rerotate(kc[s:s + n], s, shape.rope_theta)
+        mu = oracle.probe_offset(kf[:8], reuse[:8])
+        k_corr[s:s + n] = oracle.correct_chunk(reuse, reuse, np.zeros(n, bool), np.ones(n), mu)
+        v_corr[s:s + n] = oracle.correct_chunk(vc[s:s + n], vc[s:s + n], np.zeros(n, bool),
+                                               np.ones(n), mu)
+    k_corr[tc:] = kf[-wl.query_len:]
+    v_corr[tc:] = vf[-wl.query_len:]
+    o = oracle.attention(q, rows, k_corr, v_corr, pos)
+    oracle.model.output_and_mlp(h[rows], o, lw, dims)
+    t_probe = time.perf_counter() - t0
+    L = shape.n_layers
+    t_step = c * t_prefix + (L - c) * t_probe
+    try:
+        import threadpoolctl
+        threads = max(p.get("num_threads", 1) for p in threadpoolctl.threadpool_info()) or 1
+    except Exception:
+        threads = os.cpu_count() or 1
+    return {"value": T / t_step, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": (f"fp64 NumPy oracle at full width and length (T={T}): one prefix layer "
+                       f"({t_prefix:.2f} s) and one probe layer with M={m_rows} rows plus the "
+                       f"unit correction ({t_probe:.2f} s), scaled to {c} + {L - c} layers "
+                       f"(extrapolated step {t_step:.1f} s)")}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+    import torch
+
+    import synthetic
+    from paper_2607_21604_amd import akvs
+    from paper_2607_21604_amd.runtime import Engine
+
+    if not os.path.exists(akvs.LIB_PATH):
+        from paper_2607_21604_amd import build
+        build.build()
+    akvs.load()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    num, den = (int(x) for x in args.refresh.split("/"))
+    wl = synthetic.workload(args.workload, args.seed)
+    shape = wl.shape
+    print(f"# workload {wl.name}: T={wl.n_tokens} ({len(wl.chunk_lens)} units, q={wl.query_len}), "
+          f"L={shape.n_layers}, r={num}/{den}", file=sys.stderr, flush=True)
+
+    w = synthetic.make_weights(shape, seed=args.seed, device=dev)
+    eng = Engine(shape, w, dev)
+    toks = torch.tensor(synthetic.make_tokens(wl.n_tokens, shape.vocab, args.seed),
+                        dtype=torch.int32, device=dev)
+    k_cache, v_cache = eng.cache_units(toks, wl.chunk_lens)
+    torch.cuda.synchronize()
+    print("# unit caches built", file=sys.stderr, flush=True)
+
+    def reuse(outputs=None):
+        return eng.reuse_prefill(toks, wl.chunk_lens, wl.query_len, k_cache, v_cache,
+                                 (num, den), args.check_layer, 0, outputs=outputs)
+
+    out = reuse()
+    for _ in range(args.warmup):
+        reuse(out)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    akvs.akvs_profile_read(akvs.AKVS_K_GEMM)
+    akvs.akvs_profile_enable(1 << akvs.AKVS_K_GEMM)
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    t0.record(stream)
+    for _ in range(args.steps):
+        reuse(out)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    akvs.akvs_profile_enable(0)
+    ms_step = t0.elapsed_time(t1) / args.steps
+    g_launches, g_ms = akvs.akvs_profile_read(akvs.AKVS_K_GEMM)
+    m_rows = int(out["n_rows"].item())
+    print(f"# reuse: {ms_step:.3f} ms/step (wall {1e3 * wall / args.steps:.3f}), M={m_rows}",
+          file=sys.stderr, flush=True)
+
+    # full-prefill baseline on the same tokens (same kernels)
+    eng.full_prefill(toks, want_h=True)
+    for _ in range(args.warmup):
+        eng.full_prefill(toks, want_h=True)
+    torch.cuda.synchronize()
+    t0.record(stream)
+    for _ in range(args.steps):
+        eng.full_prefill(toks, want_h=True)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms_full = t0.elapsed_time(t1) / args.steps
+    print(f"# full prefill: {ms_full:.3f} ms/step", file=sys.stderr, flush=True)
+
+    flops_step = gemm_flops(shape, wl.n_tokens, wl.n_ctx, m_rows, args.check_layer)
+    achieved = flops_step * args.steps / (g_ms * 1e-3) / 1e12 if g_ms > 0 else None
+    per_launch = flops_step * args.steps / max(g_launches, 1)
+    roofline = {"bound": "mfma", "kernel": "k_gemm_bf16",
+                "achieved": achieved, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": achieved / MFMA_BF16_PEAK_TFLOPS if achieved else None,
+                "traffic": None, "launches": g_launches,
+                "avg_launch_us": 1e3 * g_ms / max(g_launches, 1),
+                "algorithmic_flops_per_launch": per_launch,
+                "gemm_share_of_step": g_ms / args.steps / ms_step}
+    cpu = None
+    if not args.no_cpu_baseline:
+        print("# timing the CPU oracle sample", file=sys.stderr, flush=True)
+        cpu = cpu_baseline(wl, (num, den), args.check_layer, args.seed, m_rows)
+    T = wl.n_tokens
+    line = {
+        "metric": "reuse-prefill tokens/s at 20% refresh + speedup vs full prefill, 1 GPU",
+        "value": T / (ms_step * 1e-3), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic: uniform token ids, N(0,0.02^2) random-init weights, unit caches "
+                "from the library's standalone prefill of each unit",
+        "config": {"workload": f"{wl.name}-class reuse prefill: {shape.n_layers} layers, "
+                               f"d_model {shape.d_model}, {shape.n_q_heads}/{shape.n_kv_heads} "
+                               f"heads x {shape.head_dim}, FFN {shape.ffn_dim}; "
+                               f"{len(wl.chunk_lens)} units + {wl.query_len} query tokens",
+                   "tokens": T, "context_tokens": wl.n_ctx, "query_tokens": wl.query_len,
+                   "refresh": f"{num}/{den}", "check_layer": args.check_layer,
+                   "recomputed_rows": m_rows, "recomputed_fraction": m_rows / T},
+        "speedup_vs_full_prefill": ms_full / ms_step,
+        "full_prefill_tokens_per_s": T / (ms_full * 1e-3), "ms_full_prefill": ms_full,
+        "full_prefill_gemm_tflops_upper": full_gemm_flops(shape, T) / (ms_full * 1e-3) / 1e12,
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line))
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,818 @@
+// C ABI of libakvs: argument validation, workspace planning, the step entries and the two
+// whole-procedure drivers (reuse prefill, full prefill). Every entry validates all host-
+// checkable arguments before it enqueues anything.
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <vector>
+
+#include "kernels.h"
+
+using namespace akvs;
+
+namespace {
+
+// ---- errors -------------------------------------------------------------------------------
+thread_local char g_err[768] = "";
+
+akvs_status fail(akvs_status s, const char *fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof g_err, fmt, ap);
+  va_end(ap);
+  return s;
+}
+
+#define REQUIRE(cond, status, ...)                 \
+  do {                                             \
+    if (!(cond)) return fail(status, __VA_ARGS__); \
+  } while (0)
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+size_t es_of(int dtype) { return dtype == AKVS_F32 ? 4 : 2; }
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// ---- kernel timing ------------------------------------------------------------------------
+struct ProfRec {
+  int cls;
+  hipEvent_t a, b;
+};
+struct Prof {
+  std::mutex mu;
+  uint32_t mask = 0;
+  std::vector<hipEvent_t> pool;
+  std::vector<ProfRec> pending;
+  int64_t launches[AKVS_K_NCLASSES] = {};
+  double ms[AKVS_K_NCLASSES] = {};
+};
+Prof g_prof;
+
+hipEvent_t prof_event() {
+  if (!g_prof.pool.empty()) {
+    hipEvent_t e = g_prof.pool.back();
+    g_prof.pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+hipEvent_t prof_begin(hipStream_t s, int cls) {
+  if (!(g_prof.mask & (1u << cls))) return nullptr;
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  hipEvent_t e = prof_event();
+  if (e && hipEventRecord(e, s) != hipSuccess) {
+    g_prof.pool.push_back(e);
+    return nullptr;
+  }
+  return e;
+}
+
+void prof_end(hipStream_t s, int cls, hipEvent_t a) {
+  if (!a) return;
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  hipEvent_t b = prof_event();
+  if (!b || hipEventRecord(b, s) != hipSuccess) {
+    g_prof.pool.push_back(a);
+    if (b) g_prof.pool.push_back(b);
+    return;
+  }
+  g_prof.pending.push_back({cls, a, b});
+}
+
+void prof_drain() {
+  for (const ProfRec &r : g_prof.pending) {
+    float ms = 0.f;
+    if (hipEventSynchronize(r.b) == hipSuccess && hipEventElapsedTime(&ms, r.a, r.b) == hipSuccess) {
+      g_prof.launches[r.cls] += 1;
+      g_prof.ms[r.cls] += ms;
+    }
+    g_prof.pool.push_back(r.a);
+    g_prof.pool.push_back(r.b);
+  }
+  g_prof.pending.clear();
+}
+
+#define LAUNCH(cls, expr)                                                                  \
+  do {                                                                                     \
+    hipEvent_t ev_ = prof_begin(stream, cls);                                                   \
+    hipError_t er_ = (expr);                                                               \
+    if (er_ != hipSuccess) return fail(AKVS_EHIP, "%s: %s", #expr, hipGetErrorString(er_)); \
+    prof_end(stream, cls, ev_);                                                            \
+  } while (0)
+
+// ---- validation -----------------------------------------------------------------------------
+akvs_status check_model(const akvs_model_cfg *m) {
+  REQUIRE(m, AKVS_EINVAL, "model cfg is NULL");
+  REQUIRE(m->dtype == AKVS_F32 || m->dtype == AKVS_BF16, AKVS_EDTYPE,
+          "model dtype must be AKVS_F32 or AKVS_BF16 (got %d)", m->dtype);
+  REQUIRE(m->n_layers >= 1 && m->d_model >= 8 && m->n_q_heads >= 1 && m->n_kv_heads >= 1 &&
+              m->ffn_dim >= 4 && m->vocab >= 1,
+          AKVS_EINVAL, "model sizes must be positive");
+  REQUIRE(m->head_dim == 64 || m->head_dim == 128, AKVS_EUNSUPPORTED,
+          "head_dim %d not supported (64 or 128)", m->head_dim);
+  REQUIRE(m->n_q_heads % m->n_kv_heads == 0, AKVS_ESHAPE,
+          "n_q_heads %d is not a multiple of n_kv_heads %d", m->n_q_heads, m->n_kv_heads);
+  REQUIRE(m->d_model % 8 == 0, AKVS_ESHAPE, "d_model must be a multiple of 8");
+  if (m->dtype == AKVS_BF16) {
+    REQUIRE(m->d_model % 64 == 0 && m->ffn_dim % 64 == 0, AKVS_EUNSUPPORTED,
+            "bf16 models need d_model and ffn_dim multiples of 64");
+  } else {
+    REQUIRE(m->ffn_dim % 4 == 0, AKVS_ESHAPE, "ffn_dim must be a multiple of 4");
+  }
+  REQUIRE(m->rope_theta > 0.f && m->rms_eps >= 0.f, AKVS_EINVAL, "rope_theta > 0, rms_eps >= 0");
+  const long long widest = (long long)(m->n_q_heads + 2 * m->n_kv_heads) * m->head_dim;
+  REQUIRE(widest < (1LL << 30) && (long long)m->d_model * m->ffn_dim < (1LL << 40), AKVS_ESHAPE,
+          "model too large");
+  return AKVS_OK;
+}
+
+akvs_status check_layers(const akvs_model_cfg *m, const akvs_layer_w *lw) {
+  REQUIRE(lw, AKVS_EINVAL, "layer weights are NULL");
+  for (int l = 0; l < m->n_layers; ++l) {
+    const void *p[6] = {lw[l].attn_norm, lw[l].w_qkv, lw[l].w_o, lw[l].mlp_norm, lw[l].w_gate_up,
+                        lw[l].w_down};
+    for (int i = 0; i < 6; ++i) {
+      REQUIRE(p[i], AKVS_EINVAL, "layer %d weight %d is NULL", l, i);
+      REQUIRE(aligned16(p[i]), AKVS_EINVAL, "layer %d weight %d not 16-byte aligned", l, i);
+    }
+  }
+  return AKVS_OK;
+}
+
+struct Meta {
+  std::vector<int32_t> m;  // [n][4]
+  long long t_ctx = 0, sum_b = 0, row_cap = 0, t_all = 0;
+};
+
+akvs_status check_reuse(const akvs_reuse_cfg *c, int n_layers, Meta *meta) {
+  REQUIRE(c, AKVS_EINVAL, "reuse cfg is NULL");
+  REQUIRE(c->n_chunks >= 1 && c->chunk_len, AKVS_EINVAL, "need n_chunks >= 1 and chunk_len");
+  REQUIRE(c->query_len >= 1, AKVS_EINVAL, "query_len must be >= 1");
+  REQUIRE(c->refresh_den >= 1 && c->refresh_num >= 0 && c->refresh_num <= c->refresh_den,
+          AKVS_EINVAL, "refresh ratio must satisfy 0 <= num <= den, den >= 1");
+  const uint32_t known = AKVS_F_NO_CORRECTION | AKVS_F_UNIT_WEIGHTS | AKVS_F_FRESH_IF_RECOMPUTED |
+                         AKVS_F_NO_PREFIX_RECOMPUTE | AKVS_F_GIVEN_PROBES;
+  REQUIRE((c->flags & ~known) == 0, AKVS_EINVAL, "unknown flag bits 0x%x", c->flags & ~known);
+  REQUIRE(!(c->flags & AKVS_F_NO_PREFIX_RECOMPUTE) || c->refresh_num == 0, AKVS_EINVAL,
+          "AKVS_F_NO_PREFIX_RECOMPUTE needs refresh_num == 0");
+  if (n_layers > 0)
+    REQUIRE(c->check_layer >= 0 && c->check_layer < n_layers, AKVS_EINVAL,
+            "check_layer %d outside [0, %d)", c->check_layer, n_layers);
+  Meta loc;
+  Meta &mt = meta ? *meta : loc;
+  mt.m.assign((size_t)c->n_chunks * 4, 0);
+  long long s = 0, off = 0, cap = 0;
+  for (int i = 0; i < c->n_chunks; ++i) {
+    const long long n = c->chunk_len[i];
+    REQUIRE(n >= 1, AKVS_EINVAL, "chunk %d has length %lld", i, n);
+    const long long b = (c->refresh_num * n + c->refresh_den - 1) / c->refresh_den;
+    mt.m[4 * i + 0] = (int32_t)s;
+    mt.m[4 * i + 1] = (int32_t)n;
+    mt.m[4 * i + 2] = (int32_t)b;
+    mt.m[4 * i + 3] = (int32_t)off;
+    s += n;
+    off += b;
+    cap += n < 2 * b ? n : 2 * b;
+    REQUIRE(s + c->query_len < (1LL << 28), AKVS_ESHAPE, "context too long");
+  }
+  mt.t_ctx = s;
+  mt.sum_b = off;
+  mt.row_cap = cap + c->query_len;
+  mt.t_all = s + c->query_len;
+  return AKVS_OK;
+}
+
+akvs_status check_cache(const akvs_cache *c, const akvs_model_cfg *m) {
+  REQUIRE(c && c->k && c->v, AKVS_EINVAL, "cache k/v are NULL");
+  REQUIRE(aligned16(c->k) && aligned16(c->v), AKVS_EINVAL, "cache not 16-byte aligned");
+  if (m->dtype == AKVS_F32) {
+    REQUIRE(c->dtype == AKVS_F32, AKVS_EDTYPE, "an fp32 model needs an AKVS_F32 cache");
+  } else {
+    REQUIRE(c->dtype == AKVS_BF16 || c->dtype == AKVS_U4G64 || c->dtype == AKVS_U2G64,
+            AKVS_EDTYPE, "a bf16 model needs an AKVS_BF16 / U4G64 / U2G64 cache");
+  }
+  if (c->dtype == AKVS_U4G64 || c->dtype == AKVS_U2G64) {
+    REQUIRE(c->k_meta && c->v_meta, AKVS_EINVAL, "quantised cache needs k_meta and v_meta");
+    REQUIRE(aligned16(c->k_meta) && aligned16(c->v_meta), AKVS_EINVAL, "meta not aligned");
+  }
+  return AKVS_OK;
+}
+
+// Cache layer view (plain or quantised) of layer l over t_ctx tokens.
+CacheLayer cache_layer(const akvs_cache *c, int l, long long t_ctx, int hkv, int hd) {
+  CacheLayer v;
+  const long long rows = t_ctx * hkv;
+  size_t row_bytes;
+  if (c->dtype == AKVS_F32) row_bytes = (size_t)hd * 4;
+  else if (c->dtype == AKVS_BF16) row_bytes = (size_t)hd * 2;
+  else if (c->dtype == AKVS_U4G64) row_bytes = (size_t)hd / 2;
+  else row_bytes = (size_t)hd / 4;
+  const size_t lb = (size_t)rows * row_bytes;
+  v.k = reinterpret_cast<const char *>(c->k) + (size_t)l * lb;
+  v.v = reinterpret_cast<const char *>(c->v) + (size_t)l * lb;
+  const size_t mb = (size_t)rows * (hd / 64) * 2;  // halfs per layer
+  v.k_meta = c->k_meta ? reinterpret_cast<const _Float16 *>(c->k_meta) + (size_t)l * mb : nullptr;
+  v.v_meta = c->v_meta ? reinterpret_cast<const _Float16 *>(c->v_meta) + (size_t)l * mb : nullptr;
+  v.dtype = c->dtype;
+  return v;
+}
+
+// ---- workspace carving ------------------------------------------------------------------------
+struct Carver {
+  char *base;
+  size_t off = 0;
+  explicit Carver(void *b) : base(reinterpret_cast<char *>(b)) {}
+  template <typename T>
+  T *take(size_t count) {
+    T *p = base ? reinterpret_cast<T *>(base + off) : nullptr;
+    off += align256(count * sizeof(T));
+    return p;
+  }
+};
+
+// Buffers of a decoder pass over `rows` rows (the full layer and the probe layers).
+struct LayerBufs {
+  void *x, *q, *att, *act;  // model dtype
+};
+
+void carve_layer_bufs(Carver &cv, const akvs_model_cfg *m, long long rows, LayerBufs &b) {
+  const size_t es = es_of(m->dtype);
+  b.x = cv.take<char>((size_t)rows * m->d_model * es);
+  b.q = cv.take<char>((size_t)rows * m->n_q_heads * m->head_dim * es);
+  b.att = cv.take<char>((size_t)rows * m->n_q_heads * m->head_dim * es);
+  b.act = cv.take<char>((size_t)rows * m->ffn_dim * es);
+}
+
+struct ReuseBufs {
+  float *rope;
+  int32_t *meta, *tok_delta, *tok_chunk;
+  float *h_full;
+  LayerBufs lb;
+  void *k_chk, *v_chk;
+  float *d_k, *d_v, *w_k, *w_v;
+  uint8_t *flags;
+  int32_t *chunk_rows, *rows, *n_rows, *fresh_row, *probe_k, *probe_v;
+  float *h_probe;
+  void *k_fresh, *v_fresh;
+  float *mu_k, *mu_v;
+};
+
+size_t carve_reuse(void *ws, const akvs_model_cfg *m, const akvs_reuse_cfg *c, const Meta &mt,
+                   ReuseBufs &b) {
+  Carver cv(ws);
+  const size_t es = es_of(m->dtype);
+  const long long T = mt.t_all, Tc = mt.t_ctx, cap = mt.row_cap;
+  const int kvw = m->n_kv_heads * m->head_dim;
+  b.rope = cv.take<float>((size_t)T * m->head_dim);
+  b.meta = cv.take<int32_t>((size_t)c->n_chunks * 4);
+  b.tok_delta = cv.take<int32_t>((size_t)Tc);
+  b.tok_chunk = cv.take<int32_t>((size_t)Tc);
+  b.h_full = cv.take<float>((size_t)T * m->d_model);
+  carve_layer_bufs(cv, m, T, b.lb);
+  b.k_chk = cv.take<char>((size_t)Tc * kvw * es);
+  b.v_chk = cv.take<char>((size_t)Tc * kvw * es);
+  b.d_k = cv.take<float>((size_t)Tc);
+  b.d_v = cv.take<float>((size_t)Tc);
+  b.w_k = cv.take<float>((size_t)Tc);
+  b.w_v = cv.take<float>((size_t)Tc);
+  b.flags = cv.take<uint8_t>((size_t)Tc);
+  b.chunk_rows = cv.take<int32_t>((size_t)c->n_chunks);
+  b.rows = cv.take<int32_t>((size_t)T);
+  b.n_rows = cv.take<int32_t>(1);
+  b.fresh_row = cv.take<int32_t>((size_t)T);
+  b.probe_k = cv.take<int32_t>((size_t)mt.sum_b + 1);
+  b.probe_v = cv.take<int32_t>((size_t)mt.sum_b + 1);
+  b.h_probe = cv.take<float>((size_t)cap * m->d_model);
+  b.k_fresh = cv.take<char>((size_t)cap * kvw * es);
+  b.v_fresh = cv.take<char>((size_t)cap * kvw * es);
+  b.mu_k = cv.take<float>((size_t)c->n_chunks * kvw);
+  b.mu_v = cv.take<float>((size_t)c->n_chunks * kvw);
+  return cv.off;
+}
+
+struct FullBufs {
+  float *rope, *h;
+  LayerBufs lb;
+};
+
+size_t carve_full(void *ws, const akvs_model_cfg *m, long long n, FullBufs &b) {
+  Carver cv(ws);
+  b.rope = cv.take<float>((size_t)n * m->head_dim);
+  b.h = cv.take<float>((size_t)n * m->d_model);
+  carve_layer_bufs(cv, m, n, b.lb);
+  return cv.off;
+}
+
+size_t carve_step(void *ws, const akvs_model_cfg *m, long long n, void **x, void **act) {
+  Carver cv(ws);
+  const size_t es = es_of(m->dtype);
+  *x = cv.take<char>((size_t)n * m->d_model * es);
+  *act = cv.take<char>((size_t)n * m->ffn_dim * es);
+  return cv.off;
+}
+
+// Small host arrays go to the device as kernel arguments (no pageable copies).
+struct IntChunk {
+  int n;
+  int32_t v[240];
+};
+__global__ void k_put_ints(IntChunk c, int32_t *dst) {
+  for (int i = threadIdx.x; i < c.n; i += blockDim.x) dst[i] = c.v[i];
+}
+hipError_t put_ints(const int32_t *host, size_t n, int32_t *dst, hipStream_t s) {
+  for (size_t o = 0; o < n; o += 240) {
+    IntChunk c;
+    c.n = (int)((n - o) < 240 ? (n - o) : 240);
+    memcpy(c.v, host + o, sizeof(int32_t) * c.n);
+    hipLaunchKernelGGL(k_put_ints, dim3(1), dim3(256), 0, s, c, dst + o);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+// ---- the layer passes -----------------------------------------------------------------------
+Epi qkv_epi(const akvs_model_cfg *m, void *q, void *k, void *v, const int32_t *pos, int pos0,
+            int kv_by_pos, const float *rope, int rope_rows, int rope_base) {
+  Epi e{};
+  e.mode = EPI_QKV;
+  e.out_dtype = m->dtype;
+  e.q_out = q;
+  e.k_out = k;
+  e.v_out = v;
+  e.n_off = 0;
+  e.hq_w = m->n_q_heads * m->head_dim;
+  e.kv_w = m->n_kv_heads * m->head_dim;
+  e.hd = m->head_dim;
+  e.pos = pos;
+  e.pos0 = pos0;
+  e.kv_by_pos = kv_by_pos;
+  e.rope = rope;
+  e.rope_rows = rope_rows;
+  e.rope_base = rope_base;
+  return e;
+}
+
+Epi simple_epi(int mode, void *out, int ldo, int dtype) {
+  Epi e{};
+  e.mode = mode;
+  e.out = out;
+  e.ldo = ldo;
+  e.out_dtype = dtype;
+  return e;
+}
+
+// Attention output projection + MLP over rows (h updated in place).
+akvs_status out_mlp(const akvs_model_cfg *m, const akvs_layer_w &w, float *h, int rows,
+                    const int32_t *rows_dev, const void *att, void *x, void *act,
+                    hipStream_t stream) {
+  const int D = m->d_model, F = m->ffn_dim, hqw = m->n_q_heads * m->head_dim;
+  LAUNCH(AKVS_K_GEMM, launch_gemm(att, hqw, w.w_o, hqw, rows, D, hqw, rows_dev, m->dtype,
+                                  simple_epi(EPI_RESID, h, D, AKVS_F32), stream));
+  LAUNCH(AKVS_K_NORM, launch_rmsnorm(h, D, rows, rows_dev, nullptr, w.mlp_norm, m->dtype, D,
+                                     m->rms_eps, x, m->dtype, D, stream));
+  LAUNCH(AKVS_K_GEMM, launch_gemm(x, D, w.w_gate_up, D, rows, F, D, rows_dev, m->dtype,
+                                  simple_epi(EPI_SWIGLU, act, F, m->dtype), stream));
+  LAUNCH(AKVS_K_GEMM, launch_gemm(act, F, w.w_down, F, rows, D, F, rows_dev, m->dtype,
+                                  simple_epi(EPI_RESID, h, D, AKVS_F32), stream));
+  return AKVS_OK;
+}
+
+// One ordinary causal layer over n consecutive rows at positions pos0.. (keys written to
+// k_dst / v_dst rows 0..n-1).
+akvs_status full_layer(const akvs_model_cfg *m, const akvs_layer_w &w, float *h, int n, int pos0,
+                       const float *rope, const LayerBufs &lb, void *k_dst, void *v_dst,
+                       hipStream_t stream) {
+  const int D = m->d_model;
+  const int qkvw = (m->n_q_heads + 2 * m->n_kv_heads) * m->head_dim;
+  LAUNCH(AKVS_K_NORM, launch_rmsnorm(h, D, n, nullptr, nullptr, w.attn_norm, m->dtype, D,
+                                     m->rms_eps, lb.x, m->dtype, D, stream));
+  LAUNCH(AKVS_K_GEMM, launch_gemm(lb.x, D, w.w_qkv, D, n, qkvw, D, nullptr, m->dtype,
+                                  qkv_epi(m, lb.q, k_dst, v_dst, nullptr, pos0, 0, rope, n, pos0),
+                                  stream));
+  LAUNCH(AKVS_K_ATTENTION, launch_attention(lb.q, nullptr, 0, n, nullptr, k_dst, v_dst, n,
+                                            m->n_q_heads, m->n_kv_heads, m->head_dim, m->dtype,
+                                            lb.att, stream));
+  return out_mlp(m, w, h, n, nullptr, lb.att, lb.x, lb.act, stream);
+}
+
+}  // namespace
+
+// =============================================================================================
+extern "C" {
+
+int32_t akvs_version(void) { return 100; }
+
+const char *akvs_status_string(akvs_status s) {
+  switch (s) {
+    case AKVS_OK: return "ok";
+    case AKVS_EINVAL: return "invalid argument";
+    case AKVS_ESHAPE: return "inconsistent shape";
+    case AKVS_EDTYPE: return "unsupported dtype for this argument";
+    case AKVS_EUNSUPPORTED: return "unsupported configuration";
+    case AKVS_ENOSPACE: return "workspace too small";
+    case AKVS_EHIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+const char *akvs_last_error(void) { return g_err; }
+
+akvs_status akvs_chunk_meta(const akvs_reuse_cfg *cfg, int32_t *meta_out, int32_t *totals_out) {
+  Meta mt;
+  akvs_status st = check_reuse(cfg, 0, &mt);
+  if (st) return st;
+  if (meta_out) memcpy(meta_out, mt.m.data(), mt.m.size() * sizeof(int32_t));
+  if (totals_out) {
+    totals_out[0] = (int32_t)mt.t_ctx;
+    totals_out[1] = (int32_t)mt.sum_b;
+    totals_out[2] = (int32_t)mt.row_cap;
+    totals_out[3] = (int32_t)mt.t_all;
+  }
+  return AKVS_OK;
+}
+
+size_t akvs_workspace_size(const akvs_model_cfg *m, const akvs_reuse_cfg *cfg, int32_t n_tokens) {
+  if (check_model(m) != AKVS_OK) return 0;
+  if (cfg) {
+    Meta mt;
+    if (check_reuse(cfg, m->n_layers, &mt) != AKVS_OK) return 0;
+    ReuseBufs b;
+    return carve_reuse(nullptr, m, cfg, mt, b);
+  }
+  if (n_tokens < 1) return 0;
+  FullBufs b;
+  return carve_full(nullptr, m, n_tokens, b);
+}
+
+size_t akvs_step_workspace_size(const akvs_model_cfg *m, int32_t n_rows) {
+  if (check_model(m) != AKVS_OK || n_rows < 0) return 0;
+  void *x, *a;
+  return carve_step(nullptr, m, n_rows, &x, &a);
+}
+
+akvs_status akvs_profile_enable(int32_t class_mask) {
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  g_prof.mask = (uint32_t)class_mask & ((1u << AKVS_K_NCLASSES) - 1u);
+  return AKVS_OK;
+}
+
+akvs_status akvs_profile_read(int32_t cls, int64_t *launches, double *total_ms) {
+  REQUIRE(cls >= 0 && cls < AKVS_K_NCLASSES, AKVS_EINVAL, "kernel class %d", cls);
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  prof_drain();
+  if (launches) *launches = g_prof.launches[cls];
+  if (total_ms) *total_ms = g_prof.ms[cls];
+  g_prof.launches[cls] = 0;
+  g_prof.ms[cls] = 0.0;
+  return AKVS_OK;
+}
+
+// ---- step entries ---------------------------------------------------------------------------
+
+akvs_status akvs_rope_table(int32_t n_pos, int32_t head_dim, float rope_theta, float *table,
+                            hipStream_t stream) {
+  REQUIRE(n_pos >= 0, AKVS_EINVAL, "n_pos must be >= 0");
+  REQUIRE(head_dim >= 2 && head_dim % 2 == 0 && head_dim <= 1024, AKVS_EINVAL, "bad head_dim");
+  REQUIRE(rope_theta > 0.f, AKVS_EINVAL, "rope_theta must be > 0");
+  REQUIRE(table && aligned16(table), AKVS_EINVAL, "table NULL or misaligned");
+  LAUNCH(AKVS_K_OTHER, launch_rope_table(0, n_pos, head_dim, (double)rope_theta, table, stream));
+  return AKVS_OK;
+}
+
+static akvs_status check_kv_geom(int32_t n_tokens, int32_t hkv, int32_t hd) {
+  REQUIRE(n_tokens >= 0 && hkv >= 1, AKVS_EINVAL, "n_tokens >= 0, n_kv_heads >= 1");
+  REQUIRE(hd == 64 || hd == 128, AKVS_EUNSUPPORTED, "head_dim %d not supported", hd);
+  REQUIRE((long long)n_tokens * hkv * hd < (1LL << 40), AKVS_ESHAPE, "too large");
+  return AKVS_OK;
+}
+
+akvs_status akvs_rerotate_keys(const akvs_cache *src, int32_t n_tokens, int32_t n_kv_heads,
+                               int32_t head_dim, const int32_t *pos_delta, const float *rope,
+                               int32_t rope_rows, void *k_dst, void *v_dst, int32_t dst_dtype,
+                               hipStream_t stream) {
+  akvs_status st = check_kv_geom(n_tokens, n_kv_heads, head_dim);
+  if (st) return st;
+  akvs_model_cfg fake{};
+  fake.dtype = dst_dtype;
+  REQUIRE(dst_dtype == AKVS_F32 || dst_dtype == AKVS_BF16, AKVS_EDTYPE, "dst dtype");
+  st = check_cache(src, &fake);
+  if (st) return st;
+  REQUIRE(pos_delta && rope && rope_rows >= 1 && k_dst && v_dst, AKVS_EINVAL, "NULL argument");
+  REQUIRE(aligned16(rope) && aligned16(k_dst) && aligned16(v_dst), AKVS_EINVAL, "misaligned");
+  CacheLayer cl = cache_layer(src, 0, n_tokens, n_kv_heads, head_dim);
+  LAUNCH(AKVS_K_CORRECTION,
+         launch_correction(cl, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
+                           nullptr, nullptr, pos_delta, nullptr, 0, n_tokens, n_tokens, n_kv_heads,
+                           head_dim, 0u, rope, rope_rows, k_dst, v_dst, dst_dtype, stream));
+  return AKVS_OK;
+}
+
+akvs_status akvs_check_divergence(const void *k_fresh, const void *v_fresh, int32_t fresh_dtype,
+                                  const akvs_cache *cache, int32_t n_tokens, int32_t n_kv_heads,
+                                  int32_t head_dim, const int32_t *pos_delta, const float *rope,
+                                  int32_t rope_rows, float *d_k, float *d_v, hipStream_t stream) {
+  akvs_status st = check_kv_geom(n_tokens, n_kv_heads, head_dim);
+  if (st) return st;
+  REQUIRE(fresh_dtype == AKVS_F32 || fresh_dtype == AKVS_BF16, AKVS_EDTYPE, "fresh dtype");
+  akvs_model_cfg fake{};
+  fake.dtype = fresh_dtype;
+  st = check_cache(cache, &fake);
+  if (st) return st;
+  REQUIRE(k_fresh && v_fresh && d_k && d_v, AKVS_EINVAL, "NULL argument");
+  REQUIRE(aligned16(k_fresh) && aligned16(v_fresh), AKVS_EINVAL, "misaligned");
+  REQUIRE(!pos_delta || (rope && rope_rows >= 1 && aligned16(rope)), AKVS_EINVAL,
+          "pos_delta needs a rotary table");
+  CacheLayer cl = cache_layer(cache, 0, n_tokens, n_kv_heads, head_dim);
+  LAUNCH(AKVS_K_DIVERGENCE,
+         launch_divergence(k_fresh, v_fresh, fresh_dtype, cl, n_tokens, n_kv_heads, head_dim,
+                           pos_delta, rope, pos_delta ? rope_rows : 1, d_k, d_v, stream));
+  return AKVS_OK;
+}
+
+akvs_status akvs_select_probes(const float *d_k, const float *d_v, const akvs_reuse_cfg *cfg,
+                               const int32_t *chunk_meta, int32_t *probe_k, int32_t *probe_v,
+                               float *w_k, float *w_v, uint8_t *flags, int32_t *chunk_rows,
+                               int32_t *rows, int32_t *n_rows, int32_t *fresh_row,
+                               hipStream_t stream) {
+  Meta mt;
+  akvs_status st = check_reuse(cfg, 0, &mt);
+  if (st) return st;
+  REQUIRE(d_k && d_v && chunk_meta && probe_k && probe_v && w_k && w_v && flags && chunk_rows &&
+              rows && n_rows && fresh_row,
+          AKVS_EINVAL, "NULL argument");
+  REQUIRE(aligned16(chunk_meta), AKVS_EINVAL, "chunk_meta misaligned");
+  LAUNCH(AKVS_K_SELECT, launch_select(d_k, d_v, chunk_meta, cfg->n_chunks, (int)mt.t_ctx,
+                                      cfg->query_len, cfg->flags, probe_k, probe_v, w_k, w_v, flags,
+                                      chunk_rows, rows, n_rows, fresh_row, stream));
+  return AKVS_OK;
+}
+
+akvs_status akvs_probe_qkv(const float *h, int32_t n_rows, const int32_t *positions,
+                           const akvs_model_cfg *m, const akvs_layer_w *lw, const float *rope,
+                           int32_t rope_rows, void *q, void *k_fresh, void *v_fresh, void *ws,
+                           size_t ws_bytes, hipStream_t stream) {
+  akvs_status st = check_model(m);
+  if (st) return st;
+  REQUIRE(n_rows >= 0, AKVS_EINVAL, "n_rows must be >= 0");
+  REQUIRE(lw && lw->attn_norm && lw->w_qkv && aligned16(lw->attn_norm) && aligned16(lw->w_qkv),
+          AKVS_EINVAL, "layer weights NULL or misaligned");
+  REQUIRE(h && positions && rope && q && k_fresh && v_fresh, AKVS_EINVAL, "NULL argument");
+  REQUIRE(aligned16(h) && aligned16(rope) && aligned16(q) && aligned16(k_fresh) &&
+              aligned16(v_fresh) && aligned16(ws),
+          AKVS_EINVAL, "misaligned argument");
+  REQUIRE(rope_rows >= 1, AKVS_EINVAL, "rope_rows must be >= 1");
+  void *x, *act;
+  const size_t need = carve_step(nullptr, m, n_rows, &x, &act);
+  REQUIRE(ws && ws_bytes >= need, AKVS_ENOSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+  carve_step(ws, m, n_rows, &x, &act);
+  const int D = m->d_model;
+  const int qkvw = (m->n_q_heads + 2 * m->n_kv_heads) * m->head_dim;
+  LAUNCH(AKVS_K_NORM, launch_rmsnorm(h, D, n_rows, nullptr, nullptr, lw->attn_norm, m->dtype, D,
+                                     m->rms_eps, x, m->dtype, D, stream));
+  LAUNCH(AKVS_K_GEMM,
+         launch_gemm(x, D, lw->w_qkv, D, n_rows, qkvw, D, nullptr, m->dtype,
+                     qkv_epi(m, q, k_fresh, v_fresh, positions, 0, 0, rope, rope_rows, 0), stream));
+  return AKVS_OK;
+}
+
+akvs_status akvs_chunk_offset(const void *k_fresh, const void *v_fresh, const int32_t *fresh_row,
+                              const akvs_cache *cache, const akvs_reuse_cfg *cfg,
+                              const int32_t *chunk_meta, const int32_t *probe_k,
+                              const int32_t *probe_v, const akvs_model_cfg *m, const float *rope,
+                              int32_t rope_rows, float *mu_k, float *mu_v, hipStream_t stream) {
+  akvs_status st = check_model(m);
+  if (st) return st;
+  Meta mt;
+  if ((st = check_reuse(cfg, 0, &mt))) return st;
+  if ((st = check_cache(cache, m))) return st;
+  REQUIRE(k_fresh && v_fresh && fresh_row && chunk_meta && probe_k && probe_v && rope && mu_k &&
+              mu_v,
+          AKVS_EINVAL, "NULL argument");
+  REQUIRE(aligned16(chunk_meta) && aligned16(mu_k) && aligned16(mu_v) && aligned16(rope),
+          AKVS_EINVAL, "misaligned argument");
+  REQUIRE(rope_rows >= 1, AKVS_EINVAL, "rope_rows must be >= 1");
+  CacheLayer cl = cache_layer(cache, 0, mt.t_ctx, m->n_kv_heads, m->head_dim);
+  LAUNCH(AKVS_K_OFFSET, launch_chunk_offset(k_fresh, v_fresh, m->dtype, fresh_row, cl, chunk_meta,
+                                            cfg->n_chunks, probe_k, probe_v, cfg->flags,
+                                            m->n_kv_heads, m->head_dim, rope, rope_rows, mu_k,
+                                            mu_v, stream));
+  return AKVS_OK;
+}
+
+akvs_status akvs_apply_correction(const akvs_cache *cache, const float *mu_k, const float *mu_v,
+                                  const float *w_k, const float *w_v, const uint8_t *flags,
+                                  const void *k_fresh, const void *v_fresh,
+                                  const int32_t *fresh_row, const akvs_reuse_cfg *cfg,
+                                  const int32_t *chunk_meta, const akvs_model_cfg *m,
+                                  const float *rope, int32_t rope_rows, void *k_corr,
+                                  void *v_corr, hipStream_t stream) {
+  akvs_status st = check_model(m);
+  if (st) return st;
+  Meta mt;
+  if ((st = check_reuse(cfg, 0, &mt))) return st;
+  if ((st = check_cache(cache, m))) return st;
+  REQUIRE(mu_k && mu_v && w_k && w_v && flags && k_fresh && v_fresh && fresh_row && chunk_meta &&
+              rope && k_corr && v_corr,
+          AKVS_EINVAL, "NULL argument");
+  REQUIRE(aligned16(mu_k) && aligned16(mu_v) && aligned16(k_fresh) && aligned16(v_fresh) &&
+              aligned16(chunk_meta) && aligned16(rope) && aligned16(k_corr) && aligned16(v_corr),
+          AKVS_EINVAL, "misaligned argument");
+  REQUIRE(rope_rows >= 1, AKVS_EINVAL, "rope_rows must be >= 1");
+  CacheLayer cl = cache_layer(cache, 0, mt.t_ctx, m->n_kv_heads, m->head_dim);
+  LAUNCH(AKVS_K_CORRECTION,
+         launch_correction(cl, mu_k, mu_v, w_k, w_v, flags, k_fresh, v_fresh, fresh_row, nullptr,
+                           nullptr, chunk_meta, cfg->n_chunks, (int)mt.t_ctx, (int)mt.t_all,
+                           m->n_kv_heads, m->head_dim, cfg->flags, rope, rope_rows, k_corr,
+                           v_corr, m->dtype, stream));
+  return AKVS_OK;
+}
+
+akvs_status akvs_sparse_query_attention(const void *q, const int32_t *positions, int32_t n_rows,
+                                        const void *k, const void *v, int32_t n_keys,
+                                        const akvs_model_cfg *m, void *out, hipStream_t stream) {
+  akvs_status st = check_model(m);
+  if (st) return st;
+  REQUIRE(n_rows >= 0 && n_keys >= 1, AKVS_EINVAL, "n_rows >= 0, n_keys >= 1");
+  REQUIRE(q && positions && k && v && out, AKVS_EINVAL, "NULL argument");
+  REQUIRE(aligned16(q) && aligned16(k) && aligned16(v) && aligned16(out), AKVS_EINVAL,
+          "misaligned argument");
+  LAUNCH(AKVS_K_ATTENTION, launch_attention(q, positions, 0, n_rows, nullptr, k, v, n_keys,
+                                            m->n_q_heads, m->n_kv_heads, m->head_dim, m->dtype,
+                                            out, stream));
+  return AKVS_OK;
+}
+
+akvs_status akvs_probe_out_mlp(float *h, int32_t n_rows, const void *attn_out,
+                               const akvs_model_cfg *m, const akvs_layer_w *lw, void *ws,
+                               size_t ws_bytes, hipStream_t stream) {
+  akvs_status st = check_model(m);
+  if (st) return st;
+  REQUIRE(n_rows >= 0, AKVS_EINVAL, "n_rows must be >= 0");
+  REQUIRE(lw && lw->w_o && lw->mlp_norm && lw->w_gate_up && lw->w_down, AKVS_EINVAL,
+          "layer weights NULL");
+  REQUIRE(aligned16(lw->w_o) && aligned16(lw->mlp_norm) && aligned16(lw->w_gate_up) &&
+              aligned16(lw->w_down),
+          AKVS_EINVAL, "layer weights misaligned");
+  REQUIRE(h && attn_out && aligned16(h) && aligned16(attn_out) && aligned16(ws), AKVS_EINVAL,
+          "NULL or misaligned argument");
+  void *x, *act;
+  const size_t need = carve_step(nullptr, m, n_rows, &x, &act);
+  REQUIRE(ws && ws_bytes >= need, AKVS_ENOSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+  carve_step(ws, m, n_rows, &x, &act);
+  return out_mlp(m, *lw, h, n_rows, nullptr, attn_out, x, act, stream);
+}
+
+akvs_status akvs_quantize_cache(const void *x, int32_t x_dtype, int32_t n_rows, int32_t head_dim,
+                                int32_t bits, uint8_t *codes, void *meta, hipStream_t stream) {
+  REQUIRE(x_dtype == AKVS_F32 || x_dtype == AKVS_BF16, AKVS_EDTYPE, "x dtype");
+  REQUIRE(bits == 2 || bits == 4, AKVS_EINVAL, "bits must be 2 or 4");
+  REQUIRE(n_rows >= 0 && head_dim >= 64 && head_dim % 64 == 0, AKVS_EINVAL,
+          "head_dim must be a positive multiple of 64");
+  REQUIRE(x && codes && meta, AKVS_EINVAL, "NULL argument");
+  LAUNCH(AKVS_K_OTHER, launch_quantize(x, x_dtype, n_rows, head_dim, bits, codes,
+                                       reinterpret_cast<_Float16 *>(meta), stream));
+  return AKVS_OK;
+}
+
+// ---- whole-procedure entries ------------------------------------------------------------------
+
+akvs_status akvs_full_prefill(const int32_t *tokens, int32_t n_tokens, int32_t pos0,
+                              const void *embed, const akvs_layer_w *lw, const void *final_norm,
+                              const akvs_model_cfg *m, float *h_out, void *k_out, void *v_out,
+                              void *ws, size_t ws_bytes, hipStream_t stream) {
+  akvs_status st = check_model(m);
+  if (st) return st;
+  if ((st = check_layers(m, lw))) return st;
+  REQUIRE(n_tokens >= 1 && pos0 >= 0 && (long long)pos0 + n_tokens < (1LL << 28), AKVS_EINVAL,
+          "need n_tokens >= 1, pos0 >= 0");
+  REQUIRE(tokens && embed && final_norm && k_out && v_out, AKVS_EINVAL, "NULL argument");
+  REQUIRE(aligned16(embed) && aligned16(final_norm) && aligned16(k_out) && aligned16(v_out) &&
+              (!h_out || aligned16(h_out)) && aligned16(ws),
+          AKVS_EINVAL, "misaligned argument");
+  FullBufs b;
+  const size_t need = carve_full(nullptr, m, n_tokens, b);
+  REQUIRE(ws && ws_bytes >= need, AKVS_ENOSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+  carve_full(ws, m, n_tokens, b);
+  const int D = m->d_model;
+  const size_t kvl = (size_t)n_tokens * m->n_kv_heads * m->head_dim * es_of(m->dtype);
+  LAUNCH(AKVS_K_OTHER, launch_rope_table(pos0, n_tokens, m->head_dim, (double)m->rope_theta,
+                                         b.rope, stream));
+  LAUNCH(AKVS_K_OTHER, launch_embed(tokens, n_tokens, embed, m->dtype, m->vocab, D, b.h, stream));
+  for (int l = 0; l < m->n_layers; ++l) {
+    st = full_layer(m, lw[l], b.h, n_tokens, pos0, b.rope, b.lb,
+                    reinterpret_cast<char *>(k_out) + l * kvl,
+                    reinterpret_cast<char *>(v_out) + l * kvl, stream);
+    if (st) return st;
+  }
+  if (h_out)
+    LAUNCH(AKVS_K_NORM, launch_rmsnorm(b.h, D, n_tokens, nullptr, nullptr, final_norm, m->dtype, D,
+                                       m->rms_eps, h_out, AKVS_F32, D, stream));
+  return AKVS_OK;
+}
+
+akvs_status akvs_reuse_prefill(const int32_t *tokens, const void *embed, const akvs_layer_w *lw,
+                               const void *final_norm, const akvs_model_cfg *m,
+                               const akvs_reuse_cfg *cfg, const akvs_cache *cache,
+                               const akvs_reuse_out *out, void *ws, size_t ws_bytes,
+                               hipStream_t stream) {
+  akvs_status st = check_model(m);
+  if (st) return st;
+  if ((st = check_layers(m, lw))) return st;
+  Meta mt;
+  if ((st = check_reuse(cfg, m->n_layers, &mt))) return st;
+  if ((st = check_cache(cache, m))) return st;
+  REQUIRE(tokens && embed && final_norm && out, AKVS_EINVAL, "NULL argument");
+  REQUIRE(out->h_query && out->k_corr && out->v_corr, AKVS_EINVAL,
+          "h_query, k_corr and v_corr are required outputs");
+  REQUIRE(aligned16(embed) && aligned16(final_norm) && aligned16(out->h_query) &&
+              aligned16(out->k_corr) && aligned16(out->v_corr) && aligned16(ws),
+          AKVS_EINVAL, "misaligned argument");
+  const bool given = (cfg->flags & AKVS_F_GIVEN_PROBES) != 0;
+  REQUIRE(!given || (out->probe_k && out->probe_v), AKVS_EINVAL,
+          "AKVS_F_GIVEN_PROBES needs out->probe_k and out->probe_v holding the sets");
+  ReuseBufs b;
+  const size_t need = carve_reuse(nullptr, m, cfg, mt, b);
+  REQUIRE(ws && ws_bytes >= need, AKVS_ENOSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+  carve_reuse(ws, m, cfg, mt, b);
+  // caller-visible outputs replace their workspace twins
+  if (out->probe_k) b.probe_k = out->probe_k;
+  if (out->probe_v) b.probe_v = out->probe_v;
+  if (out->d_k) b.d_k = out->d_k;
+  if (out->d_v) b.d_v = out->d_v;
+  if (out->rows) b.rows = out->rows;
+  if (out->n_rows) b.n_rows = out->n_rows;
+
+  const int L = m->n_layers, D = m->d_model, hkv = m->n_kv_heads, hd = m->head_dim;
+  const int kvw = hkv * hd, hqw = m->n_q_heads * hd;
+  const int T = (int)mt.t_all, Tc = (int)mt.t_ctx, cap = (int)mt.row_cap;
+  const int nch = cfg->n_chunks;
+  const bool no_prefix = (cfg->flags & AKVS_F_NO_PREFIX_RECOMPUTE) != 0;
+  const int c = no_prefix ? 0 : cfg->check_layer;
+  const size_t es = es_of(m->dtype);
+  const size_t corr_layer = (size_t)T * kvw * es;
+  char *k_corr = reinterpret_cast<char *>(out->k_corr);
+  char *v_corr = reinterpret_cast<char *>(out->v_corr);
+
+  LAUNCH(AKVS_K_OTHER, put_ints(mt.m.data(), mt.m.size(), b.meta, stream));
+  LAUNCH(AKVS_K_OTHER, launch_rope_table(0, T, hd, (double)m->rope_theta, b.rope, stream));
+  LAUNCH(AKVS_K_OTHER, launch_token_setup(b.meta, nch, b.tok_delta, b.tok_chunk, stream));
+  LAUNCH(AKVS_K_OTHER, launch_embed(tokens, T, embed, m->dtype, m->vocab, D, b.h_full, stream));
+
+  // layers before the check layer: every token
+  for (int l = 0; l < c; ++l) {
+    st = full_layer(m, lw[l], b.h_full, T, 0, b.rope, b.lb, k_corr + l * corr_layer,
+                    v_corr + l * corr_layer, stream);
+    if (st) return st;
+  }
+  // check layer: fresh K/V of every unit token, divergence against the re-rotated cache
+  if (!no_prefix) {
+    LAUNCH(AKVS_K_NORM, launch_rmsnorm(b.h_full, D, Tc, nullptr, nullptr, lw[c].attn_norm,
+                                       m->dtype, D, m->rms_eps, b.lb.x, m->dtype, D, stream));
+    Epi e = qkv_epi(m, nullptr, b.k_chk, b.v_chk, nullptr, 0, 0, b.rope, T, 0);
+    e.n_off = hqw;
+    const char *wkv = reinterpret_cast<const char *>(lw[c].w_qkv) + (size_t)hqw * D * es;
+    LAUNCH(AKVS_K_GEMM, launch_gemm(b.lb.x, D, wkv, D, Tc, 2 * kvw, D, nullptr, m->dtype, e,
+                                    stream));
+    LAUNCH(AKVS_K_DIVERGENCE,
+           launch_divergence(b.k_chk, b.v_chk, m->dtype, cache_layer(cache, c, Tc, hkv, hd), Tc,
+                             hkv, hd, b.tok_delta, b.rope, T, b.d_k, b.d_v, stream));
+  }
+  LAUNCH(AKVS_K_SELECT, launch_select(b.d_k, b.d_v, b.meta, nch, Tc, cfg->query_len, cfg->flags,
+                                      b.probe_k, b.probe_v, b.w_k, b.w_v, b.flags, b.chunk_rows,
+                                      b.rows, b.n_rows, b.fresh_row, stream));
+  LAUNCH(AKVS_K_OTHER, launch_gather_rows(b.h_full, T, b.rows, cap, b.n_rows, D, b.h_probe,
+                                          stream));
+  // from the check layer on: recomputed rows only, every unit token corrected
+  const int qkvw = hqw + 2 * kvw;
+  for (int l = c; l < L; ++l) {
+    CacheLayer cl = cache_layer(cache, l, Tc, hkv, hd);
+    LAUNCH(AKVS_K_NORM, launch_rmsnorm(b.h_probe, D, cap, b.n_rows, nullptr, lw[l].attn_norm,
+                                       m->dtype, D, m->rms_eps, b.lb.x, m->dtype, D, stream));
+    LAUNCH(AKVS_K_GEMM,
+           launch_gemm(b.lb.x, D, lw[l].w_qkv, D, cap, qkvw, D, b.n_rows, m->dtype,
+                       qkv_epi(m, b.lb.q, b.k_fresh, b.v_fresh, b.rows, 0, 0, b.rope, T, 0),
+                       stream));
+    LAUNCH(AKVS_K_OFFSET, launch_chunk_offset(b.k_fresh, b.v_fresh, m->dtype, b.fresh_row, cl,
+                                              b.meta, nch, b.probe_k, b.probe_v, cfg->flags, hkv,
+                                              hd, b.rope, T, b.mu_k, b.mu_v, stream));
+    void *kl = k_corr + l * corr_layer;
+    void *vl = v_corr + l * corr_layer;
+    LAUNCH(AKVS_K_CORRECTION,
+           launch_correction(cl, b.mu_k, b.mu_v, b.w_k, b.w_v, b.flags, b.k_fresh, b.v_fresh,
+                             b.fresh_row, b.tok_chunk, b.tok_delta, b.meta, nch, Tc, T, hkv, hd,
+                             cfg->flags, b.rope, T, kl, vl, m->dtype, stream));
+    LAUNCH(AKVS_K_ATTENTION, launch_attention(b.lb.q, b.rows, 0, cap, b.n_rows, kl, vl, T,
+                                              m->n_q_heads, hkv, hd, m->dtype, b.lb.att, stream));
+    st = out_mlp(m, lw[l], b.h_probe, cap, b.n_rows, b.lb.att, b.lb.x, b.lb.act, stream);
+    if (st) return st;
+  }
+  LAUNCH(AKVS_K_NORM, launch_rmsnorm(b.h_probe, D, cfg->query_len, nullptr, b.n_rows, final_norm,
+                                     m->dtype, D, m->rms_eps, out->h_query, AKVS_F32, D, stream));
+  return AKVS_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,324 @@
+// Projection GEMMs C = A . B^T (A [M][K] activations, B [N][K] weights) with fused
+// epilogues: RoPE + q/k/v split (QKV), residual add into the fp32 stream (RESID),
+// SiLU(gate) * up (SWIGLU) and plain stores.
+//
+// bf16 path: 128x128x64 block tiles, 4 waves in 2x2, each wave 64x64 from 2x2 MFMA
+// 32x32x16 bf16 tiles with fp32 accumulation; operand tiles double-buffered in LDS,
+// next tile prefetched into registers during the MFMA loop. The accumulator tile is
+// staged through LDS so every epilogue can pair columns (rotary halves, gate/up) and
+// write coalesced rows. fp32 path (small models): 32x128x32 VALU tiles, same epilogues.
+#include "kernels.h"
+
+namespace akvs {
+
+__device__ __forceinline__ float silu(float g) { return g / (1.0f + __expf(-g)); }
+
+// Epilogue over an LDS tile Cs[BM][ldc] holding C[m0.., n0..] (SWIGLU: gate cols [0,BN/2),
+// up cols [BN/2,BN) of output columns n0..n0+BN/2).
+template <int BM, int BN, int NT>
+__device__ void epilogue_tile(const float *Cs, int ldc, int m0, int n0, int M_eff, int N,
+                              const Epi &e) {
+  const int tid = threadIdx.x;
+  if (e.mode == EPI_STORE || e.mode == EPI_RESID) {
+    constexpr int U = BN / 4;
+    for (int idx = tid; idx < BM * U; idx += NT) {
+      const int r = idx / U, c4 = (idx - (idx / U) * U) * 4;
+      const int gm = m0 + r, gn = n0 + c4;
+      if (gm >= M_eff || gn >= N) continue;
+      const float *src = Cs + r * ldc + c4;
+      if (e.mode == EPI_RESID) {
+        float *hp = reinterpret_cast<float *>(e.out) + (size_t)gm * e.ldo + gn;
+        float4 v = *reinterpret_cast<float4 *>(hp);
+        v.x += src[0]; v.y += src[1]; v.z += src[2]; v.w += src[3];
+        *reinterpret_cast<float4 *>(hp) = v;
+      } else if (e.out_dtype == AKVS_BF16) {
+        store4(reinterpret_cast<bf16_t *>(e.out) + (size_t)gm * e.ldo + gn, src[0], src[1], src[2], src[3]);
+      } else {
+        store4(reinterpret_cast<float *>(e.out) + (size_t)gm * e.ldo + gn, src[0], src[1], src[2], src[3]);
+      }
+    }
+  } else if (e.mode == EPI_SWIGLU) {
+    constexpr int HALF = BN / 2, U = HALF / 4;
+    for (int idx = tid; idx < BM * U; idx += NT) {
+      const int r = idx / U, c4 = (idx - (idx / U) * U) * 4;
+      const int gm = m0 + r, gn = n0 + c4;
+      if (gm >= M_eff || gn >= N) continue;
+      const float *g = Cs + r * ldc + c4;
+      const float *u = g + HALF;
+      const float a0 = silu(g[0]) * u[0], a1 = silu(g[1]) * u[1];
+      const float a2 = silu(g[2]) * u[2], a3 = silu(g[3]) * u[3];
+      if (e.out_dtype == AKVS_BF16)
+        store4(reinterpret_cast<bf16_t *>(e.out) + (size_t)gm * e.ldo + gn, a0, a1, a2, a3);
+      else
+        store4(reinterpret_cast<float *>(e.out) + (size_t)gm * e.ldo + gn, a0, a1, a2, a3);
+    }
+  } else {  // EPI_QKV: every tile holds whole heads of one section
+    const int hd = e.hd, half = hd >> 1;
+    const int lo_units = half >> 2;
+    const int items = (BN / hd) * lo_units;  // per row
+    const float2 *rope = reinterpret_cast<const float2 *>(e.rope);
+    for (int idx = tid; idx < BM * items; idx += NT) {
+      const int r = idx / items, it = idx - (idx / items) * items;
+      const int hs = it / lo_units, u = it - hs * lo_units;
+      const int gm = m0 + r;
+      if (gm >= M_eff || n0 + hs * hd >= N) continue;
+      const int col = e.n_off + n0 + hs * hd + u * 4;  // logical q|k|v column of the lo half
+      const int pos = e.pos ? e.pos[gm] : e.pos0 + gm;
+      const float *src = Cs + r * ldc + hs * hd + u * 4;
+      float lo[4], hi[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        lo[i] = src[i];
+        hi[i] = src[half + i];
+      }
+      if (col < e.hq_w + e.kv_w) {
+        const int p = min(max(pos - e.rope_base, 0), e.rope_rows - 1);
+        const float2 *rr = rope + (size_t)p * half + u * 4;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float2 cs = rr[i];
+          const float a = lo[i], b = hi[i];
+          lo[i] = a * cs.x - b * cs.y;
+          hi[i] = b * cs.x + a * cs.y;
+        }
+      }
+      size_t off;
+      void *base;
+      if (col < e.hq_w) {
+        base = e.q_out;
+        off = (size_t)gm * e.hq_w + col;
+      } else {
+        const int drow = e.kv_by_pos ? pos : gm;
+        if (col < e.hq_w + e.kv_w) {
+          base = e.k_out;
+          off = (size_t)drow * e.kv_w + (col - e.hq_w);
+        } else {
+          base = e.v_out;
+          off = (size_t)drow * e.kv_w + (col - e.hq_w - e.kv_w);
+        }
+      }
+      if (e.out_dtype == AKVS_BF16) {
+        bf16_t *d = reinterpret_cast<bf16_t *>(base) + off;
+        store4(d, lo[0], lo[1], lo[2], lo[3]);
+        store4(d + half, hi[0], hi[1], hi[2], hi[3]);
+      } else {
+        float *d = reinterpret_cast<float *>(base) + off;
+        store4(d, lo[0], lo[1], lo[2], lo[3]);
+        store4(d + half, hi[0], hi[1], hi[2], hi[3]);
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------------------------------------
+// bf16 MFMA GEMM
+constexpr int GB_M = 128, GB_N = 128, GB_K = 64;
+constexpr int G_LDS = GB_K + 8;               // bf16 per LDS row (144 B: staggers banks)
+constexpr int G_TILE = 128 * G_LDS;           // one operand tile
+constexpr int G_SMEM = 2 * 2 * G_TILE * 2;    // 2 buffers x (A, B) x bytes = 73728
+constexpr int G_CLD = GB_N + 4;               // fp32 C tile row stride (67584 B total)
+
+__global__ __launch_bounds__(256, 2) void k_gemm_bf16(const bf16_t *__restrict__ A, int lda,
+                                                      const bf16_t *__restrict__ B, int ldb,
+                                                      int M, int N, int K,
+                                                      const int32_t *m_dev, Epi epi) {
+  __shared__ __attribute__((aligned(16))) unsigned char smem[G_SMEM];
+  bf16_t *sm = reinterpret_cast<bf16_t *>(smem);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  int M_eff = M;
+  if (m_dev) M_eff = min(M, *m_dev);
+  const int m0 = blockIdx.y * GB_M;
+  if (m0 >= M_eff) return;
+  const bool swiglu = epi.mode == EPI_SWIGLU;
+  const int n0 = blockIdx.x * (swiglu ? GB_N / 2 : GB_N);
+
+  const bf16_t *a_src[4];
+  const bf16_t *b_src[4];
+  bool a_ok[4], b_ok[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int c = tid + 256 * i;
+    const int r = c >> 3, kc = (c & 7) * 8;
+    const int gm = m0 + r;
+    a_ok[i] = gm < M_eff;
+    a_src[i] = A + (size_t)(a_ok[i] ? gm : 0) * lda + kc;
+    int gn;
+    if (swiglu) {
+      const int oc = n0 + (r & 63);
+      b_ok[i] = oc < N;
+      gn = (r < 64) ? oc : N + oc;
+    } else {
+      gn = n0 + r;
+      b_ok[i] = gn < N;
+    }
+    b_src[i] = B + (size_t)(b_ok[i] ? gn : 0) * ldb + kc;
+  }
+  uint4 ra[4], rb[4];
+  const uint4 z4 = make_uint4(0, 0, 0, 0);
+  auto gload = [&](int k0) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      ra[i] = a_ok[i] ? *reinterpret_cast<const uint4 *>(a_src[i] + k0) : z4;
+      rb[i] = b_ok[i] ? *reinterpret_cast<const uint4 *>(b_src[i] + k0) : z4;
+    }
+  };
+  auto sstore = [&](int buf) {
+    bf16_t *As = sm + buf * 2 * G_TILE;
+    bf16_t *Bs = As + G_TILE;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int c = tid + 256 * i;
+      const int r = c >> 3, kc = (c & 7) * 8;
+      *reinterpret_cast<uint4 *>(As + r * G_LDS + kc) = ra[i];
+      *reinterpret_cast<uint4 *>(Bs + r * G_LDS + kc) = rb[i];
+    }
+  };
+
+  f32x16_t acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  const int nk = K / GB_K;
+  gload(0);
+  sstore(0);
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    if (kt + 1 < nk) gload((kt + 1) * GB_K);
+    const bf16_t *As = sm + (kt & 1) * 2 * G_TILE;
+    const bf16_t *Bs = As + G_TILE;
+#pragma unroll
+    for (int ks = 0; ks < GB_K / 16; ++ks) {
+      bf16x8_t af[2], bfr[2];
+      const int kk = ks * 16 + (lane >> 5) * 8;
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+        af[i] = *reinterpret_cast<const bf16x8_t *>(As + (wm * 64 + i * 32 + (lane & 31)) * G_LDS + kk);
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        bfr[j] = *reinterpret_cast<const bf16x8_t *>(Bs + (wn * 64 + j * 32 + (lane & 31)) * G_LDS + kk);
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+    }
+    if (kt + 1 < nk) sstore((kt + 1) & 1);
+    __syncthreads();
+  }
+
+  float *Cs = reinterpret_cast<float *>(smem);
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = wm * 64 + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+        const int col = wn * 64 + j * 32 + (lane & 31);
+        Cs[row * G_CLD + col] = acc[i][j][r];
+      }
+  __syncthreads();
+  epilogue_tile<GB_M, GB_N, 256>(Cs, G_CLD, m0, n0, M_eff, N, epi);
+}
+
+// ------------------------------------------------------------------------------------------
+// fp32 VALU GEMM (small fp32 models). 32x128 tile, BK 32, thread = 4 rows x 4 columns.
+constexpr int GF_M = 32, GF_N = 128, GF_K = 32;
+
+__global__ __launch_bounds__(256) void k_gemm_f32(const float *__restrict__ A, int lda,
+                                                  const float *__restrict__ B, int ldb, int M,
+                                                  int N, int K, const int32_t *m_dev, Epi epi) {
+  __shared__ __attribute__((aligned(16))) float smem[GF_M * (GF_N + 4) > GF_K * (GF_M + GF_N + 8)
+                                                        ? GF_M * (GF_N + 4)
+                                                        : GF_K * (GF_M + GF_N + 8)];
+  float *As = smem;                    // [GF_K][GF_M + 4]  (k-major)
+  float *Bs = smem + GF_K * (GF_M + 4);  // [GF_K][GF_N + 4]
+  const int tid = threadIdx.x;
+  int M_eff = M;
+  if (m_dev) M_eff = min(M, *m_dev);
+  const int m0 = blockIdx.y * GF_M;
+  if (m0 >= M_eff) return;
+  const bool swiglu = epi.mode == EPI_SWIGLU;
+  const int n0 = blockIdx.x * (swiglu ? GF_N / 2 : GF_N);
+  const int tr = tid >> 5, tc = tid & 31;  // rows tr*4.., cols tc*4..
+  float acc[4][4] = {};
+  for (int k0 = 0; k0 < K; k0 += GF_K) {
+    __syncthreads();
+    {  // A: 32 rows x 32 k = 256 float4, one per thread
+      const int r = tid >> 3, kc = (tid & 7) * 4;
+      const int gm = m0 + r, gk = k0 + kc;
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (gm < M_eff && gk < K) v = *reinterpret_cast<const float4 *>(A + (size_t)gm * lda + gk);
+      As[(kc + 0) * (GF_M + 4) + r] = v.x;
+      As[(kc + 1) * (GF_M + 4) + r] = v.y;
+      As[(kc + 2) * (GF_M + 4) + r] = v.z;
+      As[(kc + 3) * (GF_M + 4) + r] = v.w;
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {  // B: 128 rows x 32 k = 1024 float4
+      const int c = tid + 256 * i;
+      const int r = c >> 3, kc = (c & 7) * 4;
+      int gn;
+      bool ok;
+      if (swiglu) {
+        const int oc = n0 + (r & 63);
+        ok = oc < N;
+        gn = (r < 64) ? oc : N + oc;
+      } else {
+        gn = n0 + r;
+        ok = gn < N;
+      }
+      const int gk = k0 + kc;
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (ok && gk < K) v = *reinterpret_cast<const float4 *>(B + (size_t)gn * ldb + gk);
+      Bs[(kc + 0) * (GF_N + 4) + r] = v.x;
+      Bs[(kc + 1) * (GF_N + 4) + r] = v.y;
+      Bs[(kc + 2) * (GF_N + 4) + r] = v.z;
+      Bs[(kc + 3) * (GF_N + 4) + r] = v.w;
+    }
+    __syncthreads();
+#pragma unroll 8
+    for (int k = 0; k < GF_K; ++k) {
+      const float4 a = *reinterpret_cast<const float4 *>(As + k * (GF_M + 4) + tr * 4);
+      const float4 b = *reinterpret_cast<const float4 *>(Bs + k * (GF_N + 4) + tc * 4);
+      const float av[4] = {a.x, a.y, a.z, a.w}, bv[4] = {b.x, b.y, b.z, b.w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(av[i], bv[j], acc[i][j]);
+    }
+  }
+  __syncthreads();
+  float *Cs = smem;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) Cs[(tr * 4 + i) * (GF_N + 4) + tc * 4 + j] = acc[i][j];
+  __syncthreads();
+  epilogue_tile<GF_M, GF_N, 256>(Cs, GF_N + 4, m0, n0, M_eff, N, epi);
+}
+
+hipError_t launch_gemm(const void *A, int lda, const void *B, int ldb, int M, int N, int K,
+                       const int32_t *m_dev, int dtype, const Epi &epi, hipStream_t s) {
+  if (M == 0 || N == 0) return hipSuccess;
+  const bool swiglu = epi.mode == EPI_SWIGLU;
+  if (dtype == AKVS_BF16) {
+    const int bn = swiglu ? GB_N / 2 : GB_N;
+    dim3 g((N + bn - 1) / bn, (M + GB_M - 1) / GB_M), b(256);
+    hipLaunchKernelGGL(k_gemm_bf16, g, b, 0, s, reinterpret_cast<const bf16_t *>(A), lda,
+                       reinterpret_cast<const bf16_t *>(B), ldb, M, N, K, m_dev, epi);
+  } else {
+    const int bn = swiglu ? GF_N / 2 : GF_N;
+    dim3 g((N + bn - 1) / bn, (M + GF_M - 1) / GF_M), b(256);
+    hipLaunchKernelGGL(k_gemm_f32, g, b, 0, s, reinterpret_cast<const float *>(A), lda,
+                       reinterpret_cast<const float *>(B), ldb, M, N, K, m_dev, epi);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace akvs

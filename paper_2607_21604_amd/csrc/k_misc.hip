@@ -1,0 +1,163 @@
+// Small bandwidth kernels: rotary table, embedding gather, RMSNorm, row gather.
+#include "kernels.h"
+
+namespace akvs {
+
+// table[p][k] = (cos, sin)(p * theta^(-2k/hd)); angle and trig in fp64.
+__global__ void k_rope_table(int p0, int n_pos, int half, int hd, double theta, float2 *table) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n_pos * half) return;
+  const int row = i / half, k = i - row * half;
+  const int p = p0 + row;
+  const double inv = pow(theta, (-2.0 * (double)k) / (double)hd);
+  const double a = (double)p * inv;
+  double sn, cs;
+  sincos(a, &sn, &cs);
+  table[i] = make_float2((float)cs, (float)sn);
+}
+
+hipError_t launch_rope_table(int p0, int n_pos, int head_dim, double theta, float *table,
+                             hipStream_t s) {
+  const int half = head_dim / 2;
+  const int total = n_pos * half;
+  if (total == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_rope_table, dim3((total + 255) / 256), dim3(256), 0, s, p0, n_pos, half,
+                     head_dim, theta, reinterpret_cast<float2 *>(table));
+  return hipGetLastError();
+}
+
+template <typename TE>
+__global__ void k_embed(const int32_t *tok, int n, const TE *embed, int vocab, int D, float *h) {
+  const int t = blockIdx.x;
+  if (t >= n) return;
+  const int id = tok[t];
+  float *dst = h + (size_t)t * D;
+  const bool ok = id >= 0 && id < vocab;
+  const TE *src = embed + (size_t)(ok ? id : 0) * D;
+  for (int e = threadIdx.x * 8; e < D; e += blockDim.x * 8) {
+    float v[8];
+    load8(src + e, v);
+    if (!ok) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] = 0.f;
+    }
+    store8(dst + e, v);
+  }
+}
+
+hipError_t launch_embed(const int32_t *tok, int n, const void *embed, int dtype, int vocab, int D,
+                        float *h, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  if (dtype == AKVS_BF16)
+    hipLaunchKernelGGL(k_embed<bf16_t>, dim3(n), dim3(128), 0, s, tok, n,
+                       reinterpret_cast<const bf16_t *>(embed), vocab, D, h);
+  else
+    hipLaunchKernelGGL(k_embed<float>, dim3(n), dim3(128), 0, s, tok, n,
+                       reinterpret_cast<const float *>(embed), vocab, D, h);
+  return hipGetLastError();
+}
+
+// One block (256 threads) per row; D % 8 == 0. Sum of squares with a fixed reduction tree.
+template <typename TG, typename TO>
+__global__ void k_rmsnorm(const float *h, int ldh, int rows, const int32_t *rows_dev,
+                          const int32_t *base_dev, const TG *gain, int D, float eps, TO *out,
+                          int ldo) {
+  const int i = blockIdx.x;
+  int lim = rows;
+  if (rows_dev && !base_dev) lim = min(lim, *rows_dev);
+  if (i >= lim) return;
+  int src = i;
+  if (base_dev) {
+    src = *base_dev - rows + i;
+    if (src < 0) return;
+  }
+  const float *x = h + (size_t)src * ldh;
+  float ss = 0.f;
+  for (int e = threadIdx.x * 8; e < D; e += 256 * 8) {
+    float v[8];
+    load8(x + e, v);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) ss = fmaf(v[k], v[k], ss);
+  }
+  __shared__ float red[4];
+  ss = wave_sum(ss);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  const float tot = (red[0] + red[1]) + (red[2] + red[3]);
+  const float inv = 1.0f / sqrtf(tot / (float)D + eps);
+  TO *y = out + (size_t)i * ldo;
+  for (int e = threadIdx.x * 8; e < D; e += 256 * 8) {
+    float v[8], g[8];
+    load8(x + e, v);
+    load8(gain + e, g);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) v[k] = v[k] * inv * g[k];
+    store8(y + e, v);
+  }
+}
+
+hipError_t launch_rmsnorm(const float *h, int ldh, int rows, const int32_t *rows_dev,
+                          const int32_t *base_dev, const void *gain, int gain_dtype, int D,
+                          float eps, void *out, int out_dtype, int ldo, hipStream_t s) {
+  if (rows == 0) return hipSuccess;
+  dim3 g(rows), b(256);
+  if (gain_dtype == AKVS_BF16) {
+    const bf16_t *gn = reinterpret_cast<const bf16_t *>(gain);
+    if (out_dtype == AKVS_BF16)
+      hipLaunchKernelGGL((k_rmsnorm<bf16_t, bf16_t>), g, b, 0, s, h, ldh, rows, rows_dev, base_dev,
+                         gn, D, eps, reinterpret_cast<bf16_t *>(out), ldo);
+    else
+      hipLaunchKernelGGL((k_rmsnorm<bf16_t, float>), g, b, 0, s, h, ldh, rows, rows_dev, base_dev,
+                         gn, D, eps, reinterpret_cast<float *>(out), ldo);
+  } else {
+    const float *gn = reinterpret_cast<const float *>(gain);
+    if (out_dtype == AKVS_BF16)
+      hipLaunchKernelGGL((k_rmsnorm<float, bf16_t>), g, b, 0, s, h, ldh, rows, rows_dev, base_dev,
+                         gn, D, eps, reinterpret_cast<bf16_t *>(out), ldo);
+    else
+      hipLaunchKernelGGL((k_rmsnorm<float, float>), g, b, 0, s, h, ldh, rows, rows_dev, base_dev,
+                         gn, D, eps, reinterpret_cast<float *>(out), ldo);
+  }
+  return hipGetLastError();
+}
+
+__global__ void k_gather_rows(const float *src, int n_src, const int32_t *idx, int cap,
+                              const int32_t *n_dev, int D, float *dst) {
+  const int i = blockIdx.x;
+  if (i >= cap || i >= *n_dev) return;
+  const int j = idx[i];
+  const bool ok = j >= 0 && j < n_src;
+  const float *a = src + (size_t)(ok ? j : 0) * D;
+  float *b = dst + (size_t)i * D;
+  for (int e = threadIdx.x * 4; e < D; e += blockDim.x * 4)
+    *reinterpret_cast<float4 *>(b + e) =
+        ok ? *reinterpret_cast<const float4 *>(a + e) : make_float4(0.f, 0.f, 0.f, 0.f);
+}
+
+hipError_t launch_gather_rows(const float *src, int n_src, const int32_t *idx, int cap,
+                              const int32_t *n_dev, int D, float *dst, hipStream_t s) {
+  if (cap == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_gather_rows, dim3(cap), dim3(256), 0, s, src, n_src, idx, cap, n_dev, D,
+                     dst);
+  return hipGetLastError();
+}
+
+__global__ void k_token_setup(const int4 *meta, int n_chunks, int32_t *tok_delta,
+                              int32_t *tok_chunk) {
+  const int c = blockIdx.x;
+  if (c >= n_chunks) return;
+  const int4 mc = meta[c];
+  for (int j = threadIdx.x; j < mc.y; j += blockDim.x) {
+    tok_delta[mc.x + j] = mc.x;
+    tok_chunk[mc.x + j] = c;
+  }
+}
+
+hipError_t launch_token_setup(const int32_t *meta, int n_chunks, int32_t *tok_delta,
+                              int32_t *tok_chunk, hipStream_t s) {
+  hipLaunchKernelGGL(k_token_setup, dim3(n_chunks), dim3(256), 0, s,
+                     reinterpret_cast<const int4 *>(meta), n_chunks, tok_delta, tok_chunk);
+  return hipGetLastError();
+}
+
+}  // namespace akvs

@@ -1,0 +1,85 @@
+// Host-side launchers of the akvs kernels. All launch on the given stream, return the
+// HIP status of the launch and assume the caller validated every size and pointer.
+#pragma once
+#include "common.h"
+
+namespace akvs {
+
+// ---- k_misc.hip ---------------------------------------------------------------------
+// table row i holds position p0 + i.
+hipError_t launch_rope_table(int p0, int n_pos, int head_dim, double theta, float *table,
+                             hipStream_t s);
+// h[t][:] = embed[tok[t]][:] (fp32), t < n; ids outside [0, vocab) give a zero row.
+hipError_t launch_embed(const int32_t *tok, int n, const void *embed, int dtype, int vocab, int D,
+                        float *h, hipStream_t s);
+// out[i] = RMSNorm(h[src(i)]) * gain, i < rows (and < *rows_dev if given).
+// src(i) = i + (base_dev ? *base_dev - rows : 0)  (base_dev selects the last `rows` rows).
+hipError_t launch_rmsnorm(const float *h, int ldh, int rows, const int32_t *rows_dev,
+                          const int32_t *base_dev, const void *gain, int gain_dtype, int D,
+                          float eps, void *out, int out_dtype, int ldo, hipStream_t s);
+// dst[i] = src[idx[i]], i < *n_dev (rows of D floats); indices outside [0, n_src) give 0.
+hipError_t launch_gather_rows(const float *src, int n_src, const int32_t *idx, int cap,
+                              const int32_t *n_dev, int D, float *dst, hipStream_t s);
+// per unit token t < T_c: tok_delta[t] = s_i, tok_chunk[t] = i.
+hipError_t launch_token_setup(const int32_t *meta, int n_chunks, int32_t *tok_delta,
+                              int32_t *tok_chunk, hipStream_t s);
+
+// ---- k_reuse.hip --------------------------------------------------------------------
+hipError_t launch_divergence(const void *k_fresh, const void *v_fresh, int fresh_dtype,
+                             CacheLayer cache, int n_tokens, int hkv, int hd,
+                             const int32_t *tok_delta, const float *rope, int rope_rows,
+                             float *d_k, float *d_v, hipStream_t s);
+hipError_t launch_select(const float *d_k, const float *d_v, const int32_t *meta, int n_chunks,
+                         int t_ctx, int q, uint32_t flags, int32_t *probe_k, int32_t *probe_v,
+                         float *w_k, float *w_v, uint8_t *tok_flags, int32_t *chunk_rows,
+                         int32_t *rows, int32_t *n_rows, int32_t *fresh_row, hipStream_t s);
+hipError_t launch_chunk_offset(const void *k_fresh, const void *v_fresh, int fresh_dtype,
+                               const int32_t *fresh_row, CacheLayer cache, const int32_t *meta,
+                               int n_chunks, const int32_t *probe_k, const int32_t *probe_v,
+                               uint32_t flags, int hkv, int hd, const float *rope, int rope_rows,
+                               float *mu_k, float *mu_v, hipStream_t s);
+// Corrected (or, with mu == nullptr and tok_flags == nullptr, just re-rotated) cache rows.
+// A token's unit and offset come from tok_chunk / tok_delta when given, else from a
+// binary search of meta (n_chunks entries).
+hipError_t launch_correction(CacheLayer cache, const float *mu_k, const float *mu_v,
+                             const float *w_k, const float *w_v, const uint8_t *tok_flags,
+                             const void *k_fresh, const void *v_fresh, const int32_t *fresh_row,
+                             const int32_t *tok_chunk, const int32_t *tok_delta,
+                             const int32_t *meta, int n_chunks, int t_ctx,
+                             int t_all, int hkv, int hd, uint32_t flags, const float *rope,
+                             int rope_rows, void *k_corr, void *v_corr, int out_dtype,
+                             hipStream_t s);
+hipError_t launch_quantize(const void *x, int x_dtype, int n_rows, int hd, int bits,
+                           uint8_t *codes, _Float16 *meta, hipStream_t s);
+
+// ---- k_gemm.hip ---------------------------------------------------------------------
+enum EpiMode { EPI_STORE = 0, EPI_QKV = 1, EPI_RESID = 2, EPI_SWIGLU = 3 };
+
+struct Epi {
+  int mode;
+  void *out;            // STORE: [M][ldo] (out_dtype); RESID: float h [M][ldo]; SWIGLU: act
+  int ldo;
+  int out_dtype;        // AKVS_F32 / AKVS_BF16 for STORE / SWIGLU / QKV outputs
+  // QKV: columns [0, hq_w) are q, [hq_w, hq_w+kv_w) k, the rest v; this GEMM's column 0
+  // is logical column n_off.
+  void *q_out, *k_out, *v_out;
+  int n_off, hq_w, kv_w, hd;
+  const int32_t *pos;   // row positions (nullptr: pos0 + row)
+  int pos0;
+  int kv_by_pos;        // k/v destination row = position (else = row)
+  const float *rope;
+  int rope_rows;
+  int rope_base;        // position of the rotary table's first row
+};
+
+// C[M][N] = A[M][K] . B[N][K]^T with epilogue. Rows >= *m_dev (if given) are skipped.
+// SWIGLU: N is the FFN width F; B has 2F rows (gate, then up).
+hipError_t launch_gemm(const void *A, int lda, const void *B, int ldb, int M, int N, int K,
+                       const int32_t *m_dev, int dtype, const Epi &epi, hipStream_t s);
+
+// ---- k_attn.hip ---------------------------------------------------------------------
+hipError_t launch_attention(const void *q, const int32_t *pos, int pos0, int rows,
+                            const int32_t *rows_dev, const void *k, const void *v, int n_keys,
+                            int hq, int hkv, int hd, int dtype, void *out, hipStream_t s);
+
+}  // namespace akvs

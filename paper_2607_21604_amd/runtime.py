@@ -1,0 +1,107 @@
+"""Device-memory plumbing around libakvs: allocate outputs and workspaces with torch,
+marshal the descriptors, call the C entry points on the current stream.
+
+Nothing here computes any part of the method; every step runs in the library.
+"""
+from __future__ import annotations
+
+from typing import Optional, Sequence
+
+import torch
+
+from . import akvs
+
+
+class Engine:
+    """A decoder (weights on one device) and the calls of the library over it."""
+
+    def __init__(self, shape, weights: dict, device="cuda"):
+        self.shape = shape
+        self.device = torch.device(device)
+        self.weights = weights
+        self.n_layers = len(weights["layers"])
+        self.m = akvs.model_cfg(shape, n_layers=self.n_layers)
+        self.layers = akvs.layer_array(weights)
+        self.dtype = torch.float32 if self.m.dtype == akvs.AKVS_F32 else torch.bfloat16
+        self._ws = None
+
+    def workspace(self, nbytes: int) -> torch.Tensor:
+        if self._ws is None or self._ws.numel() < nbytes:
+            self._ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=self.device)
+        return self._ws
+
+    def full_prefill(self, tokens: torch.Tensor, pos0: int = 0, want_h: bool = True):
+        n = int(tokens.numel())
+        sh = self.shape
+        L = self.n_layers
+        k = torch.empty((L, n, sh.n_kv_heads, sh.head_dim), dtype=self.dtype, device=self.device)
+        v = torch.empty_like(k)
+        h = torch.empty((n, sh.d_model), dtype=torch.float32, device=self.device) if want_h else None
+        ws = self.workspace(akvs.akvs_workspace_size(self.m, None, n))
+        akvs.akvs_full_prefill(tokens, n, pos0, self.weights["embed"], self.layers,
+                               self.weights["final_norm"], self.m, h, k, v, ws)
+        return h, k, v
+
+    def cache_units(self, tokens: torch.Tensor, chunk_lens: Sequence[int]):
+        """Standalone per-unit caches: each unit prefilled alone at position 0, laid out
+        [L][T_c][Hkv][hd] with the units back to back."""
+        sh = self.shape
+        tc = int(sum(chunk_lens))
+        kc = torch.empty((self.n_layers, tc, sh.n_kv_heads, sh.head_dim), dtype=self.dtype,
+                         device=self.device)
+        vc = torch.empty_like(kc)
+        s = 0
+        for n in chunk_lens:
+            _, k, v = self.full_prefill(tokens[s:s + n], 0, want_h=False)
+            kc[:, s:s + n].copy_(k)
+            vc[:, s:s + n].copy_(v)
+            s += n
+        return kc, vc
+
+    def reuse_prefill(self, tokens: torch.Tensor, chunk_lens: Sequence[int], query_len: int,
+                      k_cache: torch.Tensor, v_cache: torch.Tensor, refresh=(1, 5),
+                      check_layer: int = 1, flags: int = 0, k_meta=None, v_meta=None,
+                      cache_dtype: Optional[int] = None, given_probes=None, outputs=None):
+        """Run the reuse prefill. Returns a dict of device tensors (h_query, k_corr, v_corr,
+        probe_k, probe_v, d_k, d_v, rows, n_rows). `outputs` may pass a previous result
+        dict to reuse its buffers."""
+        sh = self.shape
+        cfg = akvs.reuse_cfg(chunk_lens, query_len, refresh, check_layer, flags)
+        _, (tc, sum_b, row_cap, t_all) = akvs.akvs_chunk_meta(cfg)
+        if outputs is None:
+            dev = self.device
+            outputs = {
+                "h_query": torch.empty((query_len, sh.d_model), dtype=torch.float32, device=dev),
+                "k_corr": torch.empty((self.n_layers, t_all, sh.n_kv_heads, sh.head_dim),
+                                      dtype=self.dtype, device=dev),
+                "probe_k": torch.empty(max(sum_b, 1), dtype=torch.int32, device=dev),
+                "probe_v": torch.empty(max(sum_b, 1), dtype=torch.int32, device=dev),
+                "d_k": torch.empty(tc, dtype=torch.float32, device=dev),
+                "d_v": torch.empty(tc, dtype=torch.float32, device=dev),
+                "rows": torch.empty(t_all, dtype=torch.int32, device=dev),
+                "n_rows": torch.empty(1, dtype=torch.int32, device=dev),
+            }
+            outputs["v_corr"] = torch.empty_like(outputs["k_corr"])
+        if given_probes is not None:
+            outputs["probe_k"][:sum_b].copy_(given_probes[0])
+            outputs["probe_v"][:sum_b].copy_(given_probes[1])
+        o = outputs
+        out = akvs.ReuseOut(*(akvs.ptr(o[k]) for k in ("h_query", "k_corr", "v_corr", "probe_k",
+                                                       "probe_v", "d_k", "d_v", "rows", "n_rows")))
+        cache = akvs.cache_struct(k_cache, v_cache, k_meta, v_meta,
+                                  cache_dtype if cache_dtype is not None else akvs.dtype_code(k_cache))
+        ws = self.workspace(akvs.akvs_workspace_size(self.m, cfg))
+        akvs.akvs_reuse_prefill(tokens, self.weights["embed"], self.layers,
+                                self.weights["final_norm"], self.m, cfg, cache, out, ws)
+        outputs["_sum_b"] = sum_b
+        return outputs
+
+
+def quantize_cache(x: torch.Tensor, bits: int):
+    """Group-64 quantised copy of a cache [..][hd] (codes uint8, meta fp16 (scale, zero))."""
+    hd = x.shape[-1]
+    rows = x.numel() // hd
+    codes = torch.empty(x.shape[:-1] + (hd * bits // 8,), dtype=torch.uint8, device=x.device)
+    meta = torch.empty(x.shape[:-1] + (hd // 64, 2), dtype=torch.float16, device=x.device)
+    akvs.akvs_quantize_cache(x.contiguous(), rows, hd, bits, codes, meta)
+    return codes, meta

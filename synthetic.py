@@ -122,7 +122,7 @@ def _normal(shape_, std: float, seed: int, dtype, device) -> torch.Tensor:
 
 
 def make_weights(shape: ModelShape, seed: int = 0, device="cpu", n_layers: Optional[int] = None,
-                 std: float = 0.02) -> dict:
+                 std: float = 0.02, embed: bool = True) -> dict:
     """Random-init decoder weights in the library's layout.
 
     Per layer: attn_norm [D], w_qkv [(Hq+2Hkv)*hd][D] (q rows, then k, then v),
@@ -150,7 +150,7 @@ def make_weights(shape: ModelShape, seed: int = 0, device="cpu", n_layers: Optio
             "w_down": _normal((D, F), std, s + 4, dt, device),
         })
     return {
-        "embed": _normal((shape.vocab, D), std, base + 11, dt, device),
+        "embed": _normal((shape.vocab, D), std, base + 11, dt, device) if embed else None,
         "final_norm": torch.ones(D, dtype=dt, device=device),
         "layers": layers,
     }

@@ -1,0 +1,147 @@
+"""The C ABI without a GPU: exported symbols, host-only helpers, argument validation."""
+import ctypes
+import json
+import os
+import subprocess
+
+import pytest
+
+import oracle
+from paper_2607_21604_amd import akvs
+from tests.libutil import ensure_built, declared_functions
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return ensure_built()
+
+
+def test_every_declared_function_is_exported(lib):
+    names = declared_functions()
+    assert len(names) >= 20
+    out = subprocess.run(["nm", "-D", "--defined-only", akvs.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = {line.split()[-1] for line in out.splitlines() if line.strip()}
+    missing = [n for n in names if n not in exported]
+    assert not missing, missing
+    # and the binding wraps exactly the declared set
+    assert sorted(akvs.EXPORTED) == names
+
+
+def test_chunk_meta_matches_budget_table(lib):
+    cases = json.load(open(os.path.join(GOLDEN, "probe_budgets.json")))["cases"]
+    for c in cases:
+        if c["num"] > c["den"]:
+            continue
+        cfg = akvs.reuse_cfg([c["n"], 3], 2, (c["num"], c["den"]), 1, 0)
+        meta, tot = akvs.akvs_chunk_meta(cfg)
+        assert int(meta[0, 2]) == c["b"]
+        assert int(meta[1, 2]) == oracle.probe_budget(3, c["num"], c["den"])
+        assert tot[0] == c["n"] + 3 and tot[3] == c["n"] + 5
+
+
+def test_chunk_meta_offsets_and_row_cap(lib):
+    lens = [5, 1, 17, 64]
+    cfg = akvs.reuse_cfg(lens, 9, (3, 10), 1, 0)
+    meta, (tc, sum_b, cap, t_all) = akvs.akvs_chunk_meta(cfg)
+    b = [oracle.probe_budget(n, 3, 10) for n in lens]
+    starts = oracle.chunk_starts(lens)
+    assert [int(x) for x in meta[:, 0]] == list(starts)
+    assert [int(x) for x in meta[:, 2]] == b
+    assert [int(x) for x in meta[:, 3]] == [0, b[0], b[0] + b[1], b[0] + b[1] + b[2]]
+    assert (tc, sum_b, t_all) == (87, sum(b), 96)
+    assert cap == sum(min(n, 2 * bb) for n, bb in zip(lens, b)) + 9
+
+
+@pytest.mark.parametrize("bad", [
+    dict(n_chunks=0), dict(query_len=0), dict(refresh=(6, 5)), dict(refresh=(1, 0)),
+    dict(flags=1 << 7), dict(lens=[4, 0, 3]), dict(flags=akvs.AKVS_F_NO_PREFIX_RECOMPUTE),
+])
+def test_invalid_reuse_configs_are_rejected(lib, bad):
+    lens = bad.get("lens", [4, 5, 3])
+    cfg = akvs.reuse_cfg(lens, bad.get("query_len", 2), bad.get("refresh", (1, 5)), 1,
+                         bad.get("flags", 0))
+    if "n_chunks" in bad:
+        cfg.n_chunks = 0
+    with pytest.raises(akvs.AkvsError) as e:
+        akvs.akvs_chunk_meta(cfg)
+    assert e.value.status == akvs.AKVS_EINVAL
+
+
+class _Shape:
+    def __init__(self, **kw):
+        d = dict(n_layers=2, d_model=256, n_q_heads=4, n_kv_heads=4, head_dim=64, ffn_dim=688,
+                 vocab=1024, rope_theta=1e4, rms_eps=1e-6, dtype="f32")
+        d.update(kw)
+        self.__dict__.update(d)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(head_dim=96), akvs.AKVS_EUNSUPPORTED),
+    (dict(n_q_heads=6, n_kv_heads=4), akvs.AKVS_ESHAPE),
+    (dict(n_layers=0), akvs.AKVS_EINVAL),
+    (dict(dtype="bf16", ffn_dim=688), akvs.AKVS_EUNSUPPORTED),
+])
+def test_invalid_models_are_rejected_before_any_launch(lib, kw, status):
+    m = akvs.model_cfg(_Shape(**kw))
+    assert akvs.akvs_workspace_size(m, None, 16) == 0
+    cfg = akvs.reuse_cfg([4, 4], 2, (1, 5), 1, 0)
+    layers = (akvs.LayerW * max(m.n_layers, 1))()
+    cache = akvs.Cache(16, 16, None, None, akvs.AKVS_F32)
+    out = akvs.ReuseOut(16, 16, 16, None, None, None, None, None, None)
+    st = lib.akvs_reuse_prefill(16, 16, layers, 16, ctypes.byref(m), ctypes.byref(cfg),
+                                ctypes.byref(cache), ctypes.byref(out), 16, 1 << 20, None)
+    assert st == status, lib.akvs_last_error()
+
+
+def _valid_args():
+    m = akvs.model_cfg(_Shape())
+    cfg = akvs.reuse_cfg([4, 4], 2, (1, 5), 1, 0)
+    layers = (akvs.LayerW * 2)(*[akvs.LayerW(*([4096] * 6)) for _ in range(2)])
+    cache = akvs.Cache(4096, 4096, None, None, akvs.AKVS_F32)
+    out = akvs.ReuseOut(4096, 4096, 4096, None, None, None, None, None, None)
+    return m, cfg, layers, cache, out
+
+
+def test_workspace_too_small_and_misalignment(lib):
+    m, cfg, layers, cache, out = _valid_args()
+    need = akvs.akvs_workspace_size(m, cfg)
+    assert need > 0
+    st = lib.akvs_reuse_prefill(4096, 4096, layers, 4096, ctypes.byref(m), ctypes.byref(cfg),
+                                ctypes.byref(cache), ctypes.byref(out), 4096, need - 1, None)
+    assert st == akvs.AKVS_ENOSPACE
+    assert b"workspace" in lib.akvs_last_error()
+    cache.k = 4100  # not 16-byte aligned
+    st = lib.akvs_reuse_prefill(4096, 4096, layers, 4096, ctypes.byref(m), ctypes.byref(cfg),
+                                ctypes.byref(cache), ctypes.byref(out), 4096, need, None)
+    assert st == akvs.AKVS_EINVAL
+
+
+def test_cache_dtype_must_match_model(lib):
+    m, cfg, layers, cache, out = _valid_args()
+    cache.dtype = akvs.AKVS_U4G64
+    st = lib.akvs_reuse_prefill(4096, 4096, layers, 4096, ctypes.byref(m), ctypes.byref(cfg),
+                                ctypes.byref(cache), ctypes.byref(out), 4096, 1 << 30, None)
+    assert st == akvs.AKVS_EDTYPE
+
+
+def test_given_probes_need_probe_buffers(lib):
+    m, cfg, layers, cache, out = _valid_args()
+    cfg.flags = akvs.AKVS_F_GIVEN_PROBES
+    st = lib.akvs_reuse_prefill(4096, 4096, layers, 4096, ctypes.byref(m), ctypes.byref(cfg),
+                                ctypes.byref(cache), ctypes.byref(out), 4096, 1 << 30, None)
+    assert st == akvs.AKVS_EINVAL
+
+
+def test_status_strings(lib):
+    for s in range(7):
+        assert lib.akvs_status_string(s)
+    assert lib.akvs_status_string(99) == b"unknown status"
+
+
+def test_missing_library_fails_loudly(tmp_path, monkeypatch):
+    monkeypatch.setattr(akvs, "_lib", None)
+    with pytest.raises(ImportError):
+        akvs.load(str(tmp_path / "nope.so"))

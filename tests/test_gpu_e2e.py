@@ -1,0 +1,198 @@
+"""Whole-procedure parity: the library's full prefill and reuse prefill against the oracle."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synthetic
+from paper_2607_21604_amd import akvs
+from paper_2607_21604_amd.runtime import Engine
+from tests.gpu_util import (DEV, to_dev, dev_weights, f64, max_rel, oracle_caches,
+                            check_valid_top_b)
+from tests.libutil import ensure_built
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def lib():
+    return ensure_built()
+
+
+class Case:
+    """A model, a context of units + query, oracle-made unit caches and a GPU engine."""
+
+    def __init__(self, name, n_layers=None, n_units=None, seed=0):
+        wl = synthetic.workload(name, seed)
+        self.shape = wl.shape if n_layers is None else wl.shape.with_layers(n_layers)
+        self.lens = list(wl.chunk_lens[:n_units] if n_units else wl.chunk_lens)
+        self.q = wl.query_len
+        self.refresh = wl.refresh[0]
+        self.tdt = synthetic.torch_dtype(self.shape)
+        self.w = synthetic.make_weights(self.shape, seed)
+        self.toks = synthetic.make_tokens(sum(self.lens) + self.q, self.shape.vocab, seed)
+        self.dims = oracle.dims_from(self.shape)
+        self.layers = [oracle.split_layer(lw, self.dims) for lw in self.w["layers"]]
+        self.kc, self.vc, self.k_all, self.v_all = oracle_caches(
+            self.toks, self.lens, self.w, self.dims, self.tdt, self.layers)
+        self.eng = Engine(self.shape, dev_weights(self.w))
+        self.tok_dev = to_dev(self.toks)
+        self.starts = oracle.chunk_starts(self.lens)
+        self.tol = 1e-4 if self.shape.dtype == "f32" else 2e-2
+
+    def oracle(self, refresh=None, check_layer=1, flags=0, probes=None, kc=None, vc=None):
+        return oracle.reuse_prefill(self.toks, self.w, self.dims, self.lens, self.q,
+                                    kc if kc is not None else self.kc,
+                                    vc if vc is not None else self.vc,
+                                    refresh or self.refresh, check_layer, flags, probes,
+                                    self.layers)
+
+    def gpu(self, refresh=None, check_layer=1, flags=0, probes=None, **kw):
+        given = None
+        if probes is not None:
+            given = (to_dev(np.concatenate(probes[0]).astype(np.int32)),
+                     to_dev(np.concatenate(probes[1]).astype(np.int32)))
+            flags |= akvs.AKVS_F_GIVEN_PROBES
+        k = kw.pop("k_cache", self.k_all)
+        v = kw.pop("v_cache", self.v_all)
+        out = self.eng.reuse_prefill(self.tok_dev, self.lens, self.q, k, v, refresh or self.refresh,
+                                     check_layer, flags, given_probes=given, **kw)
+        torch.cuda.synchronize()
+        return out
+
+    def split(self, flat, budgets):
+        off = np.concatenate([[0], np.cumsum(budgets)])
+        return [flat[off[i]:off[i + 1]] for i in range(len(budgets))]
+
+    def compare(self, out, ref, tol=None):
+        tol = tol or self.tol
+        errs = {"h_query": max_rel(f64(out["h_query"]), ref["h_query"]),
+                "k_corr": max_rel(f64(out["k_corr"]), ref["k_corr"]),
+                "v_corr": max_rel(f64(out["v_corr"]), ref["v_corr"])}
+        assert all(e <= tol for e in errs.values()), errs
+        n = int(out["n_rows"][0])
+        np.testing.assert_array_equal(out["rows"][:n].cpu().numpy(), ref["rows"])
+        return errs
+
+
+@pytest.fixture(scope="module")
+def tiny():
+    return Case("tiny")
+
+
+def test_tiny_full_prefill(tiny):
+    h, k, v = tiny.eng.full_prefill(tiny.tok_dev)
+    rh, rk, rv = oracle.full_prefill(tiny.toks, 0, tiny.w, tiny.dims, tiny.layers)
+    assert max_rel(f64(h), rh) < 1e-4 and max_rel(f64(k), rk) < 1e-4 and max_rel(f64(v), rv) < 1e-4
+
+
+def test_tiny_unit_caching_matches_oracle(tiny):
+    k, v = tiny.eng.cache_units(tiny.tok_dev, tiny.lens)
+    assert max_rel(f64(k), f64(tiny.k_all)) < 1e-5 and max_rel(f64(v), f64(tiny.v_all)) < 1e-5
+
+
+@pytest.mark.parametrize("check_layer", [1, 0])
+def test_tiny_reuse_prefill(tiny, check_layer):
+    ref = tiny.oracle(check_layer=check_layer)
+    own = tiny.gpu(check_layer=check_layer)
+    budgets = ref["budgets"]
+    d_k, d_v = f64(own["d_k"]), f64(own["d_v"])
+    # divergences agree; the GPU's own probe sets are valid top-b sets
+    scale = max(np.abs(ref["d_k"]).max(), 1e-30)
+    assert np.abs(d_k - ref["d_k"]).max() <= 1e-4 * scale + 1e-6
+    assert np.abs(d_v - ref["d_v"]).max() <= 1e-4 * max(np.abs(ref["d_v"]).max(), 1e-30) + 1e-6
+    pk = tiny.split(own["probe_k"].cpu().numpy(), budgets)
+    pv = tiny.split(own["probe_v"].cpu().numpy(), budgets)
+    slack = 2 * np.abs(d_k - ref["d_k"]).max() + 1e-6
+    check_valid_top_b(ref["d_k"], d_k, pk, tiny.starts, tiny.lens, budgets, slack)
+    slack = 2 * np.abs(d_v - ref["d_v"]).max() + 1e-6
+    check_valid_top_b(ref["d_v"], d_v, pv, tiny.starts, tiny.lens, budgets, slack)
+    # with the oracle's probe sets, every float output agrees
+    given = tiny.gpu(check_layer=check_layer, probes=(ref["probe_k"], ref["probe_v"]))
+    tiny.compare(given, ref)
+
+
+@pytest.mark.parametrize("flags", [akvs.AKVS_F_NO_CORRECTION, akvs.AKVS_F_UNIT_WEIGHTS,
+                                   akvs.AKVS_F_FRESH_IF_RECOMPUTED])
+def test_tiny_reuse_flags(tiny, flags):
+    ref = tiny.oracle(flags=flags)
+    tiny.compare(tiny.gpu(flags=flags, probes=(ref["probe_k"], ref["probe_v"])), ref)
+
+
+def test_tiny_full_refresh_equals_full_prefill(tiny):
+    out = tiny.gpu(refresh=(1, 1))
+    rh, rk, rv = oracle.full_prefill(tiny.toks, 0, tiny.w, tiny.dims, tiny.layers)
+    assert int(out["n_rows"][0]) == tiny.toks.size
+    assert max_rel(f64(out["h_query"]), rh[-tiny.q:]) < 1e-4
+    assert max_rel(f64(out["k_corr"]), rk) < 1e-4 and max_rel(f64(out["v_corr"]), rv) < 1e-4
+
+
+def test_tiny_stale_reuse(tiny):
+    flags = akvs.AKVS_F_NO_PREFIX_RECOMPUTE
+    ref = tiny.oracle(refresh=(0, 1), flags=flags)
+    out = tiny.gpu(refresh=(0, 1), flags=flags)
+    tiny.compare(out, ref)
+    tc = sum(tiny.lens)
+    # values are reused bit for bit
+    assert torch.equal(out["v_corr"][:, :tc].cpu(), tiny.v_all.cpu())
+
+
+def test_tiny_is_deterministic(tiny):
+    a = tiny.gpu()
+    b = tiny.gpu()
+    for k in ("h_query", "k_corr", "v_corr", "d_k", "probe_k", "rows"):
+        assert torch.equal(a[k], b[k]), k
+
+
+@pytest.fixture(scope="module")
+def w3b():
+    return Case("3b", n_layers=3, n_units=6)
+
+
+def test_3b_width_reuse_prefill(w3b):
+    ref = w3b.oracle()
+    own = w3b.gpu()
+    budgets = ref["budgets"]
+    d_k = f64(own["d_k"])
+    assert np.abs(d_k - ref["d_k"]).max() <= 2e-2 * np.abs(ref["d_k"]).max()
+    pk = w3b.split(own["probe_k"].cpu().numpy(), budgets)
+    check_valid_top_b(ref["d_k"], d_k, pk, w3b.starts, w3b.lens, budgets,
+                      2 * np.abs(d_k - ref["d_k"]).max())
+    errs = w3b.compare(w3b.gpu(probes=(ref["probe_k"], ref["probe_v"])), ref)
+    print("3b-width errors", errs)
+
+
+def test_3b_width_full_refresh_equals_full_prefill(w3b):
+    out = w3b.gpu(refresh=(1, 1))
+    h, k, v = w3b.eng.full_prefill(w3b.tok_dev)
+    assert max_rel(f64(out["h_query"]), f64(h)[-w3b.q:]) < 2e-2
+    assert max_rel(f64(out["k_corr"]), f64(k)) < 2e-2
+
+
+@pytest.fixture(scope="module")
+def w7b():
+    return Case("7b", n_layers=3, n_units=8)
+
+
+def test_7b_width_reuse_prefill(w7b):
+    ref = w7b.oracle()
+    errs = w7b.compare(w7b.gpu(probes=(ref["probe_k"], ref["probe_v"])), ref)
+    print("7b-width errors", errs)
+
+
+@pytest.mark.parametrize("bits", [4, 2])
+def test_7b_width_quantised_cache(w7b, bits):
+    codes_k, meta_k = oracle.quantize_g64(f64(w7b.k_all), bits)
+    codes_v, meta_v = oracle.quantize_g64(f64(w7b.v_all), bits)
+    deq_k = oracle.dequantize_g64(codes_k, meta_k)
+    deq_v = oracle.dequantize_g64(codes_v, meta_v)
+    kc = [deq_k[:, s:s + n] for s, n in zip(w7b.starts, w7b.lens)]
+    vc = [deq_v[:, s:s + n] for s, n in zip(w7b.starts, w7b.lens)]
+    ref = w7b.oracle(kc=kc, vc=vc)
+    out = w7b.gpu(probes=(ref["probe_k"], ref["probe_v"]),
+                  k_cache=to_dev(oracle.pack_codes(codes_k, bits)),
+                  v_cache=to_dev(oracle.pack_codes(codes_v, bits)),
+                  k_meta=to_dev(meta_k), v_meta=to_dev(meta_v),
+                  cache_dtype=akvs.AKVS_U4G64 if bits == 4 else akvs.AKVS_U2G64)
+    errs = w7b.compare(out, ref)
+    print(f"7b-width {bits}-bit errors", errs)
