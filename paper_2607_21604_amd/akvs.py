@@ -178,9 +178,12 @@ def reuse_cfg(chunk_lens: Sequence[int], query_len: int, refresh=(1, 5), check_l
 
 
 def cache_struct(k, v, k_meta=None, v_meta=None, dtype: Optional[int] = None) -> Cache:
+    """A Cache descriptor; it holds references to its tensors so that they outlive it."""
     if dtype is None:
         dtype = dtype_code(k)
-    return Cache(ptr(k), ptr(v), ptr(k_meta), ptr(v_meta), dtype)
+    c = Cache(ptr(k), ptr(v), ptr(k_meta), ptr(v_meta), dtype)
+    c._keep = (k, v, k_meta, v_meta)
+    return c
 
 
 # ---- wrappers with the C names -------------------------------------------------------------

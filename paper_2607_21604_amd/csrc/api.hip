@@ -119,6 +119,8 @@ akvs_status check_model(const akvs_model_cfg *m) {
   if (m->dtype == AKVS_BF16) {
     REQUIRE(m->d_model % 64 == 0 && m->ffn_dim % 64 == 0, AKVS_EUNSUPPORTED,
             "bf16 models need d_model and ffn_dim multiples of 64");
+    REQUIRE(m->n_q_heads / m->n_kv_heads <= 12, AKVS_EUNSUPPORTED,
+            "bf16 attention supports up to 12 query heads per KV head");
   } else {
     REQUIRE(m->ffn_dim % 4 == 0, AKVS_ESHAPE, "ffn_dim must be a multiple of 4");
   }
@@ -236,14 +238,31 @@ struct Carver {
 // Buffers of a decoder pass over `rows` rows (the full layer and the probe layers).
 struct LayerBufs {
   void *x, *q, *att, *act;  // model dtype
+  float *part_o, *part_ml;  // attention key-split partials (bf16 models)
 };
 
-void carve_layer_bufs(Carver &cv, const akvs_model_cfg *m, long long rows, LayerBufs &b) {
+// rows: the largest row count a layer pass uses; attn_rows[0..1]: the row counts its
+// attention calls use over n_keys keys (for the key-split partials of bf16 models).
+void carve_layer_bufs(Carver &cv, const akvs_model_cfg *m, long long rows, long long attn_rows0,
+                      long long attn_rows1, long long n_keys, LayerBufs &b) {
   const size_t es = es_of(m->dtype);
   b.x = cv.take<char>((size_t)rows * m->d_model * es);
   b.q = cv.take<char>((size_t)rows * m->n_q_heads * m->head_dim * es);
   b.att = cv.take<char>((size_t)rows * m->n_q_heads * m->head_dim * es);
   b.act = cv.take<char>((size_t)rows * m->ffn_dim * es);
+  b.part_o = nullptr;
+  b.part_ml = nullptr;
+  if (m->dtype == AKVS_BF16) {
+    long long worst = 0;
+    for (long long r : {attn_rows0, attn_rows1}) {
+      const long long sp = attn_splits((int)r, m->n_q_heads, m->n_kv_heads, (int)n_keys);
+      if (sp > 1 && sp * r > worst) worst = sp * r;
+    }
+    if (worst > 0) {
+      b.part_o = cv.take<float>((size_t)worst * m->n_q_heads * m->head_dim);
+      b.part_ml = cv.take<float>((size_t)worst * m->n_q_heads * 2);
+    }
+  }
 }
 
 struct ReuseBufs {
@@ -271,7 +290,7 @@ size_t carve_reuse(void *ws, const akvs_model_cfg *m, const akvs_reuse_cfg *c, c
   b.tok_delta = cv.take<int32_t>((size_t)Tc);
   b.tok_chunk = cv.take<int32_t>((size_t)Tc);
   b.h_full = cv.take<float>((size_t)T * m->d_model);
-  carve_layer_bufs(cv, m, T, b.lb);
+  carve_layer_bufs(cv, m, T, T, cap, T, b.lb);
   b.k_chk = cv.take<char>((size_t)Tc * kvw * es);
   b.v_chk = cv.take<char>((size_t)Tc * kvw * es);
   b.d_k = cv.take<float>((size_t)Tc);
@@ -302,7 +321,7 @@ size_t carve_full(void *ws, const akvs_model_cfg *m, long long n, FullBufs &b) {
   Carver cv(ws);
   b.rope = cv.take<float>((size_t)n * m->head_dim);
   b.h = cv.take<float>((size_t)n * m->d_model);
-  carve_layer_bufs(cv, m, n, b.lb);
+  carve_layer_bufs(cv, m, n, n, n, n, b.lb);
   return cv.off;
 }
 
@@ -395,7 +414,7 @@ akvs_status full_layer(const akvs_model_cfg *m, const akvs_layer_w &w, float *h,
                                   stream));
   LAUNCH(AKVS_K_ATTENTION, launch_attention(lb.q, nullptr, 0, n, nullptr, k_dst, v_dst, n,
                                             m->n_q_heads, m->n_kv_heads, m->head_dim, m->dtype,
-                                            lb.att, stream));
+                                            lb.att, lb.part_o, lb.part_ml, stream));
   return out_mlp(m, w, h, n, nullptr, lb.att, lb.x, lb.act, stream);
 }
 
@@ -642,7 +661,7 @@ akvs_status akvs_sparse_query_attention(const void *q, const int32_t *positions,
           "misaligned argument");
   LAUNCH(AKVS_K_ATTENTION, launch_attention(q, positions, 0, n_rows, nullptr, k, v, n_keys,
                                             m->n_q_heads, m->n_kv_heads, m->head_dim, m->dtype,
-                                            out, stream));
+                                            out, nullptr, nullptr, stream));
   return AKVS_OK;
 }
 
@@ -806,7 +825,8 @@ akvs_status akvs_reuse_prefill(const int32_t *tokens, const void *embed, const a
                              b.fresh_row, b.tok_chunk, b.tok_delta, b.meta, nch, Tc, T, hkv, hd,
                              cfg->flags, b.rope, T, kl, vl, m->dtype, stream));
     LAUNCH(AKVS_K_ATTENTION, launch_attention(b.lb.q, b.rows, 0, cap, b.n_rows, kl, vl, T,
-                                              m->n_q_heads, hkv, hd, m->dtype, b.lb.att, stream));
+                                              m->n_q_heads, hkv, hd, m->dtype, b.lb.att,
+                                              b.lb.part_o, b.lb.part_ml, stream));
     st = out_mlp(m, lw[l], b.h_probe, cap, b.n_rows, b.lb.att, b.lb.x, b.lb.act, stream);
     if (st) return st;
   }

@@ -9,6 +9,7 @@ typedef uint16_t bf16_t;  // bf16 bits as stored in memory
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
 typedef __attribute__((ext_vector_type(4))) float f32x4_t;
 typedef __attribute__((ext_vector_type(16))) float f32x16_t;
+typedef __attribute__((ext_vector_type(4))) unsigned int u32x4_t;  // 16-byte load/store unit
 
 namespace akvs {
 

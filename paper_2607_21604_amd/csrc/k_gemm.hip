@@ -111,119 +111,152 @@ __device__ void epilogue_tile(const float *Cs, int ldc, int m0, int n0, int M_ef
 }
 
 // ------------------------------------------------------------------------------------------
-// bf16 MFMA GEMM
-constexpr int GB_M = 128, GB_N = 128, GB_K = 64;
-constexpr int G_LDS = GB_K + 8;               // bf16 per LDS row (144 B: staggers banks)
-constexpr int G_TILE = 128 * G_LDS;           // one operand tile
-constexpr int G_SMEM = 2 * 2 * G_TILE * 2;    // 2 buffers x (A, B) x bytes = 73728
-constexpr int G_CLD = GB_N + 4;               // fp32 C tile row stride (67584 B total)
+// bf16 MFMA GEMM. Block tile BM x 128 x 64 (BM = 128 or 64), 256 threads as 2 x 2 waves, a
+// wave owning (BM/2) x 64 outputs as (BM/64) x 2 tiles of v_mfma_f32_32x32x16_bf16.
+// Operand tiles: two LDS buffers (rows padded to 144 B: the 16 rows one ds_read_b128 phase
+// touches fall on distinct banks) and two register stages, so the global loads of tile
+// kt+2 are in flight while tile kt is multiplied and tile kt+1 is written to LDS.
+constexpr int GB_N = 128, GB_K = 64;
+constexpr int G_LDS = GB_K + 8;  // bf16 per LDS row
+constexpr int G_CLD = GB_N + 4;  // fp32 C tile row stride
 
+template <int BM>
+struct GemmShape {
+  static constexpr int A_CH = BM * GB_K / 8 / 256;     // 16-byte A chunks per thread
+  static constexpr int B_CH = GB_N * GB_K / 8 / 256;   // 16-byte B chunks per thread
+  static constexpr int A_TILE = BM * G_LDS;            // bf16 elements
+  static constexpr int B_TILE = GB_N * G_LDS;
+  static constexpr int BUF = A_TILE + B_TILE;
+  static constexpr int LOOP_BYTES = 2 * BUF * 2;
+  static constexpr int C_BYTES = BM * G_CLD * 4;
+  static constexpr int SMEM = LOOP_BYTES > C_BYTES ? LOOP_BYTES : C_BYTES;
+  static constexpr int MI = BM / 64;                   // 32-row MFMA tiles per wave
+};
+
+template <int BM>
 __global__ __launch_bounds__(256, 2) void k_gemm_bf16(const bf16_t *__restrict__ A, int lda,
                                                       const bf16_t *__restrict__ B, int ldb,
                                                       int M, int N, int K,
                                                       const int32_t *m_dev, Epi epi) {
-  __shared__ __attribute__((aligned(16))) unsigned char smem[G_SMEM];
+  using S = GemmShape<BM>;
+  __shared__ __attribute__((aligned(16))) unsigned char smem[S::SMEM];
   bf16_t *sm = reinterpret_cast<bf16_t *>(smem);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   int M_eff = M;
   if (m_dev) M_eff = min(M, *m_dev);
-  const int m0 = blockIdx.y * GB_M;
+  const int m0 = blockIdx.y * BM;
   if (m0 >= M_eff) return;
   const bool swiglu = epi.mode == EPI_SWIGLU;
   const int n0 = blockIdx.x * (swiglu ? GB_N / 2 : GB_N);
 
-  const bf16_t *a_src[4];
-  const bf16_t *b_src[4];
-  bool a_ok[4], b_ok[4];
+  // Per-thread 16-byte chunks: chunk c = tid + 256 i covers row c / 8, k columns
+  // (c % 8) * 8 ..+7. Rows past M / N are clamped to a valid row: they only feed
+  // accumulator rows / columns the epilogue discards.
+  size_t a_off[S::A_CH], b_off[S::B_CH];
+  int la_off[S::A_CH], lb_off[S::B_CH];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+  for (int i = 0; i < S::A_CH; ++i) {
     const int c = tid + 256 * i;
     const int r = c >> 3, kc = (c & 7) * 8;
-    const int gm = m0 + r;
-    a_ok[i] = gm < M_eff;
-    a_src[i] = A + (size_t)(a_ok[i] ? gm : 0) * lda + kc;
+    a_off[i] = (size_t)min(m0 + r, M_eff - 1) * lda + kc;
+    la_off[i] = r * G_LDS + kc;
+  }
+#pragma unroll
+  for (int i = 0; i < S::B_CH; ++i) {
+    const int c = tid + 256 * i;
+    const int r = c >> 3, kc = (c & 7) * 8;
     int gn;
     if (swiglu) {
-      const int oc = n0 + (r & 63);
-      b_ok[i] = oc < N;
+      const int oc = min(n0 + (r & 63), N - 1);
       gn = (r < 64) ? oc : N + oc;
     } else {
-      gn = n0 + r;
-      b_ok[i] = gn < N;
+      gn = min(n0 + r, N - 1);
     }
-    b_src[i] = B + (size_t)(b_ok[i] ? gn : 0) * ldb + kc;
+    b_off[i] = (size_t)gn * ldb + kc;
+    lb_off[i] = S::A_TILE + r * G_LDS + kc;
   }
-  uint4 ra[4], rb[4];
-  const uint4 z4 = make_uint4(0, 0, 0, 0);
-  auto gload = [&](int k0) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      ra[i] = a_ok[i] ? *reinterpret_cast<const uint4 *>(a_src[i] + k0) : z4;
-      rb[i] = b_ok[i] ? *reinterpret_cast<const uint4 *>(b_src[i] + k0) : z4;
-    }
-  };
-  auto sstore = [&](int buf) {
-    bf16_t *As = sm + buf * 2 * G_TILE;
-    bf16_t *Bs = As + G_TILE;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int c = tid + 256 * i;
-      const int r = c >> 3, kc = (c & 7) * 8;
-      *reinterpret_cast<uint4 *>(As + r * G_LDS + kc) = ra[i];
-      *reinterpret_cast<uint4 *>(Bs + r * G_LDS + kc) = rb[i];
-    }
-  };
 
-  f32x16_t acc[2][2];
+  f32x16_t acc[S::MI][2];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < S::MI; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
+  u32x4_t ra0[S::A_CH], rb0[S::B_CH], ra1[S::A_CH], rb1[S::B_CH];
   const int nk = K / GB_K;
-  gload(0);
-  sstore(0);
+
+#define AKVS_GLOAD(RA, RB, KT)                                                      \
+  {                                                                                 \
+    const int k0_ = (KT) * GB_K;                                                    \
+    _Pragma("unroll") for (int i = 0; i < S::A_CH; ++i)                             \
+        RA[i] = *reinterpret_cast<const u32x4_t *>(A + a_off[i] + k0_);             \
+    _Pragma("unroll") for (int i = 0; i < S::B_CH; ++i)                             \
+        RB[i] = *reinterpret_cast<const u32x4_t *>(B + b_off[i] + k0_);             \
+  }
+#define AKVS_SSTORE(RA, RB, BUFI)                                                   \
+  {                                                                                 \
+    bf16_t *base_ = sm + (BUFI) * S::BUF;                                           \
+    _Pragma("unroll") for (int i = 0; i < S::A_CH; ++i)                             \
+        *reinterpret_cast<u32x4_t *>(base_ + la_off[i]) = RA[i];                    \
+    _Pragma("unroll") for (int i = 0; i < S::B_CH; ++i)                             \
+        *reinterpret_cast<u32x4_t *>(base_ + lb_off[i]) = RB[i];                    \
+  }
+#define AKVS_COMPUTE(BUFI)                                                                    \
+  {                                                                                           \
+    const bf16_t *As_ = sm + (BUFI) * S::BUF;                                                 \
+    const bf16_t *Bs_ = As_ + S::A_TILE;                                                      \
+    _Pragma("unroll") for (int ks = 0; ks < GB_K / 16; ++ks) {                                \
+      bf16x8_t af[S::MI], bfr[2];                                                             \
+      const int kk = ks * 16 + (lane >> 5) * 8;                                               \
+      _Pragma("unroll") for (int i = 0; i < S::MI; ++i) af[i] =                               \
+          *reinterpret_cast<const bf16x8_t *>(As_ + (wm * (BM / 2) + i * 32 + (lane & 31)) *  \
+                                                        G_LDS + kk);                          \
+      _Pragma("unroll") for (int j = 0; j < 2; ++j) bfr[j] =                                  \
+          *reinterpret_cast<const bf16x8_t *>(Bs_ + (wn * 64 + j * 32 + (lane & 31)) * G_LDS + \
+                                              kk);                                            \
+      _Pragma("unroll") for (int i = 0; i < S::MI; ++i)                                       \
+          _Pragma("unroll") for (int j = 0; j < 2; ++j) acc[i][j] =                           \
+              __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);     \
+    }                                                                                         \
+  }
+
+  AKVS_GLOAD(ra0, rb0, 0);
+  if (nk > 1) AKVS_GLOAD(ra1, rb1, 1);
+  AKVS_SSTORE(ra0, rb0, 0);
   __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    if (kt + 1 < nk) gload((kt + 1) * GB_K);
-    const bf16_t *As = sm + (kt & 1) * 2 * G_TILE;
-    const bf16_t *Bs = As + G_TILE;
-#pragma unroll
-    for (int ks = 0; ks < GB_K / 16; ++ks) {
-      bf16x8_t af[2], bfr[2];
-      const int kk = ks * 16 + (lane >> 5) * 8;
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-        af[i] = *reinterpret_cast<const bf16x8_t *>(As + (wm * 64 + i * 32 + (lane & 31)) * G_LDS + kk);
-#pragma unroll
-      for (int j = 0; j < 2; ++j)
-        bfr[j] = *reinterpret_cast<const bf16x8_t *>(Bs + (wn * 64 + j * 32 + (lane & 31)) * G_LDS + kk);
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
-    }
-    if (kt + 1 < nk) sstore((kt + 1) & 1);
+  for (int kt = 0; kt < nk; kt += 2) {
+    // tile kt sits in LDS buffer 0, tile kt+1 is arriving in ra1/rb1
+    if (kt + 2 < nk) AKVS_GLOAD(ra0, rb0, kt + 2);
+    AKVS_COMPUTE(0);
+    if (kt + 1 < nk) AKVS_SSTORE(ra1, rb1, 1);
+    __syncthreads();
+    if (kt + 1 >= nk) break;
+    // tile kt+1 sits in LDS buffer 1, tile kt+2 is arriving in ra0/rb0
+    if (kt + 3 < nk) AKVS_GLOAD(ra1, rb1, kt + 3);
+    AKVS_COMPUTE(1);
+    if (kt + 2 < nk) AKVS_SSTORE(ra0, rb0, 0);
     __syncthreads();
   }
+#undef AKVS_GLOAD
+#undef AKVS_SSTORE
+#undef AKVS_COMPUTE
 
   float *Cs = reinterpret_cast<float *>(smem);
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < S::MI; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int row = wm * 64 + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+        const int row = wm * (BM / 2) + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
         const int col = wn * 64 + j * 32 + (lane & 31);
         Cs[row * G_CLD + col] = acc[i][j][r];
       }
   __syncthreads();
-  epilogue_tile<GB_M, GB_N, 256>(Cs, G_CLD, m0, n0, M_eff, N, epi);
+  epilogue_tile<BM, GB_N, 256>(Cs, G_CLD, m0, n0, M_eff, N, epi);
 }
 
 // ------------------------------------------------------------------------------------------
@@ -309,9 +342,17 @@ hipError_t launch_gemm(const void *A, int lda, const void *B, int ldb, int M, in
   const bool swiglu = epi.mode == EPI_SWIGLU;
   if (dtype == AKVS_BF16) {
     const int bn = swiglu ? GB_N / 2 : GB_N;
-    dim3 g((N + bn - 1) / bn, (M + GB_M - 1) / GB_M), b(256);
-    hipLaunchKernelGGL(k_gemm_bf16, g, b, 0, s, reinterpret_cast<const bf16_t *>(A), lda,
-                       reinterpret_cast<const bf16_t *>(B), ldb, M, N, K, m_dev, epi);
+    const int n_tiles = (N + bn - 1) / bn;
+    const bf16_t *a = reinterpret_cast<const bf16_t *>(A);
+    const bf16_t *b16 = reinterpret_cast<const bf16_t *>(B);
+    // 128-row tiles unless that leaves most CUs (256 of them, 2 blocks each) idle
+    if ((long long)n_tiles * ((M + 127) / 128) >= 384) {
+      dim3 g(n_tiles, (M + 127) / 128), b(256);
+      hipLaunchKernelGGL(k_gemm_bf16<128>, g, b, 0, s, a, lda, b16, ldb, M, N, K, m_dev, epi);
+    } else {
+      dim3 g(n_tiles, (M + 63) / 64), b(256);
+      hipLaunchKernelGGL(k_gemm_bf16<64>, g, b, 0, s, a, lda, b16, ldb, M, N, K, m_dev, epi);
+    }
   } else {
     const int bn = swiglu ? GF_N / 2 : GF_N;
     dim3 g((N + bn - 1) / bn, (M + GF_M - 1) / GF_M), b(256);

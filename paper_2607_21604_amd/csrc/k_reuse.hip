@@ -237,27 +237,39 @@ hipError_t launch_select(const float *d_k, const float *d_v, const int32_t *meta
 }
 
 // ---------------------------------------------------------------------------------------
-// Per-unit offsets. grid = (m, 2 sides, pair blocks); a thread owns one lo/hi pair of one
-// head and sums its probes sequentially (ascending position order, fp32).
+// Per-unit offsets. grid = (m, 2 sides, pair blocks of 64); block = 4 waves. The unit's
+// probe positions and their rows in the fresh buffers are first staged in LDS, so the
+// data loads that follow are independent. Lane = one lo/hi pair of one head; wave w sums
+// the probes k = w, w+4, ... in ascending order, and the four partial sums are added in
+// wave order: a fixed fp32 summation order.
+constexpr int OFF_MAXB = 1024;  // probes staged per pass
+
 template <typename TF>
-__global__ void k_chunk_offset(const TF *k_fresh, const TF *v_fresh, const int32_t *fresh_row,
-                               CacheLayer cache, const int4 *meta, const int32_t *probe_k,
-                               const int32_t *probe_v, uint32_t flags, int hkv, int hd,
-                               const float2 *rope, int rope_rows, float *mu_k, float *mu_v) {
+__global__ __launch_bounds__(256) void k_chunk_offset(const TF *k_fresh, const TF *v_fresh,
+                                                      const int32_t *fresh_row, CacheLayer cache,
+                                                      const int4 *meta, const int32_t *probe_k,
+                                                      const int32_t *probe_v, uint32_t flags,
+                                                      int hkv, int hd, const float2 *rope,
+                                                      int rope_rows, float *mu_k, float *mu_v) {
+  __shared__ int s_tok[OFF_MAXB], s_row[OFF_MAXB];
+  __shared__ float s_part[4][64][2];
   const int c = blockIdx.x;
   const int side = blockIdx.y;  // 0 = K, 1 = V
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int half = hd >> 1;
   const int pairs = hkv * half;
-  const int p = blockIdx.z * blockDim.x + threadIdx.x;
-  if (p >= pairs) return;
-  const int h = p / half, e = p - h * half;
+  const int p = blockIdx.z * 64 + lane;
+  const bool active = p < pairs;
+  const int h = active ? p / half : 0, e = active ? p - h * half : 0;
   const int kvw = hkv * hd;
   const int4 mc = meta[c];
   const int b = mc.z;
   float *mu = (side == 0 ? mu_k : mu_v) + (size_t)c * kvw + h * hd;
   if (b == 0 || (flags & AKVS_F_NO_CORRECTION)) {
-    mu[e] = 0.f;
-    mu[e + half] = 0.f;
+    if (active && wave == 0) {
+      mu[e] = 0.f;
+      mu[e + half] = 0.f;
+    }
     return;
   }
   const TF *fresh = side == 0 ? k_fresh : v_fresh;
@@ -267,26 +279,45 @@ __global__ void k_chunk_offset(const TF *k_fresh, const TF *v_fresh, const int32
   const int delta = (mc.x >= 0 && mc.x < rope_rows) ? mc.x : 0;
   const float2 cs = rope[(size_t)delta * half + e];
   float slo = 0.f, shi = 0.f;
-  for (int k = 0; k < b; ++k) {
-    const int j = probes[k];
-    if (j < mc.x || j >= mc.x + mc.y) continue;  // not a token of this unit
-    const int r = fresh_row[j];
-    if (r < 0) continue;
-    const size_t frow = (size_t)r * hkv + h;
-    const size_t crow = (size_t)j * hkv + h;
-    const float flo = load1(fresh + frow * hd + e), fhi = load1(fresh + frow * hd + e + half);
-    float clo = cache_load1(cb, cm, cache.dtype, crow, hd, e);
-    float chi = cache_load1(cb, cm, cache.dtype, crow, hd, e + half);
-    if (side == 0) {
-      const float a = clo, bb = chi;
-      clo = a * cs.x - bb * cs.y;
-      chi = bb * cs.x + a * cs.y;
+  for (int kb = 0; kb < b; kb += OFF_MAXB) {
+    const int nb = min(OFF_MAXB, b - kb);
+    __syncthreads();
+    for (int k = threadIdx.x; k < nb; k += blockDim.x) {
+      const int j = probes[kb + k];
+      const bool inside = j >= mc.x && j < mc.x + mc.y;  // a token of this unit
+      const int r = inside ? fresh_row[j] : -1;
+      s_tok[k] = inside ? j : -1;
+      s_row[k] = r;
     }
-    slo += flo - clo;
-    shi += fhi - chi;
+    __syncthreads();
+    if (active) {
+      for (int k = wave; k < nb; k += 4) {
+        const int j = s_tok[k], r = s_row[k];
+        if (j < 0 || r < 0) continue;
+        const size_t frow = (size_t)r * hkv + h;
+        const size_t crow = (size_t)j * hkv + h;
+        const float flo = load1(fresh + frow * hd + e), fhi = load1(fresh + frow * hd + e + half);
+        float clo = cache_load1(cb, cm, cache.dtype, crow, hd, e);
+        float chi = cache_load1(cb, cm, cache.dtype, crow, hd, e + half);
+        if (side == 0) {
+          const float a = clo, bb = chi;
+          clo = a * cs.x - bb * cs.y;
+          chi = bb * cs.x + a * cs.y;
+        }
+        slo += flo - clo;
+        shi += fhi - chi;
+      }
+    }
   }
-  mu[e] = slo / (float)b;
-  mu[e + half] = shi / (float)b;
+  s_part[wave][lane][0] = slo;
+  s_part[wave][lane][1] = shi;
+  __syncthreads();
+  if (wave == 0 && active) {
+    const float tlo = ((s_part[0][lane][0] + s_part[1][lane][0]) + s_part[2][lane][0]) + s_part[3][lane][0];
+    const float thi = ((s_part[0][lane][1] + s_part[1][lane][1]) + s_part[2][lane][1]) + s_part[3][lane][1];
+    mu[e] = tlo / (float)b;
+    mu[e + half] = thi / (float)b;
+  }
 }
 
 hipError_t launch_chunk_offset(const void *k_fresh, const void *v_fresh, int fresh_dtype,
@@ -295,7 +326,7 @@ hipError_t launch_chunk_offset(const void *k_fresh, const void *v_fresh, int fre
                                uint32_t flags, int hkv, int hd, const float *rope, int rope_rows,
                                float *mu_k, float *mu_v, hipStream_t s) {
   const int pairs = hkv * hd / 2;
-  dim3 g(n_chunks, 2, (pairs + 255) / 256), b(256);
+  dim3 g(n_chunks, 2, (pairs + 63) / 64), b(256);
   const int4 *m4 = reinterpret_cast<const int4 *>(meta);
   const float2 *r = reinterpret_cast<const float2 *>(rope);
   if (fresh_dtype == AKVS_BF16)

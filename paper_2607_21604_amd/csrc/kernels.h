@@ -78,8 +78,14 @@ hipError_t launch_gemm(const void *A, int lda, const void *B, int ldb, int M, in
                        const int32_t *m_dev, int dtype, const Epi &epi, hipStream_t s);
 
 // ---- k_attn.hip ---------------------------------------------------------------------
+// With part_o / part_ml (bf16 path), the key range is split for parallelism:
+// part_o [splits][rows][hq][hd] fp32, part_ml [splits][rows][hq][2] fp32, splits as below.
 hipError_t launch_attention(const void *q, const int32_t *pos, int pos0, int rows,
                             const int32_t *rows_dev, const void *k, const void *v, int n_keys,
-                            int hq, int hkv, int hd, int dtype, void *out, hipStream_t s);
+                            int hq, int hkv, int hd, int dtype, void *out, float *part_o,
+                            float *part_ml, hipStream_t s);
+// number of key splits launch_attention uses for `rows` rows over n_keys keys
+int attn_splits(int rows, int hq, int hkv, int n_keys);
+int attn_split_keys(int n_keys, int n_splits);
 
 }  // namespace akvs
