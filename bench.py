@@ -37,9 +37,83 @@ def parse():
     p.add_argument("--check-layer", type=int, default=1)
     p.add_argument("--seed", type=int, default=0)
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--cpu-sample-layers", default="prefix,probe",
-                   help="oracle layers timed for the CPU baseline")
+    p.add_argument("--no-full", action="store_true", help="skip the full-prefill baseline leg")
+    p.add_argument("--random-caches", action="store_true",
+                   help="unit caches drawn at random instead of prefilled (counter runs)")
+    p.add_argument("--calibrate-copy", action="store_true",
+                   help="run one 1 GiB device copy first (FETCH/WRITE counter calibration)")
+    p.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                   help="write the GEMM traffic summary from two rocprofv3 --pmc CSVs and exit")
     return p.parse_args()
+
+
+GEMM_KERNEL = "k_gemm_bf16"
+COPY_BYTES = 1 << 30
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_gemm_bf16_traffic_3b_reuse.txt")
+GEMM_SOURCE = os.path.join(ROOT, "paper_2607_21604_amd", "csrc", "k_gemm.hip")
+
+
+def source_hash(path=GEMM_SOURCE):
+    import hashlib
+    return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+
+
+def traffic_summary(fetch_csv, write_csv):
+    """HBM bytes per GEMM launch from rocprofv3 FETCH_SIZE / WRITE_SIZE per-dispatch CSVs,
+    each scaled by what the counter reads for the 1 GiB copy kernel of the same run."""
+    import csv
+
+    def per_kernel(path, counter):
+        gemm, copy = [], []
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] != counter:
+                continue
+            v = float(r["Counter_Value"])
+            if GEMM_KERNEL in r["Kernel_Name"]:
+                gemm.append(v)
+            elif "copy" in r["Kernel_Name"].lower() and int(r["Grid_Size"]) > 1 << 20:
+                copy.append(v)
+        return gemm, copy
+
+    fg, fc = per_kernel(fetch_csv, "FETCH_SIZE")
+    wg, wc = per_kernel(write_csv, "WRITE_SIZE")
+    f_scale = COPY_BYTES / max(fc)   # bytes per counter unit (KiB nominal)
+    w_scale = COPY_BYTES / max(wc)
+    fetch = sum(fg) / len(fg) * f_scale
+    write = sum(wg) / len(wg) * w_scale
+    lines = [
+        "# k_gemm_bf16 HBM traffic, 3B-class reuse prefill (r=1/5), bench.py counter runs",
+        "# commands (from the repository root, on the GPU box):",
+        "#   rocprofv3 --pmc FETCH_SIZE -f csv -d OUT/fetch -o run -- python3 bench.py --steps 2 "
+        "--warmup 1 --no-cpu-baseline --no-full --random-caches --calibrate-copy",
+        "#   rocprofv3 --pmc WRITE_SIZE -f csv -d OUT/write -o run -- python3 bench.py --steps 2 "
+        "--warmup 1 --no-cpu-baseline --no-full --random-caches --calibrate-copy",
+        "#   python3 bench.py --traffic-summary OUT/fetch/run_counter_collection.csv "
+        "OUT/write/run_counter_collection.csv",
+        f"source_sha256_16: {source_hash()}",
+        f"gemm_launches: {len(fg)}",
+        f"copy_fetch_counter: {max(fc):.1f}  (for {COPY_BYTES} bytes read)",
+        f"copy_write_counter: {max(wc):.1f}  (for {COPY_BYTES} bytes written)",
+        f"fetch_bytes_per_launch: {fetch:.0f}",
+        f"write_bytes_per_launch: {write:.0f}",
+        f"traffic_bytes_per_launch: {fetch + write:.0f}",
+    ]
+    os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
+    open(TRAFFIC_FILE, "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def measured_traffic():
+    """HBM bytes per GEMM launch from the committed counter summary, or None when the
+    summary is missing or was taken on a different GEMM source."""
+    try:
+        kv = dict(l.split(": ", 1) for l in open(TRAFFIC_FILE).read().splitlines()
+                  if ": " in l and not l.startswith("#"))
+        if kv.get("source_sha256_16") != source_hash():
+            return None
+        return float(kv["traffic_bytes_per_launch"])
+    except (OSError, KeyError, ValueError):
+        return None
 
 
 def gemm_flops(shape, rows_full, t_ctx, m_rows, c):
@@ -119,6 +193,9 @@ def cpu_baseline(wl, refresh, c, seed, m_rows):
 
 def main():
     args = parse()
+    if args.traffic_summary:
+        traffic_summary(*args.traffic_summary)
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
                           "n_gpus": args.gpus}))
@@ -141,11 +218,24 @@ def main():
     print(f"# workload {wl.name}: T={wl.n_tokens} ({len(wl.chunk_lens)} units, q={wl.query_len}), "
           f"L={shape.n_layers}, r={num}/{den}", file=sys.stderr, flush=True)
 
+    if args.calibrate_copy:
+        src = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     w = synthetic.make_weights(shape, seed=args.seed, device=dev)
     eng = Engine(shape, w, dev)
     toks = torch.tensor(synthetic.make_tokens(wl.n_tokens, shape.vocab, args.seed),
                         dtype=torch.int32, device=dev)
-    k_cache, v_cache = eng.cache_units(toks, wl.chunk_lens)
+    if args.random_caches:
+        g = torch.Generator(device=dev)
+        g.manual_seed(args.seed + 3)
+        k_cache = torch.randn((shape.n_layers, wl.n_ctx, shape.n_kv_heads, shape.head_dim),
+                              generator=g, device=dev).to(torch.bfloat16)
+        v_cache = torch.randn(k_cache.shape, generator=g, device=dev).to(torch.bfloat16)
+    else:
+        k_cache, v_cache = eng.cache_units(toks, wl.chunk_lens)
     torch.cuda.synchronize()
     print("# unit caches built", file=sys.stderr, flush=True)
 
@@ -178,17 +268,19 @@ def main():
           file=sys.stderr, flush=True)
 
     # full-prefill baseline on the same tokens (same kernels)
-    eng.full_prefill(toks, want_h=True)
-    for _ in range(args.warmup):
+    ms_full = None
+    if not args.no_full:
         eng.full_prefill(toks, want_h=True)
-    torch.cuda.synchronize()
-    t0.record(stream)
-    for _ in range(args.steps):
-        eng.full_prefill(toks, want_h=True)
-    t1.record(stream)
-    torch.cuda.synchronize()
-    ms_full = t0.elapsed_time(t1) / args.steps
-    print(f"# full prefill: {ms_full:.3f} ms/step", file=sys.stderr, flush=True)
+        for _ in range(args.warmup):
+            eng.full_prefill(toks, want_h=True)
+        torch.cuda.synchronize()
+        t0.record(stream)
+        for _ in range(args.steps):
+            eng.full_prefill(toks, want_h=True)
+        t1.record(stream)
+        torch.cuda.synchronize()
+        ms_full = t0.elapsed_time(t1) / args.steps
+        print(f"# full prefill: {ms_full:.3f} ms/step", file=sys.stderr, flush=True)
 
     flops_step = gemm_flops(shape, wl.n_tokens, wl.n_ctx, m_rows, args.check_layer)
     achieved = flops_step * args.steps / (g_ms * 1e-3) / 1e12 if g_ms > 0 else None
@@ -196,7 +288,8 @@ def main():
     roofline = {"bound": "mfma", "kernel": "k_gemm_bf16",
                 "achieved": achieved, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                 "frac": achieved / MFMA_BF16_PEAK_TFLOPS if achieved else None,
-                "traffic": None, "launches": g_launches,
+                "traffic": measured_traffic(), "traffic_unit": "HBM bytes per launch",
+                "launches": g_launches,
                 "avg_launch_us": 1e3 * g_ms / max(g_launches, 1),
                 "algorithmic_flops_per_launch": per_launch,
                 "gemm_share_of_step": g_ms / args.steps / ms_step}
@@ -219,9 +312,9 @@ def main():
                    "tokens": T, "context_tokens": wl.n_ctx, "query_tokens": wl.query_len,
                    "refresh": f"{num}/{den}", "check_layer": args.check_layer,
                    "recomputed_rows": m_rows, "recomputed_fraction": m_rows / T},
-        "speedup_vs_full_prefill": ms_full / ms_step,
-        "full_prefill_tokens_per_s": T / (ms_full * 1e-3), "ms_full_prefill": ms_full,
-        "full_prefill_gemm_tflops_upper": full_gemm_flops(shape, T) / (ms_full * 1e-3) / 1e12,
+        "speedup_vs_full_prefill": ms_full / ms_step if ms_full else None,
+        "full_prefill_tokens_per_s": T / (ms_full * 1e-3) if ms_full else None,
+        "ms_full_prefill": ms_full,
         "roofline": roofline,
         "cpu_baseline": cpu,
     }

@@ -4,6 +4,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <algorithm>
 #include <mutex>
 #include <vector>
 
@@ -239,12 +240,27 @@ struct Carver {
 struct LayerBufs {
   void *x, *q, *att, *act;  // model dtype
   float *part_o, *part_ml;  // attention key-split partials (bf16 models)
+  float *gpart;             // GEMM K-split partials (bf16 models)
 };
+
+// GEMM partial-tile workspace (floats) of the four projections of one layer over `rows`.
+size_t layer_gemm_part(const akvs_model_cfg *m, long long rows) {
+  if (m->dtype != AKVS_BF16) return 0;
+  const int D = m->d_model, F = m->ffn_dim, hqw = m->n_q_heads * m->head_dim;
+  const int qkvw = hqw + 2 * m->n_kv_heads * m->head_dim;
+  const int r = (int)rows;
+  size_t w = gemm_part_floats(r, qkvw, D, EPI_QKV);
+  w = std::max(w, gemm_part_floats(r, D, hqw, EPI_RESID));
+  w = std::max(w, gemm_part_floats(r, F, D, EPI_SWIGLU));
+  w = std::max(w, gemm_part_floats(r, D, F, EPI_RESID));
+  return w;
+}
 
 // rows: the largest row count a layer pass uses; attn_rows[0..1]: the row counts its
 // attention calls use over n_keys keys (for the key-split partials of bf16 models).
 void carve_layer_bufs(Carver &cv, const akvs_model_cfg *m, long long rows, long long attn_rows0,
-                      long long attn_rows1, long long n_keys, LayerBufs &b) {
+                      long long attn_rows1, long long attn_rows2, long long n_keys,
+                      LayerBufs &b) {
   const size_t es = es_of(m->dtype);
   b.x = cv.take<char>((size_t)rows * m->d_model * es);
   b.q = cv.take<char>((size_t)rows * m->n_q_heads * m->head_dim * es);
@@ -252,9 +268,15 @@ void carve_layer_bufs(Carver &cv, const akvs_model_cfg *m, long long rows, long 
   b.act = cv.take<char>((size_t)rows * m->ffn_dim * es);
   b.part_o = nullptr;
   b.part_ml = nullptr;
+  b.gpart = nullptr;
+  {
+    const size_t g = std::max(std::max(layer_gemm_part(m, attn_rows0), layer_gemm_part(m, attn_rows1)),
+                              layer_gemm_part(m, attn_rows2));
+    if (g) b.gpart = cv.take<float>(g);
+  }
   if (m->dtype == AKVS_BF16) {
     long long worst = 0;
-    for (long long r : {attn_rows0, attn_rows1}) {
+    for (long long r : {attn_rows0, attn_rows1, attn_rows2}) {
       const long long sp = attn_splits((int)r, m->n_q_heads, m->n_kv_heads, (int)n_keys);
       if (sp > 1 && sp * r > worst) worst = sp * r;
     }
@@ -277,6 +299,8 @@ struct ReuseBufs {
   float *h_probe;
   void *k_fresh, *v_fresh;
   float *mu_k, *mu_v;
+  float *h_last;  // the query rows' residual stream at the last layer
+  void *q_last;   // and their queries
 };
 
 size_t carve_reuse(void *ws, const akvs_model_cfg *m, const akvs_reuse_cfg *c, const Meta &mt,
@@ -290,7 +314,7 @@ size_t carve_reuse(void *ws, const akvs_model_cfg *m, const akvs_reuse_cfg *c, c
   b.tok_delta = cv.take<int32_t>((size_t)Tc);
   b.tok_chunk = cv.take<int32_t>((size_t)Tc);
   b.h_full = cv.take<float>((size_t)T * m->d_model);
-  carve_layer_bufs(cv, m, T, T, cap, T, b.lb);
+  carve_layer_bufs(cv, m, T, T, cap, c->query_len, T, b.lb);
   b.k_chk = cv.take<char>((size_t)Tc * kvw * es);
   b.v_chk = cv.take<char>((size_t)Tc * kvw * es);
   b.d_k = cv.take<float>((size_t)Tc);
@@ -309,6 +333,8 @@ size_t carve_reuse(void *ws, const akvs_model_cfg *m, const akvs_reuse_cfg *c, c
   b.v_fresh = cv.take<char>((size_t)cap * kvw * es);
   b.mu_k = cv.take<float>((size_t)c->n_chunks * kvw);
   b.mu_v = cv.take<float>((size_t)c->n_chunks * kvw);
+  b.h_last = cv.take<float>((size_t)c->query_len * m->d_model);
+  b.q_last = cv.take<char>((size_t)c->query_len * m->n_q_heads * m->head_dim * es);
   return cv.off;
 }
 
@@ -321,15 +347,18 @@ size_t carve_full(void *ws, const akvs_model_cfg *m, long long n, FullBufs &b) {
   Carver cv(ws);
   b.rope = cv.take<float>((size_t)n * m->head_dim);
   b.h = cv.take<float>((size_t)n * m->d_model);
-  carve_layer_bufs(cv, m, n, n, n, n, b.lb);
+  carve_layer_bufs(cv, m, n, n, n, n, n, b.lb);
   return cv.off;
 }
 
-size_t carve_step(void *ws, const akvs_model_cfg *m, long long n, void **x, void **act) {
+size_t carve_step(void *ws, const akvs_model_cfg *m, long long n, void **x, void **act,
+                  float **gpart) {
   Carver cv(ws);
   const size_t es = es_of(m->dtype);
   *x = cv.take<char>((size_t)n * m->d_model * es);
   *act = cv.take<char>((size_t)n * m->ffn_dim * es);
+  const size_t g = layer_gemm_part(m, n);
+  *gpart = g ? cv.take<float>(g) : nullptr;
   return cv.off;
 }
 
@@ -386,17 +415,17 @@ Epi simple_epi(int mode, void *out, int ldo, int dtype) {
 
 // Attention output projection + MLP over rows (h updated in place).
 akvs_status out_mlp(const akvs_model_cfg *m, const akvs_layer_w &w, float *h, int rows,
-                    const int32_t *rows_dev, const void *att, void *x, void *act,
+                    const int32_t *rows_dev, const void *att, void *x, void *act, float *gpart,
                     hipStream_t stream) {
   const int D = m->d_model, F = m->ffn_dim, hqw = m->n_q_heads * m->head_dim;
   LAUNCH(AKVS_K_GEMM, launch_gemm(att, hqw, w.w_o, hqw, rows, D, hqw, rows_dev, m->dtype,
-                                  simple_epi(EPI_RESID, h, D, AKVS_F32), stream));
+                                  simple_epi(EPI_RESID, h, D, AKVS_F32), stream, gpart));
   LAUNCH(AKVS_K_NORM, launch_rmsnorm(h, D, rows, rows_dev, nullptr, w.mlp_norm, m->dtype, D,
                                      m->rms_eps, x, m->dtype, D, stream));
   LAUNCH(AKVS_K_GEMM, launch_gemm(x, D, w.w_gate_up, D, rows, F, D, rows_dev, m->dtype,
-                                  simple_epi(EPI_SWIGLU, act, F, m->dtype), stream));
+                                  simple_epi(EPI_SWIGLU, act, F, m->dtype), stream, gpart));
   LAUNCH(AKVS_K_GEMM, launch_gemm(act, F, w.w_down, F, rows, D, F, rows_dev, m->dtype,
-                                  simple_epi(EPI_RESID, h, D, AKVS_F32), stream));
+                                  simple_epi(EPI_RESID, h, D, AKVS_F32), stream, gpart));
   return AKVS_OK;
 }
 
@@ -411,11 +440,11 @@ akvs_status full_layer(const akvs_model_cfg *m, const akvs_layer_w &w, float *h,
                                      m->rms_eps, lb.x, m->dtype, D, stream));
   LAUNCH(AKVS_K_GEMM, launch_gemm(lb.x, D, w.w_qkv, D, n, qkvw, D, nullptr, m->dtype,
                                   qkv_epi(m, lb.q, k_dst, v_dst, nullptr, pos0, 0, rope, n, pos0),
-                                  stream));
+                                  stream, lb.gpart));
   LAUNCH(AKVS_K_ATTENTION, launch_attention(lb.q, nullptr, 0, n, nullptr, k_dst, v_dst, n,
                                             m->n_q_heads, m->n_kv_heads, m->head_dim, m->dtype,
                                             lb.att, lb.part_o, lb.part_ml, stream));
-  return out_mlp(m, w, h, n, nullptr, lb.att, lb.x, lb.act, stream);
+  return out_mlp(m, w, h, n, nullptr, lb.att, lb.x, lb.act, lb.gpart, stream);
 }
 
 }  // namespace
@@ -470,7 +499,8 @@ size_t akvs_workspace_size(const akvs_model_cfg *m, const akvs_reuse_cfg *cfg, i
 size_t akvs_step_workspace_size(const akvs_model_cfg *m, int32_t n_rows) {
   if (check_model(m) != AKVS_OK || n_rows < 0) return 0;
   void *x, *a;
-  return carve_step(nullptr, m, n_rows, &x, &a);
+  float *g;
+  return carve_step(nullptr, m, n_rows, &x, &a, &g);
 }
 
 akvs_status akvs_profile_enable(int32_t class_mask) {
@@ -585,16 +615,18 @@ akvs_status akvs_probe_qkv(const float *h, int32_t n_rows, const int32_t *positi
           AKVS_EINVAL, "misaligned argument");
   REQUIRE(rope_rows >= 1, AKVS_EINVAL, "rope_rows must be >= 1");
   void *x, *act;
-  const size_t need = carve_step(nullptr, m, n_rows, &x, &act);
+  float *gpart;
+  const size_t need = carve_step(nullptr, m, n_rows, &x, &act, &gpart);
   REQUIRE(ws && ws_bytes >= need, AKVS_ENOSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
-  carve_step(ws, m, n_rows, &x, &act);
+  carve_step(ws, m, n_rows, &x, &act, &gpart);
   const int D = m->d_model;
   const int qkvw = (m->n_q_heads + 2 * m->n_kv_heads) * m->head_dim;
   LAUNCH(AKVS_K_NORM, launch_rmsnorm(h, D, n_rows, nullptr, nullptr, lw->attn_norm, m->dtype, D,
                                      m->rms_eps, x, m->dtype, D, stream));
   LAUNCH(AKVS_K_GEMM,
          launch_gemm(x, D, lw->w_qkv, D, n_rows, qkvw, D, nullptr, m->dtype,
-                     qkv_epi(m, q, k_fresh, v_fresh, positions, 0, 0, rope, rope_rows, 0), stream));
+                     qkv_epi(m, q, k_fresh, v_fresh, positions, 0, 0, rope, rope_rows, 0), stream,
+                     gpart));
   return AKVS_OK;
 }
 
@@ -679,10 +711,11 @@ akvs_status akvs_probe_out_mlp(float *h, int32_t n_rows, const void *attn_out,
   REQUIRE(h && attn_out && aligned16(h) && aligned16(attn_out) && aligned16(ws), AKVS_EINVAL,
           "NULL or misaligned argument");
   void *x, *act;
-  const size_t need = carve_step(nullptr, m, n_rows, &x, &act);
+  float *gpart;
+  const size_t need = carve_step(nullptr, m, n_rows, &x, &act, &gpart);
   REQUIRE(ws && ws_bytes >= need, AKVS_ENOSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
-  carve_step(ws, m, n_rows, &x, &act);
-  return out_mlp(m, *lw, h, n_rows, nullptr, attn_out, x, act, stream);
+  carve_step(ws, m, n_rows, &x, &act, &gpart);
+  return out_mlp(m, *lw, h, n_rows, nullptr, attn_out, x, act, gpart, stream);
 }
 
 akvs_status akvs_quantize_cache(const void *x, int32_t x_dtype, int32_t n_rows, int32_t head_dim,
@@ -814,7 +847,7 @@ akvs_status akvs_reuse_prefill(const int32_t *tokens, const void *embed, const a
     LAUNCH(AKVS_K_GEMM,
            launch_gemm(b.lb.x, D, lw[l].w_qkv, D, cap, qkvw, D, b.n_rows, m->dtype,
                        qkv_epi(m, b.lb.q, b.k_fresh, b.v_fresh, b.rows, 0, 0, b.rope, T, 0),
-                       stream));
+                       stream, b.lb.gpart));
     LAUNCH(AKVS_K_OFFSET, launch_chunk_offset(b.k_fresh, b.v_fresh, m->dtype, b.fresh_row, cl,
                                               b.meta, nch, b.probe_k, b.probe_v, cfg->flags, hkv,
                                               hd, b.rope, T, b.mu_k, b.mu_v, stream));
@@ -824,13 +857,29 @@ akvs_status akvs_reuse_prefill(const int32_t *tokens, const void *embed, const a
            launch_correction(cl, b.mu_k, b.mu_v, b.w_k, b.w_v, b.flags, b.k_fresh, b.v_fresh,
                              b.fresh_row, b.tok_chunk, b.tok_delta, b.meta, nch, Tc, T, hkv, hd,
                              cfg->flags, b.rope, T, kl, vl, m->dtype, stream));
-    LAUNCH(AKVS_K_ATTENTION, launch_attention(b.lb.q, b.rows, 0, cap, b.n_rows, kl, vl, T,
+    if (l + 1 < L) {
+      LAUNCH(AKVS_K_ATTENTION, launch_attention(b.lb.q, b.rows, 0, cap, b.n_rows, kl, vl, T,
+                                                m->n_q_heads, hkv, hd, m->dtype, b.lb.att,
+                                                b.lb.part_o, b.lb.part_ml, stream));
+      st = out_mlp(m, lw[l], b.h_probe, cap, b.n_rows, b.lb.att, b.lb.x, b.lb.act, b.lb.gpart,
+                   stream);
+      if (st) return st;
+      continue;
+    }
+    // last layer: only the query rows' attention and MLP reach the returned outputs (the
+    // recomputed unit rows only had to supply this layer's fresh keys and values)
+    const int q = cfg->query_len;
+    LAUNCH(AKVS_K_OTHER, launch_copy_tail_rows(b.lb.q, (size_t)hqw * es, q, b.n_rows, b.q_last,
+                                               stream));
+    LAUNCH(AKVS_K_OTHER, launch_copy_tail_rows(b.h_probe, (size_t)D * 4, q, b.n_rows, b.h_last,
+                                               stream));
+    LAUNCH(AKVS_K_ATTENTION, launch_attention(b.q_last, nullptr, Tc, q, nullptr, kl, vl, T,
                                               m->n_q_heads, hkv, hd, m->dtype, b.lb.att,
                                               b.lb.part_o, b.lb.part_ml, stream));
-    st = out_mlp(m, lw[l], b.h_probe, cap, b.n_rows, b.lb.att, b.lb.x, b.lb.act, stream);
+    st = out_mlp(m, lw[l], b.h_last, q, nullptr, b.lb.att, b.lb.x, b.lb.act, b.lb.gpart, stream);
     if (st) return st;
   }
-  LAUNCH(AKVS_K_NORM, launch_rmsnorm(b.h_probe, D, cfg->query_len, nullptr, b.n_rows, final_norm,
+  LAUNCH(AKVS_K_NORM, launch_rmsnorm(b.h_last, D, cfg->query_len, nullptr, nullptr, final_norm,
                                      m->dtype, D, m->rms_eps, out->h_query, AKVS_F32, D, stream));
   return AKVS_OK;
 }

@@ -18,6 +18,11 @@ namespace akvs {
 // stage each 64-key K / V tile in LDS for all of them (double buffered, next tile
 // prefetched into registers during the current one). Block b serves KV head b % Hkv, so
 // the blocks streaming one head's keys run on the same XCD and share its L2.
+// Column (bf16 element) of key group g (4 keys) in row r of the V^T tile (rows of 64
+// elements, no padding). The XOR swizzle makes every 16-lane pass of both the transposed
+// 8-byte writes and the 8-byte fragment reads touch 32 distinct 4-byte banks.
+__device__ __forceinline__ int vt_col(int r, int g) { return (g ^ ((r ^ (r >> 3)) & 15)) * 4; }
+
 template <int HD>
 __global__ __launch_bounds__(768) void k_attn_bf16(const bf16_t *__restrict__ Q,
                                                    const int32_t *pos, int pos0, int rows,
@@ -32,7 +37,7 @@ __global__ __launch_bounds__(768) void k_attn_bf16(const bf16_t *__restrict__ Q,
   constexpr int KS = HD / 32;          // contraction steps of S
   constexpr int HB = HD / 16;          // 16-wide head-dim blocks of O
   constexpr int KST = HD + 8;          // K tile row stride (bf16)
-  constexpr int VST = 64 + 4;          // V^T tile row stride (bf16)
+  constexpr int VST = 64;              // V^T tile row stride (bf16), swizzled by vt_col
   constexpr int CPK = HD / 8;          // 16-byte chunks per key row
   constexpr int KCH = 64 * CPK / 256;  // K chunks per loading thread
   constexpr int VKEYS = CPK / 4;       // keys per loading thread in the V transpose
@@ -122,10 +127,11 @@ __global__ __launch_bounds__(768) void k_attn_bf16(const bf16_t *__restrict__ Q,
         uint2 v2;                                                                           \
         v2.x = hi_ ? ((a0 >> 16) | (a1 & 0xffff0000u)) : ((a0 & 0xffffu) | (a1 << 16));    \
         v2.y = hi_ ? ((a2 >> 16) | (a3 & 0xffff0000u)) : ((a2 & 0xffffu) | (a3 << 16));    \
-        *reinterpret_cast<uint2 *>(vt_ + (ve0 + d) * VST + vkg * 4) = v2;                  \
+        *reinterpret_cast<uint2 *>(vt_ + (ve0 + d) * VST + vt_col(ve0 + d, vkg)) = v2;     \
       } else {                                                                              \
         const uint32_t a0 = vreg[0][word], a1 = vreg[VKEYS > 1 ? 1 : 0][word];              \
-        *reinterpret_cast<uint32_t *>(vt_ + (ve0 + d) * VST + vkg * 2) =                    \
+        *reinterpret_cast<uint32_t *>(vt_ + (ve0 + d) * VST + vt_col(ve0 + d, vkg >> 1) +     \
+                                      (vkg & 1) * 2) =                                      \
             hi_ ? ((a0 >> 16) | (a1 & 0xffff0000u)) : ((a0 & 0xffffu) | (a1 << 16));        \
       }                                                                                     \
     }                                                                                       \
@@ -197,10 +203,12 @@ __global__ __launch_bounds__(768) void k_attn_bf16(const bf16_t *__restrict__ Q,
         __builtin_memcpy(&pb, pw, 16);
 #pragma unroll
         for (int hb = 0; hb < HB; ++hb) {
-          const bf16_t *vrow = vt_ + (hb * 16 + (lane & 15)) * VST + st * 32 + (lane >> 4) * 4;
+          const int vr = hb * 16 + (lane & 15);
+          const bf16_t *vrow = vt_ + vr * VST;
+          const int kg = st * 8 + (lane >> 4);
           uint32_t vw[4];
-          const uint2 x0 = *reinterpret_cast<const uint2 *>(vrow);
-          const uint2 x1 = *reinterpret_cast<const uint2 *>(vrow + 16);
+          const uint2 x0 = *reinterpret_cast<const uint2 *>(vrow + vt_col(vr, kg));
+          const uint2 x1 = *reinterpret_cast<const uint2 *>(vrow + vt_col(vr, kg + 4));
           vw[0] = x0.x; vw[1] = x0.y; vw[2] = x1.x; vw[3] = x1.y;
           bf16x8_t a;
           __builtin_memcpy(&a, vw, 16);

@@ -7,6 +7,8 @@
 // next tile prefetched into registers during the MFMA loop. The accumulator tile is
 // staged through LDS so every epilogue can pair columns (rotary halves, gate/up) and
 // write coalesced rows. fp32 path (small models): 32x128x32 VALU tiles, same epilogues.
+#include <type_traits>
+
 #include "kernels.h"
 
 namespace akvs {
@@ -117,10 +119,35 @@ __device__ void epilogue_tile(const float *Cs, int ldc, int m0, int n0, int M_ef
 // touches fall on distinct banks) and two register stages, so the global loads of tile
 // kt+2 are in flight while tile kt is multiplied and tile kt+1 is written to LDS.
 constexpr int GB_N = 128, GB_K = 64;
+
+template <bool MF16>
+__device__ __forceinline__ typename std::conditional<MF16, f32x4_t, f32x16_t>::type mfma_tile(
+    bf16x8_t a, bf16x8_t b, typename std::conditional<MF16, f32x4_t, f32x16_t>::type c);
+template <>
+__device__ __forceinline__ f32x4_t mfma_tile<true>(bf16x8_t a, bf16x8_t b, f32x4_t c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+template <>
+__device__ __forceinline__ f32x16_t mfma_tile<false>(bf16x8_t a, bf16x8_t b, f32x16_t c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
 constexpr int G_LDS = GB_K + 8;  // bf16 per LDS row
 constexpr int G_CLD = GB_N + 4;  // fp32 C tile row stride
 
-template <int BM>
+// K splits for a grid of `tiles` output tiles, n_slots = 2 x compute units (two resident
+// blocks each): grids that would leave most units with a single block are split so that
+// every unit gets about two, each split keeping >= 4 k-steps of 64.
+__host__ __device__ inline int gemm_k_splits(int tiles, int nk, int n_slots) {
+  // measured: only long reductions (K >= 6144) gain from the extra partial-tile traffic
+  if (tiles <= 0 || nk < 96 || 2 * tiles > n_slots + n_slots / 8) return 1;
+  int sp = (n_slots + tiles - 1) / tiles;
+  const int cap = nk / 4;
+  if (sp > cap) sp = cap;
+  if (sp > 64) sp = 64;
+  return sp < 2 ? 1 : sp;
+}
+
+template <int BM, bool MF16>
 struct GemmShape {
   static constexpr int A_CH = BM * GB_K / 8 / 256;     // 16-byte A chunks per thread
   static constexpr int B_CH = GB_N * GB_K / 8 / 256;   // 16-byte B chunks per thread
@@ -130,25 +157,46 @@ struct GemmShape {
   static constexpr int LOOP_BYTES = 2 * BUF * 2;
   static constexpr int C_BYTES = BM * G_CLD * 4;
   static constexpr int SMEM = LOOP_BYTES > C_BYTES ? LOOP_BYTES : C_BYTES;
-  static constexpr int MI = BM / 64;                   // 32-row MFMA tiles per wave
+  // per wave (BM/2) x 64 outputs: MF16 -> (BM/32) x 4 tiles of 16x16, else (BM/64) x 2 of 32x32
+  static constexpr int MT = MF16 ? 16 : 32;
+  static constexpr int MI = (BM / 2) / MT;
+  static constexpr int NJ = 64 / MT;
+  static constexpr int KSTEP = MF16 ? 32 : 16;
 };
 
-template <int BM>
+// Blocks form a 1-D grid over (tile, k-split) work items decoded on the device from the
+// live row count. With k_splits > 1 every tile's K range is cut in k_splits slices whose
+// fp32 partial tiles go to `part` ([tile][split][BM][128]); k_gemm_fixup then adds them in
+// split order and runs the epilogue. k_splits follows gemm_k_splits(live tile count).
+template <int BM, bool MF16>
 __global__ __launch_bounds__(256, 2) void k_gemm_bf16(const bf16_t *__restrict__ A, int lda,
                                                       const bf16_t *__restrict__ B, int ldb,
                                                       int M, int N, int K,
-                                                      const int32_t *m_dev, Epi epi) {
-  using S = GemmShape<BM>;
+                                                      const int32_t *m_dev, Epi epi,
+                                                      int n_slots, float *__restrict__ part) {
+  using S = GemmShape<BM, MF16>;
+  using AccT = typename std::conditional<MF16, f32x4_t, f32x16_t>::type;
+  constexpr int ACC_N = MF16 ? 4 : 16;
   __shared__ __attribute__((aligned(16))) unsigned char smem[S::SMEM];
   bf16_t *sm = reinterpret_cast<bf16_t *>(smem);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   int M_eff = M;
   if (m_dev) M_eff = min(M, *m_dev);
-  const int m0 = blockIdx.y * BM;
-  if (m0 >= M_eff) return;
   const bool swiglu = epi.mode == EPI_SWIGLU;
-  const int n0 = blockIdx.x * (swiglu ? GB_N / 2 : GB_N);
+  const int bn_out = swiglu ? GB_N / 2 : GB_N;
+  const int n_tiles = (N + bn_out - 1) / bn_out;
+  const int tiles = ((M_eff + BM - 1) / BM) * n_tiles;
+  const int nk = K / GB_K;
+  const int splits = part ? gemm_k_splits(tiles, nk, n_slots) : 1;
+  const int item = blockIdx.x;
+  if (item >= tiles * splits) return;
+  const int tile = item / splits, split = item - tile * splits;
+  const int m0 = (tile / n_tiles) * BM;
+  const int n0 = (tile - (tile / n_tiles) * n_tiles) * bn_out;
+  const int k_per = (nk + splits - 1) / splits;
+  const int kt0 = min(nk, split * k_per), kt1 = min(nk, kt0 + k_per);
+  const int nkt = kt1 - kt0;
 
   // Per-thread 16-byte chunks: chunk c = tid + 256 i covers row c / 8, k columns
   // (c % 8) * 8 ..+7. Rows past M / N are clamped to a valid row: they only feed
@@ -177,16 +225,15 @@ __global__ __launch_bounds__(256, 2) void k_gemm_bf16(const bf16_t *__restrict__
     lb_off[i] = S::A_TILE + r * G_LDS + kc;
   }
 
-  f32x16_t acc[S::MI][2];
+  AccT acc[S::MI][S::NJ];
 #pragma unroll
   for (int i = 0; i < S::MI; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < S::NJ; ++j)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+      for (int r = 0; r < ACC_N; ++r) acc[i][j][r] = 0.f;
 
   u32x4_t ra0[S::A_CH], rb0[S::B_CH], ra1[S::A_CH], rb1[S::B_CH];
-  const int nk = K / GB_K;
 
 #define AKVS_GLOAD(RA, RB, KT)                                                      \
   {                                                                                 \
@@ -208,53 +255,92 @@ __global__ __launch_bounds__(256, 2) void k_gemm_bf16(const bf16_t *__restrict__
   {                                                                                           \
     const bf16_t *As_ = sm + (BUFI) * S::BUF;                                                 \
     const bf16_t *Bs_ = As_ + S::A_TILE;                                                      \
-    _Pragma("unroll") for (int ks = 0; ks < GB_K / 16; ++ks) {                                \
-      bf16x8_t af[S::MI], bfr[2];                                                             \
-      const int kk = ks * 16 + (lane >> 5) * 8;                                               \
+    _Pragma("unroll") for (int ks = 0; ks < GB_K / S::KSTEP; ++ks) {                          \
+      bf16x8_t af[S::MI], bfr[S::NJ];                                                         \
+      const int kk = ks * S::KSTEP + (lane / S::MT) * 8;                                      \
       _Pragma("unroll") for (int i = 0; i < S::MI; ++i) af[i] =                               \
-          *reinterpret_cast<const bf16x8_t *>(As_ + (wm * (BM / 2) + i * 32 + (lane & 31)) *  \
+          *reinterpret_cast<const bf16x8_t *>(                                                \
+              As_ + (wm * (BM / 2) + i * S::MT + (lane % S::MT)) * G_LDS + kk);                \
+      _Pragma("unroll") for (int j = 0; j < S::NJ; ++j) bfr[j] =                              \
+          *reinterpret_cast<const bf16x8_t *>(Bs_ + (wn * 64 + j * S::MT + (lane % S::MT)) *  \
                                                         G_LDS + kk);                          \
-      _Pragma("unroll") for (int j = 0; j < 2; ++j) bfr[j] =                                  \
-          *reinterpret_cast<const bf16x8_t *>(Bs_ + (wn * 64 + j * 32 + (lane & 31)) * G_LDS + \
-                                              kk);                                            \
       _Pragma("unroll") for (int i = 0; i < S::MI; ++i)                                       \
-          _Pragma("unroll") for (int j = 0; j < 2; ++j) acc[i][j] =                           \
-              __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);     \
+          _Pragma("unroll") for (int j = 0; j < S::NJ; ++j) acc[i][j] = mfma_tile<MF16>(      \
+              af[i], bfr[j], acc[i][j]);                                                      \
     }                                                                                         \
   }
 
-  AKVS_GLOAD(ra0, rb0, 0);
-  if (nk > 1) AKVS_GLOAD(ra1, rb1, 1);
-  AKVS_SSTORE(ra0, rb0, 0);
+  if (nkt > 0) {
+    AKVS_GLOAD(ra0, rb0, kt0);
+    if (nkt > 1) AKVS_GLOAD(ra1, rb1, kt0 + 1);
+    AKVS_SSTORE(ra0, rb0, 0);
+  }
   __syncthreads();
-  for (int kt = 0; kt < nk; kt += 2) {
-    // tile kt sits in LDS buffer 0, tile kt+1 is arriving in ra1/rb1
-    if (kt + 2 < nk) AKVS_GLOAD(ra0, rb0, kt + 2);
+  for (int j = 0; j < nkt; j += 2) {
+    // tile kt0+j sits in LDS buffer 0, tile kt0+j+1 is arriving in ra1/rb1
+    if (j + 2 < nkt) AKVS_GLOAD(ra0, rb0, kt0 + j + 2);
     AKVS_COMPUTE(0);
-    if (kt + 1 < nk) AKVS_SSTORE(ra1, rb1, 1);
+    if (j + 1 < nkt) AKVS_SSTORE(ra1, rb1, 1);
     __syncthreads();
-    if (kt + 1 >= nk) break;
-    // tile kt+1 sits in LDS buffer 1, tile kt+2 is arriving in ra0/rb0
-    if (kt + 3 < nk) AKVS_GLOAD(ra1, rb1, kt + 3);
+    if (j + 1 >= nkt) break;
+    // tile kt0+j+1 sits in LDS buffer 1, tile kt0+j+2 is arriving in ra0/rb0
+    if (j + 3 < nkt) AKVS_GLOAD(ra1, rb1, kt0 + j + 3);
     AKVS_COMPUTE(1);
-    if (kt + 2 < nk) AKVS_SSTORE(ra0, rb0, 0);
+    if (j + 2 < nkt) AKVS_SSTORE(ra0, rb0, 0);
     __syncthreads();
   }
 #undef AKVS_GLOAD
 #undef AKVS_SSTORE
 #undef AKVS_COMPUTE
 
-  float *Cs = reinterpret_cast<float *>(smem);
+  // split K: the partial tile goes to the workspace, k_gemm_fixup finishes it
+  float *Cs = splits > 1 ? part + (size_t)item * BM * GB_N : reinterpret_cast<float *>(smem);
+  const int ldc = splits > 1 ? GB_N : G_CLD;
 #pragma unroll
   for (int i = 0; i < S::MI; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < S::NJ; ++j)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = wm * (BM / 2) + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-        const int col = wn * 64 + j * 32 + (lane & 31);
-        Cs[row * G_CLD + col] = acc[i][j][r];
+      for (int r = 0; r < ACC_N; ++r) {
+        // 32x32 tile: row (r/4)*8 + (lane/32)*4 + r%4; 16x16 tile: row (lane/16)*4 + r
+        const int trow = MF16 ? (lane >> 4) * 4 + r : (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+        const int row = wm * (BM / 2) + i * S::MT + trow;
+        const int col = wn * 64 + j * S::MT + (lane % S::MT);
+        Cs[row * ldc + col] = acc[i][j][r];
       }
+  if (splits > 1) return;
+  __syncthreads();
+  epilogue_tile<BM, GB_N, 256>(Cs, G_CLD, m0, n0, M_eff, N, epi);
+}
+
+// Second pass of a K-split GEMM: one block per tile adds its partial tiles in split order
+// into an LDS tile and runs the epilogue.
+template <int BM>
+__global__ __launch_bounds__(256) void k_gemm_fixup(int M, int N, int K, const int32_t *m_dev,
+                                                    Epi epi, int n_slots,
+                                                    const float *__restrict__ part) {
+  __shared__ __attribute__((aligned(16))) float Cs[BM * G_CLD];
+  int M_eff = M;
+  if (m_dev) M_eff = min(M, *m_dev);
+  const bool swiglu = epi.mode == EPI_SWIGLU;
+  const int bn_out = swiglu ? GB_N / 2 : GB_N;
+  const int n_tiles = (N + bn_out - 1) / bn_out;
+  const int tiles = ((M_eff + BM - 1) / BM) * n_tiles;
+  const int splits = gemm_k_splits(tiles, K / GB_K, n_slots);
+  const int tile = blockIdx.x;
+  if (splits < 2 || tile >= tiles) return;
+  const int m0 = (tile / n_tiles) * BM;
+  const int n0 = (tile - (tile / n_tiles) * n_tiles) * bn_out;
+  const float *src = part + (size_t)tile * splits * BM * GB_N;
+  for (int e4 = threadIdx.x; e4 < BM * GB_N / 4; e4 += 256) {
+    const int row = e4 / (GB_N / 4), c4 = (e4 - row * (GB_N / 4)) * 4;
+    float4 acc = *reinterpret_cast<const float4 *>(src + row * GB_N + c4);
+    for (int sp = 1; sp < splits; ++sp) {
+      const float4 v = *reinterpret_cast<const float4 *>(src + (size_t)sp * BM * GB_N + row * GB_N + c4);
+      acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+    }
+    *reinterpret_cast<float4 *>(Cs + row * G_CLD + c4) = acc;
+  }
   __syncthreads();
   epilogue_tile<BM, GB_N, 256>(Cs, G_CLD, m0, n0, M_eff, N, epi);
 }
@@ -336,22 +422,61 @@ __global__ __launch_bounds__(256) void k_gemm_f32(const float *__restrict__ A, i
   epilogue_tile<GF_M, GF_N, 256>(Cs, GF_N + 4, m0, n0, M_eff, N, epi);
 }
 
+int gemm_cu_count() {
+  static int n = 0;
+  if (n == 0) {
+    int dev = 0, cu = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+        cu > 0)
+      n = cu;
+    else
+      n = 256;
+  }
+  return n;
+}
+
+size_t gemm_part_floats(int M, int N, int K, int mode) {
+  const int bn = mode == EPI_SWIGLU ? GB_N / 2 : GB_N;
+  const int tiles_cap = ((N + bn - 1) / bn) * ((M + 127) / 128);
+  const int n_slots = 2 * gemm_cu_count();
+  size_t items = 0;
+  for (int t = 1; t <= tiles_cap; ++t) {
+    const int sp = gemm_k_splits(t, K / GB_K, n_slots);
+    if (sp > 1 && (size_t)t * sp > items) items = (size_t)t * sp;
+  }
+  return items * 128 * GB_N;
+}
+
 hipError_t launch_gemm(const void *A, int lda, const void *B, int ldb, int M, int N, int K,
-                       const int32_t *m_dev, int dtype, const Epi &epi, hipStream_t s) {
+                       const int32_t *m_dev, int dtype, const Epi &epi, hipStream_t s,
+                       float *part) {
   if (M == 0 || N == 0) return hipSuccess;
   const bool swiglu = epi.mode == EPI_SWIGLU;
   if (dtype == AKVS_BF16) {
     const int bn = swiglu ? GB_N / 2 : GB_N;
     const int n_tiles = (N + bn - 1) / bn;
+    const int tiles_cap = n_tiles * ((M + 127) / 128);
     const bf16_t *a = reinterpret_cast<const bf16_t *>(A);
     const bf16_t *b16 = reinterpret_cast<const bf16_t *>(B);
-    // 128-row tiles unless that leaves most CUs (256 of them, 2 blocks each) idle
-    if ((long long)n_tiles * ((M + 127) / 128) >= 384) {
-      dim3 g(n_tiles, (M + 127) / 128), b(256);
-      hipLaunchKernelGGL(k_gemm_bf16<128>, g, b, 0, s, a, lda, b16, ldb, M, N, K, m_dev, epi);
-    } else {
-      dim3 g(n_tiles, (M + 63) / 64), b(256);
-      hipLaunchKernelGGL(k_gemm_bf16<64>, g, b, 0, s, a, lda, b16, ldb, M, N, K, m_dev, epi);
+    const int n_slots = part ? 2 * gemm_cu_count() : 0;
+    // the live row count decides the split on the device; size the grid for any count
+    int items = tiles_cap;
+    bool any_split = false;
+    if (part) {
+      for (int t = 1; t <= tiles_cap; ++t) {
+        const int sp = gemm_k_splits(t, K / GB_K, n_slots);
+        any_split |= sp > 1;
+        if (t * sp > items) items = t * sp;
+      }
+    }
+    hipLaunchKernelGGL((k_gemm_bf16<128, false>), dim3(items), dim3(256), 0, s, a, lda, b16, ldb,
+                       M, N, K, m_dev, epi, n_slots, part);
+    if (any_split) {
+      hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+      hipLaunchKernelGGL((k_gemm_fixup<128>), dim3(tiles_cap), dim3(256), 0, s, M, N, K, m_dev,
+                         epi, n_slots, part);
     }
   } else {
     const int bn = swiglu ? GF_N / 2 : GF_N;

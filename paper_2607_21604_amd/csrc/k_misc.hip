@@ -142,6 +142,26 @@ hipError_t launch_gather_rows(const float *src, int n_src, const int32_t *idx, i
   return hipGetLastError();
 }
 
+// dst[i] = src[*n_dev - n + i] for i < n (rows of row_bytes bytes, a multiple of 16).
+__global__ void k_copy_tail_rows(const char *src, size_t row_bytes, int n, const int32_t *n_dev,
+                                 char *dst) {
+  const int i = blockIdx.x;
+  const int j = *n_dev - n + i;
+  if (i >= n || j < 0) return;
+  const uint4 *a = reinterpret_cast<const uint4 *>(src + (size_t)j * row_bytes);
+  uint4 *b = reinterpret_cast<uint4 *>(dst + (size_t)i * row_bytes);
+  for (size_t e = threadIdx.x; e < row_bytes / 16; e += blockDim.x) b[e] = a[e];
+}
+
+hipError_t launch_copy_tail_rows(const void *src, size_t row_bytes, int n, const int32_t *n_dev,
+                                 void *dst, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_copy_tail_rows, dim3(n), dim3(256), 0, s,
+                     reinterpret_cast<const char *>(src), row_bytes, n, n_dev,
+                     reinterpret_cast<char *>(dst));
+  return hipGetLastError();
+}
+
 __global__ void k_token_setup(const int4 *meta, int n_chunks, int32_t *tok_delta,
                               int32_t *tok_chunk) {
   const int c = blockIdx.x;

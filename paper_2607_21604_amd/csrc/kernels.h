@@ -20,6 +20,9 @@ hipError_t launch_rmsnorm(const float *h, int ldh, int rows, const int32_t *rows
 // dst[i] = src[idx[i]], i < *n_dev (rows of D floats); indices outside [0, n_src) give 0.
 hipError_t launch_gather_rows(const float *src, int n_src, const int32_t *idx, int cap,
                               const int32_t *n_dev, int D, float *dst, hipStream_t s);
+// dst row i = src row (*n_dev - n + i), i < n: the last n of *n_dev rows.
+hipError_t launch_copy_tail_rows(const void *src, size_t row_bytes, int n, const int32_t *n_dev,
+                                 void *dst, hipStream_t s);
 // per unit token t < T_c: tok_delta[t] = s_i, tok_chunk[t] = i.
 hipError_t launch_token_setup(const int32_t *meta, int n_chunks, int32_t *tok_delta,
                               int32_t *tok_chunk, hipStream_t s);
@@ -73,9 +76,14 @@ struct Epi {
 };
 
 // C[M][N] = A[M][K] . B[N][K]^T with epilogue. Rows >= *m_dev (if given) are skipped.
-// SWIGLU: N is the FFN width F; B has 2F rows (gate, then up).
+// SWIGLU: N is the FFN width F; B has 2F rows (gate, then up). `part` (bf16 path, may be
+// null) is a workspace of gemm_part_floats(M, N, K, mode) floats that lets grids too small
+// to fill the GPU split K (partials summed in a fixed order by a second kernel).
 hipError_t launch_gemm(const void *A, int lda, const void *B, int ldb, int M, int N, int K,
-                       const int32_t *m_dev, int dtype, const Epi &epi, hipStream_t s);
+                       const int32_t *m_dev, int dtype, const Epi &epi, hipStream_t s,
+                       float *part = nullptr);
+size_t gemm_part_floats(int M, int N, int K, int mode);
+int gemm_cu_count();
 
 // ---- k_attn.hip ---------------------------------------------------------------------
 // With part_o / part_ml (bf16 path), the key range is split for parallelism:
