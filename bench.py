@@ -41,7 +41,7 @@ def parse():
     p.add_argument("--random-caches", action="store_true",
                    help="unit caches drawn at random instead of prefilled (counter runs)")
     p.add_argument("--calibrate-copy", action="store_true",
-                   help="run one 1 GiB device copy first (FETCH/WRITE counter calibration)")
+                   help="run one 1 GiB read + 1 GiB write kernel first (FETCH/WRITE counter calibration)")
     p.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                    help="write the GEMM traffic summary from two rocprofv3 --pmc CSVs and exit")
     return p.parse_args()
@@ -60,7 +60,8 @@ def source_hash(path=GEMM_SOURCE):
 
 def traffic_summary(fetch_csv, write_csv):
     """HBM bytes per GEMM launch from rocprofv3 FETCH_SIZE / WRITE_SIZE per-dispatch CSVs,
-    each scaled by what the counter reads for the 1 GiB copy kernel of the same run."""
+    each scaled by what the counter reads for the 1 GiB read + 1 GiB write elementwise
+    calibration kernel (torch.neg) of the same run."""
     import csv
 
     def per_kernel(path, counter):
@@ -71,7 +72,7 @@ def traffic_summary(fetch_csv, write_csv):
             v = float(r["Counter_Value"])
             if GEMM_KERNEL in r["Kernel_Name"]:
                 gemm.append(v)
-            elif "copy" in r["Kernel_Name"].lower() and int(r["Grid_Size"]) > 1 << 20:
+            elif "neg_kernel" in r["Kernel_Name"]:
                 copy.append(v)
         return gemm, copy
 
@@ -219,9 +220,11 @@ def main():
           f"L={shape.n_layers}, r={num}/{den}", file=sys.stderr, flush=True)
 
     if args.calibrate_copy:
+        # an elementwise kernel that reads and writes COPY_BYTES once each (a same-dtype
+        # copy_ may go to the DMA engines and show no kernel dispatch)
         src = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device=dev).fill_(1.0)
         dst = torch.empty_like(src)
-        dst.copy_(src)
+        torch.neg(src, out=dst)
         torch.cuda.synchronize()
         del src, dst
     w = synthetic.make_weights(shape, seed=args.seed, device=dev)

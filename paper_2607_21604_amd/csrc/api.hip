@@ -147,7 +147,7 @@ akvs_status check_layers(const akvs_model_cfg *m, const akvs_layer_w *lw) {
 
 struct Meta {
   std::vector<int32_t> m;  // [n][4]
-  long long t_ctx = 0, sum_b = 0, row_cap = 0, t_all = 0;
+  long long t_ctx = 0, sum_b = 0, row_cap = 0, row_min = 0, t_all = 0;
 };
 
 akvs_status check_reuse(const akvs_reuse_cfg *c, int n_layers, Meta *meta) {
@@ -167,7 +167,7 @@ akvs_status check_reuse(const akvs_reuse_cfg *c, int n_layers, Meta *meta) {
   Meta loc;
   Meta &mt = meta ? *meta : loc;
   mt.m.assign((size_t)c->n_chunks * 4, 0);
-  long long s = 0, off = 0, cap = 0;
+  long long s = 0, off = 0, cap = 0, lo = 0;
   for (int i = 0; i < c->n_chunks; ++i) {
     const long long n = c->chunk_len[i];
     REQUIRE(n >= 1, AKVS_EINVAL, "chunk %d has length %lld", i, n);
@@ -179,11 +179,13 @@ akvs_status check_reuse(const akvs_reuse_cfg *c, int n_layers, Meta *meta) {
     s += n;
     off += b;
     cap += n < 2 * b ? n : 2 * b;
+    lo += n < b ? n : b;  // the key probes alone are min(n, b) distinct rows
     REQUIRE(s + c->query_len < (1LL << 28), AKVS_ESHAPE, "context too long");
   }
   mt.t_ctx = s;
   mt.sum_b = off;
   mt.row_cap = cap + c->query_len;
+  mt.row_min = lo + c->query_len;
   mt.t_all = s + c->query_len;
   return AKVS_OK;
 }
@@ -416,16 +418,19 @@ Epi simple_epi(int mode, void *out, int ldo, int dtype) {
 // Attention output projection + MLP over rows (h updated in place).
 akvs_status out_mlp(const akvs_model_cfg *m, const akvs_layer_w &w, float *h, int rows,
                     const int32_t *rows_dev, const void *att, void *x, void *act, float *gpart,
-                    hipStream_t stream) {
+                    hipStream_t stream, int rows_min = 0) {
   const int D = m->d_model, F = m->ffn_dim, hqw = m->n_q_heads * m->head_dim;
   LAUNCH(AKVS_K_GEMM, launch_gemm(att, hqw, w.w_o, hqw, rows, D, hqw, rows_dev, m->dtype,
-                                  simple_epi(EPI_RESID, h, D, AKVS_F32), stream, gpart));
+                                  simple_epi(EPI_RESID, h, D, AKVS_F32), stream, gpart,
+                                  rows_min));
   LAUNCH(AKVS_K_NORM, launch_rmsnorm(h, D, rows, rows_dev, nullptr, w.mlp_norm, m->dtype, D,
                                      m->rms_eps, x, m->dtype, D, stream));
   LAUNCH(AKVS_K_GEMM, launch_gemm(x, D, w.w_gate_up, D, rows, F, D, rows_dev, m->dtype,
-                                  simple_epi(EPI_SWIGLU, act, F, m->dtype), stream, gpart));
+                                  simple_epi(EPI_SWIGLU, act, F, m->dtype), stream, gpart,
+                                  rows_min));
   LAUNCH(AKVS_K_GEMM, launch_gemm(act, F, w.w_down, F, rows, D, F, rows_dev, m->dtype,
-                                  simple_epi(EPI_RESID, h, D, AKVS_F32), stream, gpart));
+                                  simple_epi(EPI_RESID, h, D, AKVS_F32), stream, gpart,
+                                  rows_min));
   return AKVS_OK;
 }
 
@@ -847,7 +852,7 @@ akvs_status akvs_reuse_prefill(const int32_t *tokens, const void *embed, const a
     LAUNCH(AKVS_K_GEMM,
            launch_gemm(b.lb.x, D, lw[l].w_qkv, D, cap, qkvw, D, b.n_rows, m->dtype,
                        qkv_epi(m, b.lb.q, b.k_fresh, b.v_fresh, b.rows, 0, 0, b.rope, T, 0),
-                       stream, b.lb.gpart));
+                       stream, b.lb.gpart, (int)mt.row_min));
     LAUNCH(AKVS_K_OFFSET, launch_chunk_offset(b.k_fresh, b.v_fresh, m->dtype, b.fresh_row, cl,
                                               b.meta, nch, b.probe_k, b.probe_v, cfg->flags, hkv,
                                               hd, b.rope, T, b.mu_k, b.mu_v, stream));
@@ -862,7 +867,7 @@ akvs_status akvs_reuse_prefill(const int32_t *tokens, const void *embed, const a
                                                 m->n_q_heads, hkv, hd, m->dtype, b.lb.att,
                                                 b.lb.part_o, b.lb.part_ml, stream));
       st = out_mlp(m, lw[l], b.h_probe, cap, b.n_rows, b.lb.att, b.lb.x, b.lb.act, b.lb.gpart,
-                   stream);
+                   stream, (int)mt.row_min);
       if (st) return st;
       continue;
     }

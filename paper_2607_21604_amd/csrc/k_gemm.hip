@@ -132,6 +132,7 @@ __device__ __forceinline__ f32x16_t mfma_tile<false>(bf16x8_t a, bf16x8_t b, f32
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 constexpr int G_LDS = GB_K + 8;  // bf16 per LDS row
+constexpr int G_NS = 3;          // register prefetch stages
 constexpr int G_CLD = GB_N + 4;  // fp32 C tile row stride
 
 // K splits for a grid of `tiles` output tiles, n_slots = 2 x compute units (two resident
@@ -233,23 +234,24 @@ __global__ __launch_bounds__(256, 2) void k_gemm_bf16(const bf16_t *__restrict__
 #pragma unroll
       for (int r = 0; r < ACC_N; ++r) acc[i][j][r] = 0.f;
 
-  u32x4_t ra0[S::A_CH], rb0[S::B_CH], ra1[S::A_CH], rb1[S::B_CH];
+  // three register stages (ring slots) of operand chunks in flight
+  u32x4_t ra[G_NS][S::A_CH], rb[G_NS][S::B_CH];
 
-#define AKVS_GLOAD(RA, RB, KT)                                                      \
+#define AKVS_GLOAD(SL, KT)                                                          \
   {                                                                                 \
     const int k0_ = (KT) * GB_K;                                                    \
     _Pragma("unroll") for (int i = 0; i < S::A_CH; ++i)                             \
-        RA[i] = *reinterpret_cast<const u32x4_t *>(A + a_off[i] + k0_);             \
+        ra[SL][i] = *reinterpret_cast<const u32x4_t *>(A + a_off[i] + k0_);         \
     _Pragma("unroll") for (int i = 0; i < S::B_CH; ++i)                             \
-        RB[i] = *reinterpret_cast<const u32x4_t *>(B + b_off[i] + k0_);             \
+        rb[SL][i] = *reinterpret_cast<const u32x4_t *>(B + b_off[i] + k0_);         \
   }
-#define AKVS_SSTORE(RA, RB, BUFI)                                                   \
+#define AKVS_SSTORE(SL, BUFI)                                                       \
   {                                                                                 \
     bf16_t *base_ = sm + (BUFI) * S::BUF;                                           \
     _Pragma("unroll") for (int i = 0; i < S::A_CH; ++i)                             \
-        *reinterpret_cast<u32x4_t *>(base_ + la_off[i]) = RA[i];                    \
+        *reinterpret_cast<u32x4_t *>(base_ + la_off[i]) = ra[SL][i];                \
     _Pragma("unroll") for (int i = 0; i < S::B_CH; ++i)                             \
-        *reinterpret_cast<u32x4_t *>(base_ + lb_off[i]) = RB[i];                    \
+        *reinterpret_cast<u32x4_t *>(base_ + lb_off[i]) = rb[SL][i];                \
   }
 #define AKVS_COMPUTE(BUFI)                                                                    \
   {                                                                                           \
@@ -270,25 +272,35 @@ __global__ __launch_bounds__(256, 2) void k_gemm_bf16(const bf16_t *__restrict__
     }                                                                                         \
   }
 
-  if (nkt > 0) {
-    AKVS_GLOAD(ra0, rb0, kt0);
-    if (nkt > 1) AKVS_GLOAD(ra1, rb1, kt0 + 1);
-    AKVS_SSTORE(ra0, rb0, 0);
+  // One k-step: multiply the tile in LDS buffer u&1, move the next tile from its ring
+  // slot to the other buffer, then refill that slot G_NS tiles ahead. Loads past the
+  // range re-read its last tile, so every load is unconditional and the compiler's
+  // count of outstanding loads stays exact (each wait only covers the oldest stage);
+  // the scheduling barrier keeps the refill ahead of the next step's LDS traffic.
+#define AKVS_STEP(U, J)                                                             \
+  {                                                                                 \
+    AKVS_COMPUTE((U) & 1);                                                          \
+    AKVS_SSTORE(((U) + 1) % G_NS, ((U) + 1) & 1);                                   \
+    __syncthreads();                                                                \
+    AKVS_GLOAD(((U) + 1) % G_NS, min(kt0 + (J) + 1 + G_NS, kl));                    \
+    __builtin_amdgcn_sched_barrier(0);                                              \
   }
+  const int kl = kt1 - 1;  // kt1 >= 1: a valid tile even for an empty range
+#pragma unroll
+  for (int sl = 0; sl < G_NS; ++sl) AKVS_GLOAD(sl, min(kt0 + sl, kl));
+  AKVS_SSTORE(0, 0);
+  AKVS_GLOAD(0, min(kt0 + G_NS, kl));
   __syncthreads();
-  for (int j = 0; j < nkt; j += 2) {
-    // tile kt0+j sits in LDS buffer 0, tile kt0+j+1 is arriving in ra1/rb1
-    if (j + 2 < nkt) AKVS_GLOAD(ra0, rb0, kt0 + j + 2);
-    AKVS_COMPUTE(0);
-    if (j + 1 < nkt) AKVS_SSTORE(ra1, rb1, 1);
-    __syncthreads();
-    if (j + 1 >= nkt) break;
-    // tile kt0+j+1 sits in LDS buffer 1, tile kt0+j+2 is arriving in ra0/rb0
-    if (j + 3 < nkt) AKVS_GLOAD(ra1, rb1, kt0 + j + 3);
-    AKVS_COMPUTE(1);
-    if (j + 2 < nkt) AKVS_SSTORE(ra0, rb0, 0);
-    __syncthreads();
+  constexpr int UNR = 2 * G_NS;  // ring slot and LDS buffer both return to 0
+  int j = 0;
+  for (; j + UNR <= nkt; j += UNR) {
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) AKVS_STEP(u, j + u);
   }
+#pragma unroll
+  for (int u = 0; u < UNR; ++u)
+    if (j + u < nkt) AKVS_STEP(u, j + u);
+#undef AKVS_STEP
 #undef AKVS_GLOAD
 #undef AKVS_SSTORE
 #undef AKVS_COMPUTE
@@ -450,7 +462,7 @@ size_t gemm_part_floats(int M, int N, int K, int mode) {
 
 hipError_t launch_gemm(const void *A, int lda, const void *B, int ldb, int M, int N, int K,
                        const int32_t *m_dev, int dtype, const Epi &epi, hipStream_t s,
-                       float *part) {
+                       float *part, int m_min) {
   if (M == 0 || N == 0) return hipSuccess;
   const bool swiglu = epi.mode == EPI_SWIGLU;
   if (dtype == AKVS_BF16) {
@@ -459,16 +471,20 @@ hipError_t launch_gemm(const void *A, int lda, const void *B, int ldb, int M, in
     const int tiles_cap = n_tiles * ((M + 127) / 128);
     const bf16_t *a = reinterpret_cast<const bf16_t *>(A);
     const bf16_t *b16 = reinterpret_cast<const bf16_t *>(B);
-    const int n_slots = part ? 2 * gemm_cu_count() : 0;
-    // the live row count decides the split on the device; size the grid for any count
+    int n_slots = part ? 2 * gemm_cu_count() : 0;
+    // The live row count decides the split on the device; size the grid for every count
+    // the host cannot rule out (exactly M without a device count, else [m_min, M]).
+    const int lo = m_dev ? (m_min > 1 ? m_min : 1) : M;
+    const int t_lo = n_tiles * ((lo + 127) / 128);
     int items = tiles_cap;
     bool any_split = false;
     if (part) {
-      for (int t = 1; t <= tiles_cap; ++t) {
+      for (int t = t_lo; t <= tiles_cap; ++t) {
         const int sp = gemm_k_splits(t, K / GB_K, n_slots);
         any_split |= sp > 1;
         if (t * sp > items) items = t * sp;
       }
+      if (!any_split) n_slots = 0;  // no count in range splits: the device never splits
     }
     hipLaunchKernelGGL((k_gemm_bf16<128, false>), dim3(items), dim3(256), 0, s, a, lda, b16, ldb,
                        M, N, K, m_dev, epi, n_slots, part);

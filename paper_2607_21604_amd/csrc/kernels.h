@@ -78,10 +78,12 @@ struct Epi {
 // C[M][N] = A[M][K] . B[N][K]^T with epilogue. Rows >= *m_dev (if given) are skipped.
 // SWIGLU: N is the FFN width F; B has 2F rows (gate, then up). `part` (bf16 path, may be
 // null) is a workspace of gemm_part_floats(M, N, K, mode) floats that lets grids too small
-// to fill the GPU split K (partials summed in a fixed order by a second kernel).
+// to fill the GPU split K (partials summed in a fixed order by a second kernel). m_min is
+// a lower bound on *m_dev known to the host: the split (and its second kernel) is only
+// set up when some row count in [m_min, M] needs it.
 hipError_t launch_gemm(const void *A, int lda, const void *B, int ldb, int M, int N, int K,
                        const int32_t *m_dev, int dtype, const Epi &epi, hipStream_t s,
-                       float *part = nullptr);
+                       float *part = nullptr, int m_min = 0);
 size_t gemm_part_floats(int M, int N, int K, int mode);
 int gemm_cu_count();
 
