@@ -120,8 +120,6 @@ akvs_status check_model(const akvs_model_cfg *m) {
   if (m->dtype == AKVS_BF16) {
     REQUIRE(m->d_model % 64 == 0 && m->ffn_dim % 64 == 0, AKVS_EUNSUPPORTED,
             "bf16 models need d_model and ffn_dim multiples of 64");
-    REQUIRE(m->n_q_heads / m->n_kv_heads <= 12, AKVS_EUNSUPPORTED,
-            "bf16 attention supports up to 12 query heads per KV head");
   } else {
     REQUIRE(m->ffn_dim % 4 == 0, AKVS_ESHAPE, "ffn_dim must be a multiple of 4");
   }

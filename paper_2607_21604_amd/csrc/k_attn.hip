@@ -1,41 +1,60 @@
 // Attention of (sparse, position-sorted) query rows over a causal key range.
 //
-// bf16 path: one block = the query heads of one KV head over a tile of rows; each wave owns
-// 16 rows of one query head. Keys stream through LDS in tiles of 64 (K row-major, V
-// transposed), shared by every wave of the block. Scores are computed transposed,
-// S^T = K Q^T, with MFMA 16x16x32 bf16: each lane then holds 16 scores of ONE query row,
-// so the online softmax needs only two cross-lane steps, and the probabilities already
-// sit in the operand layout of the second product O^T = V^T P^T (the pairing of the
-// 32 contraction slots with keys is a fixed permutation applied to both operands).
+// bf16 path: one block = a group of the query heads that read one KV head, over a tile of
+// rows; each wave owns 32 rows of one query head. Keys stream through LDS in tiles of 64
+// (K row-major, V transposed), shared by every wave of the block. Scores are computed
+// transposed, S^T = K Q^T, with MFMA 32x32x16 bf16: each lane then holds 16 scores of ONE
+// query row (the other 16 of that row's 32 keys sit in lane ^ 32), and the probabilities
+// already sit in the operand layout of the second product O^T = V^T P^T (the pairing of
+// the 16 contraction slots with keys is a fixed permutation applied to both operands).
+// The running maximum is only raised when a score exceeds it by more than 2^8, which
+// keeps the rescaling of O off the common path while p = 2^(s - m) stays <= 256.
 // Row tiles are launched longest-first (rows are sorted by position, so later tiles
 // see more keys).
 #include "kernels.h"
 
 namespace akvs {
 
-// A block serves one KV head: RB query rows x all G query heads that read it. Wave w owns
-// 16 rows (row block w / G) of query head w % G; NW = (RB / 16) * G waves (<= 12). Waves 0-3
-// stage each 64-key K / V tile in LDS for all of them (double buffered, next tile
-// prefetched into registers during the current one). Block b serves KV head b % Hkv, so
-// the blocks streaming one head's keys run on the same XCD and share its L2.
 // Column (bf16 element) of key group g (4 keys) in row r of the V^T tile (rows of 64
 // elements, no padding). The XOR swizzle makes every 16-lane pass of both the transposed
 // 8-byte writes and the 8-byte fragment reads touch 32 distinct 4-byte banks.
 __device__ __forceinline__ int vt_col(int r, int g) { return (g ^ ((r ^ (r >> 3)) & 15)) * 4; }
 
+// Block shape for G query heads per KV head: heads per block gh (G split into G / gh
+// groups, gh <= 8) and 32-row blocks per block nrb, so that 4 <= gh * nrb <= 8 waves.
+struct AttnShape {
+  int gh, n_groups, nrb;
+};
+static inline AttnShape attn_shape(int G) {
+  AttnShape a{0, 0, 0};
+  if (G < 1) return a;
+  int n = (G + 7) / 8;
+  while (G % n) ++n;
+  a.n_groups = n;
+  a.gh = G / n;
+  a.nrb = 8 / a.gh < 4 ? 8 / a.gh : 4;
+  return a;
+}
+
+// A block serves head group hg of KV head kvh: 32 * nrb query rows x gh query heads. Wave
+// w owns 32 rows (row block w / gh) of query head kvh * G + hg * gh + w % gh. Waves 0-3
+// stage each 64-key K / V tile in LDS for all of them (double buffered, next tile
+// prefetched into registers during the current one). Block b serves KV head b % Hkv, so
+// the blocks streaming one head's keys run on the same XCD and share its L2.
 template <int HD>
-__global__ __launch_bounds__(768) void k_attn_bf16(const bf16_t *__restrict__ Q,
+__global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
                                                    const int32_t *pos, int pos0, int rows,
                                                    const int32_t *rows_dev,
                                                    const bf16_t *__restrict__ Kc,
                                                    const bf16_t *__restrict__ Vc, int n_keys,
-                                                   int hq, int hkv, int rb_rows, int n_tiles,
-                                                   int n_splits, int split_keys,
-                                                   float scale_log2, bf16_t *__restrict__ out,
+                                                   int hq, int hkv, int gh, int n_groups,
+                                                   int nrb, int n_tiles, int n_splits,
+                                                   int split_keys, float scale_log2,
+                                                   bf16_t *__restrict__ out,
                                                    float *__restrict__ part_o,
                                                    float *__restrict__ part_ml) {
-  constexpr int KS = HD / 32;          // contraction steps of S
-  constexpr int HB = HD / 16;          // 16-wide head-dim blocks of O
+  constexpr int KS = HD / 16;          // contraction steps of S
+  constexpr int DB = HD / 32;          // 32-wide head-dim blocks of O
   constexpr int KST = HD + 8;          // K tile row stride (bf16)
   constexpr int VST = 64;              // V^T tile row stride (bf16), swizzled by vt_col
   constexpr int CPK = HD / 8;          // 16-byte chunks per key row
@@ -44,27 +63,34 @@ __global__ __launch_bounds__(768) void k_attn_bf16(const bf16_t *__restrict__ Q,
   constexpr int KBUF = 64 * KST, VBUF = HD * VST;
   __shared__ __attribute__((aligned(16))) bf16_t Ks[2 * KBUF];
   __shared__ __attribute__((aligned(16))) bf16_t Vt[2 * VBUF];
-  __shared__ int s_max[12];
+  __shared__ int s_max[8];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int nw = blockDim.x >> 6;
   const bool loader = wave < 4;
   const int G = hq / hkv;
   const int kvh = blockIdx.x % hkv;
-  const int rest = (int)(blockIdx.x / hkv);
+  int rest = (int)(blockIdx.x / hkv);
+  const int hg = rest % n_groups;
+  rest /= n_groups;
   const int split = rest % n_splits;
   const int tile = n_tiles - 1 - rest / n_splits;
-  const int head = kvh * G + wave % G;
+  const int head = kvh * G + hg * gh + wave % gh;
   int R = rows;
   if (rows_dev) R = min(R, *rows_dev);
+  const int rb_rows = 32 * nrb;
   const int row0 = tile * rb_rows;
   if (tile < 0 || row0 >= R) return;
-  const int r = row0 + (wave / G) * 16 + (lane & 15);
+  const int hi = lane >> 5;  // which half of a row's 32 keys (and 32 dims) this lane holds
+  const int r = row0 + (wave / gh) * 32 + (lane & 31);
   const bool rvalid = r < R;
   const int rp = rvalid ? (pos ? pos[r] : pos0 + r) : -1;
   const int rpos = rvalid ? rp : 0;
-  int wmax = rp;
+  int wmax = rp, wmin = rvalid ? rp : 0x7fffffff;
 #pragma unroll
-  for (int o = 1; o < 64; o <<= 1) wmax = max(wmax, __shfl_xor(wmax, o, 64));
+  for (int o = 1; o < 32; o <<= 1) {
+    wmax = max(wmax, __shfl_xor(wmax, o, 64));
+    wmin = min(wmin, __shfl_xor(wmin, o, 64));
+  }
   if (lane == 0) s_max[wave] = wmax;
   __syncthreads();
   int bmax = -1;
@@ -75,23 +101,26 @@ __global__ __launch_bounds__(768) void k_attn_bf16(const bf16_t *__restrict__ Q,
   const int nkt = kv_end > kv_begin ? (kv_end - kv_begin + 63) / 64 : 0;
   const size_t prow = ((size_t)split * rows + r) * hq + head;  // partial slot of this lane's row
   if (nkt == 0) {
-    if (n_splits > 1 && rvalid && lane < 16) {
+    if (n_splits > 1 && rvalid && hi == 0) {
       part_ml[2 * prow] = -INFINITY;
       part_ml[2 * prow + 1] = 0.f;
     }
     return;
   }
 
+  // Q^T operand of S: lane holds dims ks*16 + hi*8 .. +7 of its row
   bf16x8_t qf[KS];
   {
-    const bf16_t *qrow = Q + ((size_t)(rvalid ? r : row0) * hq + head) * HD + (lane >> 4) * 8;
+    const bf16_t *qrow = Q + ((size_t)(rvalid ? r : row0) * hq + head) * HD + hi * 8;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) qf[ks] = *reinterpret_cast<const bf16x8_t *>(qrow + ks * 32);
+    for (int ks = 0; ks < KS; ++ks) qf[ks] = *reinterpret_cast<const bf16x8_t *>(qrow + ks * 16);
   }
-  f32x4_t o[HB];
+  f32x16_t o[DB];
 #pragma unroll
-  for (int hb = 0; hb < HB; ++hb) o[hb] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
-  float m_run = -INFINITY, l_run = 0.f;
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) o[db][i] = 0.f;
+  float m_run = -INFINITY, l_run = 0.f;  // l_run: this lane's half of the row sum
 
   // One K / V tile in the loading waves' registers. Keys past kv_end are clamped to the
   // last key: finite data that the score mask gives probability 0.
@@ -152,67 +181,64 @@ __global__ __launch_bounds__(768) void k_attn_bf16(const bf16_t *__restrict__ Q,
     for (int st = 0; st < 2; ++st) {
       const int sk0 = key0 + st * 32;
       if (sk0 <= wmax) {  // skip keys past every row of this wave
-        f32x4_t s[2];
-        s[0] = s[1] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+        // S^T block: 32 keys x 32 rows; s[i] is key sk0 + (i/4)*8 + hi*4 + i%4 of row r
+        f32x16_t sc;
 #pragma unroll
-        for (int kb2 = 0; kb2 < 2; ++kb2) {
-          const bf16_t *krow = ks_ + ((st * 2 + kb2) * 16 + (lane & 15)) * KST + (lane >> 4) * 8;
+        for (int i = 0; i < 16; ++i) sc[i] = 0.f;
+        const bf16_t *krow = ks_ + (st * 32 + (lane & 31)) * KST + hi * 8;
 #pragma unroll
-          for (int ks = 0; ks < KS; ++ks) {
-            const bf16x8_t a = *reinterpret_cast<const bf16x8_t *>(krow + ks * 32);
-            s[kb2] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[ks], s[kb2], 0, 0, 0);
+        for (int ks = 0; ks < KS; ++ks) {
+          const bf16x8_t a = *reinterpret_cast<const bf16x8_t *>(krow + ks * 16);
+          sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ks], sc, 0, 0, 0);
+        }
+        if (sk0 + 31 > wmin || sk0 + 31 >= kv_end) {  // causal / range mask needed
+#pragma unroll
+          for (int i = 0; i < 16; ++i) {
+            const int key = sk0 + (i >> 2) * 8 + hi * 4 + (i & 3);
+            if (key > rpos || key >= kv_end) sc[i] = -INFINITY;
           }
         }
-        float mx = -INFINITY;
+        float mx = sc[0];
 #pragma unroll
-        for (int kb2 = 0; kb2 < 2; ++kb2)
+        for (int i = 1; i < 16; ++i) mx = fmaxf(mx, sc[i]);
+        // raise the running maximum only when some score exceeds it by more than 2^8
+        if (__ballot(mx * scale_log2 > m_run + 8.f)) {
+          const float mp = fmaxf(mx, __shfl_xor(mx, 32, 64)) * scale_log2;
+          const float m_new = fmaxf(m_run, mp);
+          const float alpha = m_new == -INFINITY ? 1.f : exp2f(m_run - m_new);
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int key = sk0 + kb2 * 16 + (lane >> 4) * 4 + i;
-            const float v = (key > rpos || key >= kv_end) ? -INFINITY : s[kb2][i] * scale_log2;
-            s[kb2][i] = v;
-            mx = fmaxf(mx, v);
+          for (int db = 0; db < DB; ++db) o[db] *= alpha;
+          l_run *= alpha;
+          m_run = m_new;
+        }
+        // rows with no key yet keep m = -inf: offset by 0 then (every p is 0)
+        const float m_off = m_run == -INFINITY ? 0.f : m_run;
+        float pv[16];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          pv[i] = exp2f(fmaf(sc[i], scale_log2, -m_off));
+          l_run += pv[i];
+        }
+        // P^T operand of k-step t: slots hi*8 + j hold keys 16t + (j/4)*8 + hi*4 + j%4
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+          uint32_t pw[4];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) pw[j] = pack_bf2(pv[8 * t + 2 * j], pv[8 * t + 2 * j + 1]);
+          bf16x8_t pb;
+          __builtin_memcpy(&pb, pw, 16);
+          const int kg = st * 8 + 4 * t + hi;  // key groups kg and kg + 2 of the tile
+#pragma unroll
+          for (int db = 0; db < DB; ++db) {
+            const int vr = db * 32 + (lane & 31);
+            const bf16_t *vrow = vt_ + vr * VST;
+            const uint2 x0 = *reinterpret_cast<const uint2 *>(vrow + vt_col(vr, kg));
+            const uint2 x1 = *reinterpret_cast<const uint2 *>(vrow + vt_col(vr, kg + 2));
+            uint32_t vw[4] = {x0.x, x0.y, x1.x, x1.y};
+            bf16x8_t va;
+            __builtin_memcpy(&va, vw, 16);
+            o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb, o[db], 0, 0, 0);
           }
-        mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-        const float m_new = fmaxf(m_run, mx);
-        // rows with no key yet in this split keep m = -inf; offset by 0 then (p, alpha = 0)
-        const float m_off = m_new == -INFINITY ? 0.f : m_new;
-        const float alpha = exp2f(m_run - m_off);
-        float rs = 0.f;
-#pragma unroll
-        for (int kb2 = 0; kb2 < 2; ++kb2)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const float p = exp2f(s[kb2][i] - m_off);
-            s[kb2][i] = p;
-            rs += p;
-          }
-        rs += __shfl_xor(rs, 16, 64);
-        rs += __shfl_xor(rs, 32, 64);
-        l_run = l_run * alpha + rs;
-        m_run = m_new;
-#pragma unroll
-        for (int hb = 0; hb < HB; ++hb) o[hb] *= alpha;
-        uint32_t pw[4];
-        pw[0] = pack_bf2(s[0][0], s[0][1]);
-        pw[1] = pack_bf2(s[0][2], s[0][3]);
-        pw[2] = pack_bf2(s[1][0], s[1][1]);
-        pw[3] = pack_bf2(s[1][2], s[1][3]);
-        bf16x8_t pb;
-        __builtin_memcpy(&pb, pw, 16);
-#pragma unroll
-        for (int hb = 0; hb < HB; ++hb) {
-          const int vr = hb * 16 + (lane & 15);
-          const bf16_t *vrow = vt_ + vr * VST;
-          const int kg = st * 8 + (lane >> 4);
-          uint32_t vw[4];
-          const uint2 x0 = *reinterpret_cast<const uint2 *>(vrow + vt_col(vr, kg));
-          const uint2 x1 = *reinterpret_cast<const uint2 *>(vrow + vt_col(vr, kg + 4));
-          vw[0] = x0.x; vw[1] = x0.y; vw[2] = x1.x; vw[3] = x1.y;
-          bf16x8_t a;
-          __builtin_memcpy(&a, vw, 16);
-          o[hb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb, o[hb], 0, 0, 0);
         }
       }
     }
@@ -221,22 +247,31 @@ __global__ __launch_bounds__(768) void k_attn_bf16(const bf16_t *__restrict__ Q,
   }
 #undef AKVS_KV_LOAD
 #undef AKVS_KV_STORE
+  const float l_row = l_run + __shfl_xor(l_run, 32, 64);
   if (!rvalid) return;
+  // o[db][i] is dim db*32 + (i/4)*8 + hi*4 + i%4 of row r
   if (n_splits > 1) {  // unnormalised partial + (max, sum) for the combine pass
-    float *po = part_o + prow * HD + (lane >> 4) * 4;
+    float *po = part_o + prow * HD + hi * 4;
 #pragma unroll
-    for (int hb = 0; hb < HB; ++hb) store4(po + hb * 16, o[hb][0], o[hb][1], o[hb][2], o[hb][3]);
-    if (lane < 16) {
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4)
+        store4(po + db * 32 + q4 * 8, o[db][4 * q4], o[db][4 * q4 + 1], o[db][4 * q4 + 2],
+               o[db][4 * q4 + 3]);
+    if (hi == 0) {
       part_ml[2 * prow] = m_run;
-      part_ml[2 * prow + 1] = l_run;
+      part_ml[2 * prow + 1] = l_row;
     }
     return;
   }
-  const float inv = 1.0f / l_run;
-  bf16_t *orow = out + ((size_t)r * hq + head) * HD + (lane >> 4) * 4;
+  const float inv = 1.0f / l_row;
+  bf16_t *orow = out + ((size_t)r * hq + head) * HD + hi * 4;
 #pragma unroll
-  for (int hb = 0; hb < HB; ++hb)
-    store4(orow + hb * 16, o[hb][0] * inv, o[hb][1] * inv, o[hb][2] * inv, o[hb][3] * inv);
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int q4 = 0; q4 < 4; ++q4)
+      store4(orow + db * 32 + q4 * 8, o[db][4 * q4] * inv, o[db][4 * q4 + 1] * inv,
+             o[db][4 * q4 + 2] * inv, o[db][4 * q4 + 3] * inv);
 }
 
 // Merge of the key splits of one (row, head): weights 2^(m_s - max m), fixed split order.
@@ -265,13 +300,6 @@ __global__ __launch_bounds__(256) void k_attn_combine(const float *__restrict__ 
   const float inv = 1.0f / l;
   out[(size_t)item * hd + lane] = f2bf(a0 * inv);
   if (hd > 64) out[(size_t)item * hd + lane + 64] = f2bf(a1 * inv);
-}
-
-// Rows per block of the bf16 kernel for G query heads per KV head (0: not supported).
-static inline int attn_block_rows(int G) {
-  if (G < 1 || G > 12) return 0;
-  const int rb = 12 / G;
-  return 16 * (rb > 4 ? 4 : rb);
 }
 
 // fp32 path (small models): one wave per (row, head), keys in tiles of 64, online softmax.
@@ -331,9 +359,10 @@ __global__ __launch_bounds__(64) void k_attn_f32(const float *__restrict__ Q, co
 }
 
 int attn_splits(int rows, int hq, int hkv, int n_keys) {
-  const int rb = attn_block_rows(hq / hkv);
-  if (rb == 0 || rows <= 0) return 1;
-  const long long base = (long long)((rows + rb - 1) / rb) * hkv;
+  const AttnShape a = attn_shape(hq / hkv);
+  if (a.gh == 0 || rows <= 0) return 1;
+  const int rb = 32 * a.nrb;
+  const long long base = (long long)((rows + rb - 1) / rb) * hkv * a.n_groups;
   long long sp = (512 + base - 1) / base;           // aim at ~512 blocks
   const long long cap = (n_keys + 255) / 256;        // at least 256 keys per split
   if (sp > cap) sp = cap;
@@ -357,21 +386,21 @@ hipError_t launch_attention(const void *q, const int32_t *pos, int pos0, int row
     const bf16_t *K = reinterpret_cast<const bf16_t *>(k);
     const bf16_t *V = reinterpret_cast<const bf16_t *>(v);
     bf16_t *O = reinterpret_cast<bf16_t *>(out);
-    const int G = hq / hkv;
-    const int rb = attn_block_rows(G);
-    if (rb == 0) return hipErrorInvalidValue;
+    const AttnShape a = attn_shape(hq / hkv);
+    if (a.gh == 0) return hipErrorInvalidValue;
+    const int rb = 32 * a.nrb;
     const int n_tiles = (rows + rb - 1) / rb;
     const int n_splits = part_o ? attn_splits(rows, hq, hkv, n_keys) : 1;
     const int split_keys = attn_split_keys(n_keys, n_splits);
-    dim3 g(n_tiles * hkv * n_splits), b(64 * (rb / 16) * G);
+    dim3 g(n_tiles * hkv * a.n_groups * n_splits), b(64 * a.nrb * a.gh);
     if (hd == 128)
       hipLaunchKernelGGL(k_attn_bf16<128>, g, b, 0, s, Q, pos, pos0, rows, rows_dev, K, V, n_keys,
-                         hq, hkv, rb, n_tiles, n_splits, split_keys, scale_log2, O, part_o,
-                         part_ml);
+                         hq, hkv, a.gh, a.n_groups, a.nrb, n_tiles, n_splits, split_keys,
+                         scale_log2, O, part_o, part_ml);
     else
       hipLaunchKernelGGL(k_attn_bf16<64>, g, b, 0, s, Q, pos, pos0, rows, rows_dev, K, V, n_keys,
-                         hq, hkv, rb, n_tiles, n_splits, split_keys, scale_log2, O, part_o,
-                         part_ml);
+                         hq, hkv, a.gh, a.n_groups, a.nrb, n_tiles, n_splits, split_keys,
+                         scale_log2, O, part_o, part_ml);
     if (n_splits > 1) {
       hipError_t e = hipGetLastError();
       if (e != hipSuccess) return e;
