@@ -114,6 +114,9 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
     const bf16_t *qrow = Q + ((size_t)(rvalid ? r : row0) * hq + head) * HD + hi * 8;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) qf[ks] = *reinterpret_cast<const bf16x8_t *>(qrow + ks * 16);
+    // vmcnt(0): the query fragments are complete before the key loop, so the loop's waits
+    // on the K / V prefetch never cover them
+    __builtin_amdgcn_s_waitcnt(0x0f70);
   }
   f32x16_t o[DB];
 #pragma unroll
@@ -205,7 +208,7 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
         if (__ballot(mx * scale_log2 > m_run + 8.f)) {
           const float mp = fmaxf(mx, __shfl_xor(mx, 32, 64)) * scale_log2;
           const float m_new = fmaxf(m_run, mp);
-          const float alpha = m_new == -INFINITY ? 1.f : exp2f(m_run - m_new);
+          const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
 #pragma unroll
           for (int db = 0; db < DB; ++db) o[db] *= alpha;
           l_run *= alpha;
@@ -216,7 +219,7 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
         float pv[16];
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-          pv[i] = exp2f(fmaf(sc[i], scale_log2, -m_off));
+          pv[i] = __builtin_amdgcn_exp2f(fmaf(sc[i], scale_log2, -m_off));  // v_exp_f32: arguments <= 8
           l_run += pv[i];
         }
         // P^T operand of k-step t: slots hi*8 + j hold keys 16t + (j/4)*8 + hi*4 + j%4
