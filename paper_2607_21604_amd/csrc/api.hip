@@ -104,6 +104,14 @@ void prof_drain() {
     prof_end(stream, cls, ev_);                                                            \
   } while (0)
 
+// A projection GEMM and, when it splits K, its fixup pass (timed in the OTHER class so the
+// GEMM class times the main kernel alone).
+#define GEMM(...)                                                  \
+  do {                                                             \
+    LAUNCH(AKVS_K_GEMM, launch_gemm(__VA_ARGS__));                 \
+    LAUNCH(AKVS_K_OTHER, launch_gemm_fixup(__VA_ARGS__));          \
+  } while (0)
+
 // ---- validation -----------------------------------------------------------------------------
 akvs_status check_model(const akvs_model_cfg *m) {
   REQUIRE(m, AKVS_EINVAL, "model cfg is NULL");
@@ -418,17 +426,17 @@ akvs_status out_mlp(const akvs_model_cfg *m, const akvs_layer_w &w, float *h, in
                     const int32_t *rows_dev, const void *att, void *x, void *act, float *gpart,
                     hipStream_t stream, int rows_min = 0) {
   const int D = m->d_model, F = m->ffn_dim, hqw = m->n_q_heads * m->head_dim;
-  LAUNCH(AKVS_K_GEMM, launch_gemm(att, hqw, w.w_o, hqw, rows, D, hqw, rows_dev, m->dtype,
+  GEMM(att, hqw, w.w_o, hqw, rows, D, hqw, rows_dev, m->dtype,
                                   simple_epi(EPI_RESID, h, D, AKVS_F32), stream, gpart,
-                                  rows_min));
+                                  rows_min);
   LAUNCH(AKVS_K_NORM, launch_rmsnorm(h, D, rows, rows_dev, nullptr, w.mlp_norm, m->dtype, D,
                                      m->rms_eps, x, m->dtype, D, stream));
-  LAUNCH(AKVS_K_GEMM, launch_gemm(x, D, w.w_gate_up, D, rows, F, D, rows_dev, m->dtype,
+  GEMM(x, D, w.w_gate_up, D, rows, F, D, rows_dev, m->dtype,
                                   simple_epi(EPI_SWIGLU, act, F, m->dtype), stream, gpart,
-                                  rows_min));
-  LAUNCH(AKVS_K_GEMM, launch_gemm(act, F, w.w_down, F, rows, D, F, rows_dev, m->dtype,
+                                  rows_min);
+  GEMM(act, F, w.w_down, F, rows, D, F, rows_dev, m->dtype,
                                   simple_epi(EPI_RESID, h, D, AKVS_F32), stream, gpart,
-                                  rows_min));
+                                  rows_min);
   return AKVS_OK;
 }
 
@@ -441,9 +449,9 @@ akvs_status full_layer(const akvs_model_cfg *m, const akvs_layer_w &w, float *h,
   const int qkvw = (m->n_q_heads + 2 * m->n_kv_heads) * m->head_dim;
   LAUNCH(AKVS_K_NORM, launch_rmsnorm(h, D, n, nullptr, nullptr, w.attn_norm, m->dtype, D,
                                      m->rms_eps, lb.x, m->dtype, D, stream));
-  LAUNCH(AKVS_K_GEMM, launch_gemm(lb.x, D, w.w_qkv, D, n, qkvw, D, nullptr, m->dtype,
+  GEMM(lb.x, D, w.w_qkv, D, n, qkvw, D, nullptr, m->dtype,
                                   qkv_epi(m, lb.q, k_dst, v_dst, nullptr, pos0, 0, rope, n, pos0),
-                                  stream, lb.gpart));
+                                  stream, lb.gpart);
   LAUNCH(AKVS_K_ATTENTION, launch_attention(lb.q, nullptr, 0, n, nullptr, k_dst, v_dst, n,
                                             m->n_q_heads, m->n_kv_heads, m->head_dim, m->dtype,
                                             lb.att, lb.part_o, lb.part_ml, stream));
@@ -626,10 +634,9 @@ akvs_status akvs_probe_qkv(const float *h, int32_t n_rows, const int32_t *positi
   const int qkvw = (m->n_q_heads + 2 * m->n_kv_heads) * m->head_dim;
   LAUNCH(AKVS_K_NORM, launch_rmsnorm(h, D, n_rows, nullptr, nullptr, lw->attn_norm, m->dtype, D,
                                      m->rms_eps, x, m->dtype, D, stream));
-  LAUNCH(AKVS_K_GEMM,
-         launch_gemm(x, D, lw->w_qkv, D, n_rows, qkvw, D, nullptr, m->dtype,
+  GEMM(x, D, lw->w_qkv, D, n_rows, qkvw, D, nullptr, m->dtype,
                      qkv_epi(m, q, k_fresh, v_fresh, positions, 0, 0, rope, rope_rows, 0), stream,
-                     gpart));
+                     gpart);
   return AKVS_OK;
 }
 
@@ -830,8 +837,8 @@ akvs_status akvs_reuse_prefill(const int32_t *tokens, const void *embed, const a
     Epi e = qkv_epi(m, nullptr, b.k_chk, b.v_chk, nullptr, 0, 0, b.rope, T, 0);
     e.n_off = hqw;
     const char *wkv = reinterpret_cast<const char *>(lw[c].w_qkv) + (size_t)hqw * D * es;
-    LAUNCH(AKVS_K_GEMM, launch_gemm(b.lb.x, D, wkv, D, Tc, 2 * kvw, D, nullptr, m->dtype, e,
-                                    stream));
+    GEMM(b.lb.x, D, wkv, D, Tc, 2 * kvw, D, nullptr, m->dtype, e,
+                                    stream);
     LAUNCH(AKVS_K_DIVERGENCE,
            launch_divergence(b.k_chk, b.v_chk, m->dtype, cache_layer(cache, c, Tc, hkv, hd), Tc,
                              hkv, hd, b.tok_delta, b.rope, T, b.d_k, b.d_v, stream));
@@ -847,10 +854,9 @@ akvs_status akvs_reuse_prefill(const int32_t *tokens, const void *embed, const a
     CacheLayer cl = cache_layer(cache, l, Tc, hkv, hd);
     LAUNCH(AKVS_K_NORM, launch_rmsnorm(b.h_probe, D, cap, b.n_rows, nullptr, lw[l].attn_norm,
                                        m->dtype, D, m->rms_eps, b.lb.x, m->dtype, D, stream));
-    LAUNCH(AKVS_K_GEMM,
-           launch_gemm(b.lb.x, D, lw[l].w_qkv, D, cap, qkvw, D, b.n_rows, m->dtype,
+    GEMM(b.lb.x, D, lw[l].w_qkv, D, cap, qkvw, D, b.n_rows, m->dtype,
                        qkv_epi(m, b.lb.q, b.k_fresh, b.v_fresh, b.rows, 0, 0, b.rope, T, 0),
-                       stream, b.lb.gpart, (int)mt.row_min));
+                       stream, b.lb.gpart, (int)mt.row_min);
     LAUNCH(AKVS_K_OFFSET, launch_chunk_offset(b.k_fresh, b.v_fresh, m->dtype, b.fresh_row, cl,
                                               b.meta, nch, b.probe_k, b.probe_v, cfg->flags, hkv,
                                               hd, b.rope, T, b.mu_k, b.mu_v, stream));

@@ -325,13 +325,14 @@ __global__ __launch_bounds__(256, 2) void k_gemm_bf16(const bf16_t *__restrict__
   epilogue_tile<BM, GB_N, 256>(Cs, G_CLD, m0, n0, M_eff, N, epi);
 }
 
-// Second pass of a K-split GEMM: one block per tile adds its partial tiles in split order
-// into an LDS tile and runs the epilogue.
+// Second pass of a K-split GEMM: a block takes G_FR rows of one tile, adds their partial
+// rows in split order into an LDS slice and runs the epilogue on it.
+constexpr int G_FR = 16;
 template <int BM>
 __global__ __launch_bounds__(256) void k_gemm_fixup(int M, int N, int K, const int32_t *m_dev,
                                                     Epi epi, int n_slots,
                                                     const float *__restrict__ part) {
-  __shared__ __attribute__((aligned(16))) float Cs[BM * G_CLD];
+  __shared__ __attribute__((aligned(16))) float Cs[G_FR * G_CLD];
   int M_eff = M;
   if (m_dev) M_eff = min(M, *m_dev);
   const bool swiglu = epi.mode == EPI_SWIGLU;
@@ -339,22 +340,28 @@ __global__ __launch_bounds__(256) void k_gemm_fixup(int M, int N, int K, const i
   const int n_tiles = (N + bn_out - 1) / bn_out;
   const int tiles = ((M_eff + BM - 1) / BM) * n_tiles;
   const int splits = gemm_k_splits(tiles, K / GB_K, n_slots);
-  const int tile = blockIdx.x;
+  constexpr int SLICES = BM / G_FR;
+  const int tile = blockIdx.x / SLICES, slice = blockIdx.x - tile * SLICES;
   if (splits < 2 || tile >= tiles) return;
-  const int m0 = (tile / n_tiles) * BM;
+  const int m0 = (tile / n_tiles) * BM + slice * G_FR;
+  if (m0 >= M_eff) return;
   const int n0 = (tile - (tile / n_tiles) * n_tiles) * bn_out;
-  const float *src = part + (size_t)tile * splits * BM * GB_N;
-  for (int e4 = threadIdx.x; e4 < BM * GB_N / 4; e4 += 256) {
+  const float *src = part + (size_t)tile * splits * BM * GB_N + (size_t)slice * G_FR * GB_N;
+  constexpr int PER = G_FR * GB_N / 4 / 256;  // float4 per thread
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const int e4 = threadIdx.x + 256 * i;
     const int row = e4 / (GB_N / 4), c4 = (e4 - row * (GB_N / 4)) * 4;
-    float4 acc = *reinterpret_cast<const float4 *>(src + row * GB_N + c4);
+    const float *p = src + row * GB_N + c4;
+    float4 acc = *reinterpret_cast<const float4 *>(p);
     for (int sp = 1; sp < splits; ++sp) {
-      const float4 v = *reinterpret_cast<const float4 *>(src + (size_t)sp * BM * GB_N + row * GB_N + c4);
+      const float4 v = *reinterpret_cast<const float4 *>(p + (size_t)sp * BM * GB_N);
       acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
     }
     *reinterpret_cast<float4 *>(Cs + row * G_CLD + c4) = acc;
   }
   __syncthreads();
-  epilogue_tile<BM, GB_N, 256>(Cs, G_CLD, m0, n0, M_eff, N, epi);
+  epilogue_tile<G_FR, GB_N, 256>(Cs, G_CLD, m0, n0, M_eff, N, epi);
 }
 
 // ------------------------------------------------------------------------------------------
@@ -460,46 +467,62 @@ size_t gemm_part_floats(int M, int N, int K, int mode) {
   return items * 128 * GB_N;
 }
 
+// Grid of the bf16 GEMM: work items (tile x K-split) for every row count the host cannot
+// rule out (exactly M without a device count, else [m_min, M]); n_slots = 0 when no such
+// count splits K, so the device never splits either.
+struct GemmPlan {
+  int items, tiles_cap, n_slots;
+  bool any_split;
+};
+static GemmPlan gemm_plan(int M, int N, int K, const int32_t *m_dev, const Epi &epi,
+                          const float *part, int m_min) {
+  const int bn = epi.mode == EPI_SWIGLU ? GB_N / 2 : GB_N;
+  const int n_tiles = (N + bn - 1) / bn;
+  GemmPlan p;
+  p.tiles_cap = n_tiles * ((M + 127) / 128);
+  p.items = p.tiles_cap;
+  p.any_split = false;
+  p.n_slots = part ? 2 * gemm_cu_count() : 0;
+  if (part) {
+    const int lo = m_dev ? (m_min > 1 ? m_min : 1) : M;
+    for (int t = n_tiles * ((lo + 127) / 128); t <= p.tiles_cap; ++t) {
+      const int sp = gemm_k_splits(t, K / GB_K, p.n_slots);
+      p.any_split |= sp > 1;
+      if (t * sp > p.items) p.items = t * sp;
+    }
+    if (!p.any_split) p.n_slots = 0;
+  }
+  return p;
+}
+
 hipError_t launch_gemm(const void *A, int lda, const void *B, int ldb, int M, int N, int K,
                        const int32_t *m_dev, int dtype, const Epi &epi, hipStream_t s,
                        float *part, int m_min) {
   if (M == 0 || N == 0) return hipSuccess;
-  const bool swiglu = epi.mode == EPI_SWIGLU;
   if (dtype == AKVS_BF16) {
-    const int bn = swiglu ? GB_N / 2 : GB_N;
-    const int n_tiles = (N + bn - 1) / bn;
-    const int tiles_cap = n_tiles * ((M + 127) / 128);
-    const bf16_t *a = reinterpret_cast<const bf16_t *>(A);
-    const bf16_t *b16 = reinterpret_cast<const bf16_t *>(B);
-    int n_slots = part ? 2 * gemm_cu_count() : 0;
-    // The live row count decides the split on the device; size the grid for every count
-    // the host cannot rule out (exactly M without a device count, else [m_min, M]).
-    const int lo = m_dev ? (m_min > 1 ? m_min : 1) : M;
-    const int t_lo = n_tiles * ((lo + 127) / 128);
-    int items = tiles_cap;
-    bool any_split = false;
-    if (part) {
-      for (int t = t_lo; t <= tiles_cap; ++t) {
-        const int sp = gemm_k_splits(t, K / GB_K, n_slots);
-        any_split |= sp > 1;
-        if (t * sp > items) items = t * sp;
-      }
-      if (!any_split) n_slots = 0;  // no count in range splits: the device never splits
-    }
-    hipLaunchKernelGGL((k_gemm_bf16<128, false>), dim3(items), dim3(256), 0, s, a, lda, b16, ldb,
-                       M, N, K, m_dev, epi, n_slots, part);
-    if (any_split) {
-      hipError_t e = hipGetLastError();
-      if (e != hipSuccess) return e;
-      hipLaunchKernelGGL((k_gemm_fixup<128>), dim3(tiles_cap), dim3(256), 0, s, M, N, K, m_dev,
-                         epi, n_slots, part);
-    }
+    const GemmPlan p = gemm_plan(M, N, K, m_dev, epi, part, m_min);
+    hipLaunchKernelGGL((k_gemm_bf16<128, false>), dim3(p.items), dim3(256), 0, s,
+                       reinterpret_cast<const bf16_t *>(A), lda,
+                       reinterpret_cast<const bf16_t *>(B), ldb, M, N, K, m_dev, epi, p.n_slots,
+                       part);
   } else {
+    const bool swiglu = epi.mode == EPI_SWIGLU;
     const int bn = swiglu ? GF_N / 2 : GF_N;
     dim3 g((N + bn - 1) / bn, (M + GF_M - 1) / GF_M), b(256);
     hipLaunchKernelGGL(k_gemm_f32, g, b, 0, s, reinterpret_cast<const float *>(A), lda,
                        reinterpret_cast<const float *>(B), ldb, M, N, K, m_dev, epi);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm_fixup(const void *, int, const void *, int, int M, int N, int K,
+                             const int32_t *m_dev, int dtype, const Epi &epi, hipStream_t s,
+                             float *part, int m_min) {
+  if (M == 0 || N == 0 || dtype != AKVS_BF16) return hipSuccess;
+  const GemmPlan p = gemm_plan(M, N, K, m_dev, epi, part, m_min);
+  if (!p.any_split) return hipSuccess;
+  hipLaunchKernelGGL((k_gemm_fixup<128>), dim3(p.tiles_cap * (128 / G_FR)), dim3(256), 0, s, M,
+                     N, K, m_dev, epi, p.n_slots, part);
   return hipGetLastError();
 }
 

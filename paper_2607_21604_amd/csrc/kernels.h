@@ -84,6 +84,11 @@ struct Epi {
 hipError_t launch_gemm(const void *A, int lda, const void *B, int ldb, int M, int N, int K,
                        const int32_t *m_dev, int dtype, const Epi &epi, hipStream_t s,
                        float *part = nullptr, int m_min = 0);
+// Second kernel of a K-split GEMM (same arguments as launch_gemm, launched right after it on
+// the same stream); launches nothing when the first one cannot have split.
+hipError_t launch_gemm_fixup(const void *A, int lda, const void *B, int ldb, int M, int N,
+                             int K, const int32_t *m_dev, int dtype, const Epi &epi,
+                             hipStream_t s, float *part = nullptr, int m_min = 0);
 size_t gemm_part_floats(int M, int N, int K, int mode);
 int gemm_cu_count();
 
