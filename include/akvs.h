@@ -136,6 +136,10 @@ akvs_status akvs_chunk_meta(const akvs_reuse_cfg *cfg, int32_t *meta_out, int32_
 size_t akvs_workspace_size(const akvs_model_cfg *m, const akvs_reuse_cfg *cfg, int32_t n_tokens);
 /* Workspace bytes of akvs_probe_qkv / akvs_probe_out_mlp over n_rows rows. */
 size_t akvs_step_workspace_size(const akvs_model_cfg *m, int32_t n_rows);
+/* Workspace bytes that let akvs_sparse_query_attention split the key range of n_rows rows
+ * over n_keys keys (the launch configuration of the reuse prefill); 0 when that call would
+ * not split (fp32 models, or enough row tiles to fill the GPU). */
+size_t akvs_attention_workspace_size(const akvs_model_cfg *m, int32_t n_rows, int32_t n_keys);
 
 /* ---- step entries ---------------------------------------------------------------- */
 
@@ -217,10 +221,14 @@ akvs_status akvs_apply_correction(const akvs_cache *cache, const float *mu_k, co
  * rows against the whole corrected context): row r at position positions[r] attends
  * to keys 0..positions[r] (< n_keys) with scores q.k/sqrt(hd), fp32 softmax, query
  * head h reading KV head h/(Hq/Hkv). q: [n_rows][Hq][hd]; k, v: [n_keys][Hkv][hd];
- * out: [n_rows][Hq*hd]; all model dtype. positions must be ascending. */
+ * out: [n_rows][Hq*hd]; all model dtype. positions must be ascending. ws (may be NULL)
+ * of ws_bytes >= akvs_attention_workspace_size lets the call split the key range and
+ * merge the parts, as the reuse prefill does; a non-NULL ws that is too small is
+ * AKVS_ENOSPACE. */
 akvs_status akvs_sparse_query_attention(const void *q, const int32_t *positions, int32_t n_rows,
                                         const void *k, const void *v, int32_t n_keys,
-                                        const akvs_model_cfg *m, void *out, hipStream_t stream);
+                                        const akvs_model_cfg *m, void *out, void *ws,
+                                        size_t ws_bytes, hipStream_t stream);
 
 /* Rest of the probe rows' layer: h += attn_out W_o^T; x = RMSNorm(h) * mlp_norm;
  * h += (silu(x W_gate^T) * (x W_up^T)) W_down^T. h: [n_rows][D] fp32 (updated in

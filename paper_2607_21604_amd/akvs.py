@@ -78,6 +78,7 @@ _SIGS = {
     "akvs_chunk_meta": (_I, [ctypes.POINTER(ReuseCfg), _P, _P]),
     "akvs_workspace_size": (ctypes.c_size_t, [ctypes.POINTER(ModelCfg), ctypes.POINTER(ReuseCfg), _I]),
     "akvs_step_workspace_size": (ctypes.c_size_t, [ctypes.POINTER(ModelCfg), _I]),
+    "akvs_attention_workspace_size": (ctypes.c_size_t, [ctypes.POINTER(ModelCfg), _I, _I]),
     "akvs_rope_table": (_I, [_I, _I, ctypes.c_float, _P, _P]),
     "akvs_rerotate_keys": (_I, [ctypes.POINTER(Cache), _I, _I, _I, _P, _P, _I, _P, _P, _I, _P]),
     "akvs_check_divergence": (_I, [_P, _P, _I, ctypes.POINTER(Cache), _I, _I, _I, _P, _P, _I, _P,
@@ -91,7 +92,8 @@ _SIGS = {
     "akvs_apply_correction": (_I, [ctypes.POINTER(Cache), _P, _P, _P, _P, _P, _P, _P, _P,
                                    ctypes.POINTER(ReuseCfg), _P, ctypes.POINTER(ModelCfg), _P, _I,
                                    _P, _P, _P]),
-    "akvs_sparse_query_attention": (_I, [_P, _P, _I, _P, _P, _I, ctypes.POINTER(ModelCfg), _P, _P]),
+    "akvs_sparse_query_attention": (_I, [_P, _P, _I, _P, _P, _I, ctypes.POINTER(ModelCfg), _P, _P,
+                                         ctypes.c_size_t, _P]),
     "akvs_probe_out_mlp": (_I, [_P, _I, _P, ctypes.POINTER(ModelCfg), ctypes.POINTER(LayerW), _P,
                                 ctypes.c_size_t, _P]),
     "akvs_quantize_cache": (_I, [_P, _I, _I, _I, _I, _P, _P, _P]),
@@ -210,6 +212,10 @@ def akvs_step_workspace_size(m: ModelCfg, n_rows: int) -> int:
     return load().akvs_step_workspace_size(ctypes.byref(m), int(n_rows))
 
 
+def akvs_attention_workspace_size(m: ModelCfg, n_rows: int, n_keys: int) -> int:
+    return load().akvs_attention_workspace_size(ctypes.byref(m), int(n_rows), int(n_keys))
+
+
 def akvs_rope_table(n_pos, head_dim, theta, table, stream=None):
     _check(load().akvs_rope_table(n_pos, head_dim, theta, ptr(table), stream_handle(stream)),
            "akvs_rope_table")
@@ -264,9 +270,12 @@ def akvs_apply_correction(cache: Cache, mu_k, mu_v, w_k, w_v, flags, k_fresh, v_
                                         ptr(v_corr), stream_handle(stream)), "akvs_apply_correction")
 
 
-def akvs_sparse_query_attention(q, positions, n_rows, k, v, n_keys, m: ModelCfg, out, stream=None):
+def akvs_sparse_query_attention(q, positions, n_rows, k, v, n_keys, m: ModelCfg, out, ws=None,
+                                stream=None):
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
     _check(load().akvs_sparse_query_attention(ptr(q), ptr(positions), n_rows, ptr(k), ptr(v), n_keys,
-                                              ctypes.byref(m), ptr(out), stream_handle(stream)),
+                                              ctypes.byref(m), ptr(out), ptr(ws), nbytes,
+                                              stream_handle(stream)),
            "akvs_sparse_query_attention")
 
 

@@ -692,18 +692,49 @@ akvs_status akvs_apply_correction(const akvs_cache *cache, const float *mu_k, co
   return AKVS_OK;
 }
 
+// Key-split partials of one attention call over `rows` rows (bf16 models that split).
+static size_t attention_part_floats(const akvs_model_cfg *m, long long rows, long long n_keys,
+                                    size_t *ml_floats) {
+  *ml_floats = 0;
+  if (m->dtype != AKVS_BF16 || rows <= 0) return 0;
+  const long long sp = attn_splits((int)rows, m->n_q_heads, m->n_kv_heads, (int)n_keys);
+  if (sp < 2) return 0;
+  *ml_floats = (size_t)(sp * rows) * m->n_q_heads * 2;
+  return (size_t)(sp * rows) * m->n_q_heads * m->head_dim;
+}
+
+size_t akvs_attention_workspace_size(const akvs_model_cfg *m, int32_t n_rows, int32_t n_keys) {
+  if (check_model(m) != AKVS_OK || n_rows < 0 || n_keys < 1) return 0;
+  size_t ml;
+  const size_t o = attention_part_floats(m, n_rows, n_keys, &ml);
+  return o ? align256(o * sizeof(float)) + align256(ml * sizeof(float)) : 0;
+}
+
 akvs_status akvs_sparse_query_attention(const void *q, const int32_t *positions, int32_t n_rows,
                                         const void *k, const void *v, int32_t n_keys,
-                                        const akvs_model_cfg *m, void *out, hipStream_t stream) {
+                                        const akvs_model_cfg *m, void *out, void *ws,
+                                        size_t ws_bytes, hipStream_t stream) {
   akvs_status st = check_model(m);
   if (st) return st;
   REQUIRE(n_rows >= 0 && n_keys >= 1, AKVS_EINVAL, "n_rows >= 0, n_keys >= 1");
   REQUIRE(q && positions && k && v && out, AKVS_EINVAL, "NULL argument");
-  REQUIRE(aligned16(q) && aligned16(k) && aligned16(v) && aligned16(out), AKVS_EINVAL,
-          "misaligned argument");
+  REQUIRE(aligned16(q) && aligned16(k) && aligned16(v) && aligned16(out) && aligned16(ws),
+          AKVS_EINVAL, "misaligned argument");
+  float *part_o = nullptr, *part_ml = nullptr;
+  if (ws) {
+    size_t ml;
+    const size_t o = attention_part_floats(m, n_rows, n_keys, &ml);
+    const size_t need = o ? align256(o * sizeof(float)) + align256(ml * sizeof(float)) : 0;
+    REQUIRE(ws_bytes >= need, AKVS_ENOSPACE, "workspace %zu bytes, need %zu", ws_bytes, need);
+    if (o) {
+      Carver cv(ws);
+      part_o = cv.take<float>(o);
+      part_ml = cv.take<float>(ml);
+    }
+  }
   LAUNCH(AKVS_K_ATTENTION, launch_attention(q, positions, 0, n_rows, nullptr, k, v, n_keys,
                                             m->n_q_heads, m->n_kv_heads, m->head_dim, m->dtype,
-                                            out, nullptr, nullptr, stream));
+                                            out, part_o, part_ml, stream));
   return AKVS_OK;
 }
 

@@ -145,3 +145,17 @@ def test_missing_library_fails_loudly(tmp_path, monkeypatch):
     monkeypatch.setattr(akvs, "_lib", None)
     with pytest.raises(ImportError):
         akvs.load(str(tmp_path / "nope.so"))
+
+
+def test_attention_workspace(lib):
+    """The key-split workspace of the attention step: sized like the reuse prefill's probe
+    layers for a bf16 3B-class head layout, 0 for fp32 models, and a short one refused."""
+    m = akvs.ModelCfg(1, 3072, 24, 8, 128, 8192, 16, 1e6, 1e-6, akvs.AKVS_BF16)
+    need = akvs.akvs_attention_workspace_size(m, 1400, 4516)
+    assert need > 0 and need % 256 == 0
+    assert akvs.akvs_attention_workspace_size(m, 50000, 4516) == 0  # enough row tiles: no split
+    m32 = akvs.ModelCfg(1, 256, 4, 4, 64, 688, 16, 1e4, 1e-6, akvs.AKVS_F32)
+    assert akvs.akvs_attention_workspace_size(m32, 1400, 4516) == 0
+    st = lib.akvs_sparse_query_attention(4096, 4096, 1400, 4096, 4096, 4516, ctypes.byref(m), 4096,
+                                         4096, need - 256, None)
+    assert st == akvs.AKVS_ENOSPACE

@@ -310,10 +310,13 @@ def test_sparse_query_attention(dtype, hq, hkv, hd, n_rows, n_keys):
     k = storage_round(synthetic.random_array((n_keys, hkv, hd), 32), tdt)
     v = storage_round(synthetic.random_array((n_keys, hkv, hd), 33), tdt)
     m = akvs.ModelCfg(1, 64, hq, hkv, hd, 64, 16, 1e4, 1e-6, akvs.dtype_code(q))
-    out = torch.empty((n_rows, hq * hd), dtype=tdt, device=DEV)
-    akvs.akvs_sparse_query_attention(to_dev(q), to_dev(pos), n_rows, to_dev(k), to_dev(v), n_keys, m, out)
     ref = oracle.attention(f64(q), pos, f64(k), f64(v), np.arange(n_keys)).reshape(n_rows, -1)
-    assert max_rel(f64(out), ref) < (1e-2 if dtype == "bf16" else 1e-5)
+    nbytes = akvs.akvs_attention_workspace_size(m, n_rows, n_keys)
+    for ws in (None, torch.empty(max(nbytes, 1), dtype=torch.uint8, device=DEV)):
+        out = torch.empty((n_rows, hq * hd), dtype=tdt, device=DEV)
+        akvs.akvs_sparse_query_attention(to_dev(q), to_dev(pos), n_rows, to_dev(k), to_dev(v), n_keys,
+                                         m, out, ws)
+        assert max_rel(f64(out), ref) < (1e-2 if dtype == "bf16" else 1e-5)
 
 
 def gemm_case(shape, n_rows, seed):
