@@ -125,6 +125,8 @@ akvs_status check_model(const akvs_model_cfg *m) {
   REQUIRE(m->n_q_heads % m->n_kv_heads == 0, AKVS_ESHAPE,
           "n_q_heads %d is not a multiple of n_kv_heads %d", m->n_q_heads, m->n_kv_heads);
   REQUIRE(m->d_model % 8 == 0, AKVS_ESHAPE, "d_model must be a multiple of 8");
+  REQUIRE(m->n_kv_heads * m->head_dim <= 2048, AKVS_EUNSUPPORTED,
+          "n_kv_heads * head_dim %d above 2048", m->n_kv_heads * m->head_dim);
   if (m->dtype == AKVS_BF16) {
     REQUIRE(m->d_model % 64 == 0 && m->ffn_dim % 64 == 0, AKVS_EUNSUPPORTED,
             "bf16 models need d_model and ffn_dim multiples of 64");

@@ -237,39 +237,33 @@ hipError_t launch_select(const float *d_k, const float *d_v, const int32_t *meta
 }
 
 // ---------------------------------------------------------------------------------------
-// Per-unit offsets. grid = (m, 2 sides, pair blocks of 64); block = 4 waves. The unit's
-// probe positions and their rows in the fresh buffers are first staged in LDS, so the
-// data loads that follow are independent. Lane = one lo/hi pair of one head; wave w sums
-// the probes k = w, w+4, ... in ascending order, and the four partial sums are added in
-// wave order: a fixed fp32 summation order.
-constexpr int OFF_MAXB = 1024;  // probes staged per pass
+// Per-unit offsets. grid = (m, 2 sides); block = up to 16 waves. Wave w sums the probes
+// k = w, w + W, ... of the unit in ascending order; lane u handles the 8 lo/hi element
+// pairs e0..e0+7 (and + hd/2) of head u / (hd/16), so a wave reads a whole K (or V) row per
+// probe with 16-byte loads. The W wave partials are then added in wave order through LDS:
+// a fixed fp32 summation order.
+constexpr int OFF_LDS = 16384;  // floats: waves x Hkv*hd partial rows
 
-template <typename TF>
-__global__ __launch_bounds__(256) void k_chunk_offset(const TF *k_fresh, const TF *v_fresh,
-                                                      const int32_t *fresh_row, CacheLayer cache,
-                                                      const int4 *meta, const int32_t *probe_k,
-                                                      const int32_t *probe_v, uint32_t flags,
-                                                      int hkv, int hd, const float2 *rope,
-                                                      int rope_rows, float *mu_k, float *mu_v) {
-  __shared__ int s_tok[OFF_MAXB], s_row[OFF_MAXB];
-  __shared__ float s_part[4][64][2];
+template <typename TF, int UP>
+__global__ __launch_bounds__(UP == 1 ? 1024 : 512) void k_chunk_offset(const TF *__restrict__ k_fresh,
+                                                       const TF *__restrict__ v_fresh,
+                                                       const int32_t *fresh_row, CacheLayer cache,
+                                                       const int4 *meta, const int32_t *probe_k,
+                                                       const int32_t *probe_v, uint32_t flags,
+                                                       int hkv, int hd, const float2 *rope,
+                                                       int rope_rows, float *mu_k, float *mu_v) {
+  __shared__ float s_part[OFF_LDS];
   const int c = blockIdx.x;
   const int side = blockIdx.y;  // 0 = K, 1 = V
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int half = hd >> 1;
-  const int pairs = hkv * half;
-  const int p = blockIdx.z * 64 + lane;
-  const bool active = p < pairs;
-  const int h = active ? p / half : 0, e = active ? p - h * half : 0;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  const int half = hd >> 1, upr = half >> 3;  // 8-pair units per head
+  const int units = hkv * upr;                // <= 64 * UP
   const int kvw = hkv * hd;
   const int4 mc = meta[c];
   const int b = mc.z;
-  float *mu = (side == 0 ? mu_k : mu_v) + (size_t)c * kvw + h * hd;
+  float *mu = (side == 0 ? mu_k : mu_v) + (size_t)c * kvw;
   if (b == 0 || (flags & AKVS_F_NO_CORRECTION)) {
-    if (active && wave == 0) {
-      mu[e] = 0.f;
-      mu[e + half] = 0.f;
-    }
+    for (int e = threadIdx.x; e < kvw; e += blockDim.x) mu[e] = 0.f;
     return;
   }
   const TF *fresh = side == 0 ? k_fresh : v_fresh;
@@ -277,46 +271,57 @@ __global__ __launch_bounds__(256) void k_chunk_offset(const TF *k_fresh, const T
   const _Float16 *cm = side == 0 ? cache.k_meta : cache.v_meta;
   const int32_t *probes = (side == 0 ? probe_k : probe_v) + mc.w;
   const int delta = (mc.x >= 0 && mc.x < rope_rows) ? mc.x : 0;
-  const float2 cs = rope[(size_t)delta * half + e];
-  float slo = 0.f, shi = 0.f;
-  for (int kb = 0; kb < b; kb += OFF_MAXB) {
-    const int nb = min(OFF_MAXB, b - kb);
-    __syncthreads();
-    for (int k = threadIdx.x; k < nb; k += blockDim.x) {
-      const int j = probes[kb + k];
-      const bool inside = j >= mc.x && j < mc.x + mc.y;  // a token of this unit
-      const int r = inside ? fresh_row[j] : -1;
-      s_tok[k] = inside ? j : -1;
-      s_row[k] = r;
-    }
-    __syncthreads();
-    if (active) {
-      for (int k = wave; k < nb; k += 4) {
-        const int j = s_tok[k], r = s_row[k];
-        if (j < 0 || r < 0) continue;
-        const size_t frow = (size_t)r * hkv + h;
+  const float2 *rrow = rope + (size_t)delta * half;
+  float acc[UP][16];
+#pragma unroll
+  for (int q = 0; q < UP; ++q)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) acc[q][i] = 0.f;
+#pragma unroll 2
+  for (int k = wave; k < b; k += nw) {
+    const int j = probes[k];
+    const bool inside = j >= mc.x && j < mc.x + mc.y;  // a token of this unit
+    const int r = inside ? fresh_row[j] : -1;
+    if (r < 0) continue;  // uniform over the wave
+#pragma unroll
+    for (int q = 0; q < UP; ++q) {
+      const int u = lane + 64 * q;
+      if (u < units) {
+        const int h = u / upr, e0 = (u - h * upr) * 8;
+        float flo[8], fhi[8], clo[8], chi[8];
+        const TF *fr = fresh + ((size_t)r * hkv + h) * hd;
+        load8(fr + e0, flo);
+        load8(fr + e0 + half, fhi);
         const size_t crow = (size_t)j * hkv + h;
-        const float flo = load1(fresh + frow * hd + e), fhi = load1(fresh + frow * hd + e + half);
-        float clo = cache_load1(cb, cm, cache.dtype, crow, hd, e);
-        float chi = cache_load1(cb, cm, cache.dtype, crow, hd, e + half);
-        if (side == 0) {
-          const float a = clo, bb = chi;
-          clo = a * cs.x - bb * cs.y;
-          chi = bb * cs.x + a * cs.y;
+        cache_load8(cb, cm, cache.dtype, crow, hd, e0, clo);
+        cache_load8(cb, cm, cache.dtype, crow, hd, e0 + half, chi);
+        if (side == 0) rotate8(rrow, e0, clo, chi);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          acc[q][i] += flo[i] - clo[i];
+          acc[q][8 + i] += fhi[i] - chi[i];
         }
-        slo += flo - clo;
-        shi += fhi - chi;
       }
     }
   }
-  s_part[wave][lane][0] = slo;
-  s_part[wave][lane][1] = shi;
+#pragma unroll
+  for (int q = 0; q < UP; ++q) {
+    const int u = lane + 64 * q;
+    if (u < units) {
+      const int h = u / upr, e0 = (u - h * upr) * 8;
+      float *dst = s_part + wave * kvw + h * hd + e0;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        dst[i] = acc[q][i];
+        dst[half + i] = acc[q][8 + i];
+      }
+    }
+  }
   __syncthreads();
-  if (wave == 0 && active) {
-    const float tlo = ((s_part[0][lane][0] + s_part[1][lane][0]) + s_part[2][lane][0]) + s_part[3][lane][0];
-    const float thi = ((s_part[0][lane][1] + s_part[1][lane][1]) + s_part[2][lane][1]) + s_part[3][lane][1];
-    mu[e] = tlo / (float)b;
-    mu[e + half] = thi / (float)b;
+  for (int e = threadIdx.x; e < kvw; e += blockDim.x) {
+    float t = 0.f;
+    for (int w = 0; w < nw; ++w) t += s_part[w * kvw + e];
+    mu[e] = t / (float)b;
   }
 }
 
@@ -325,24 +330,31 @@ hipError_t launch_chunk_offset(const void *k_fresh, const void *v_fresh, int fre
                                int n_chunks, const int32_t *probe_k, const int32_t *probe_v,
                                uint32_t flags, int hkv, int hd, const float *rope, int rope_rows,
                                float *mu_k, float *mu_v, hipStream_t s) {
-  const int pairs = hkv * hd / 2;
-  dim3 g(n_chunks, 2, (pairs + 63) / 64), b(256);
+  const int kvw = hkv * hd;
+  if (kvw > 2048 || hd % 16) return hipErrorInvalidValue;
+  int nw = OFF_LDS / kvw;
+  if (nw > 16) nw = 16;
+  if (kvw > 1024 && nw > 8) nw = 8;  // two units per lane: 8 waves of up to 256 registers
+  dim3 g(n_chunks, 2), b(64 * nw);
   const int4 *m4 = reinterpret_cast<const int4 *>(meta);
   const float2 *r = reinterpret_cast<const float2 *>(rope);
-  if (fresh_dtype == AKVS_BF16)
-    hipLaunchKernelGGL(k_chunk_offset<bf16_t>, g, b, 0, s, as<bf16_t>(k_fresh), as<bf16_t>(v_fresh),
-                       fresh_row, cache, m4, probe_k, probe_v, flags, hkv, hd, r, rope_rows, mu_k,
-                       mu_v);
-  else
-    hipLaunchKernelGGL(k_chunk_offset<float>, g, b, 0, s, as<float>(k_fresh), as<float>(v_fresh),
-                       fresh_row, cache, m4, probe_k, probe_v, flags, hkv, hd, r, rope_rows, mu_k,
-                       mu_v);
+#define AKVS_OFFSET(TF, UP)                                                                    \
+  hipLaunchKernelGGL((k_chunk_offset<TF, UP>), g, b, 0, s, as<TF>(k_fresh), as<TF>(v_fresh),      \
+                     fresh_row, cache, m4, probe_k, probe_v, flags, hkv, hd, r, rope_rows, mu_k, \
+                     mu_v)
+  const bool wide = kvw > 1024;
+  if (fresh_dtype == AKVS_BF16) {
+    if (wide) AKVS_OFFSET(bf16_t, 2); else AKVS_OFFSET(bf16_t, 1);
+  } else {
+    if (wide) AKVS_OFFSET(float, 2); else AKVS_OFFSET(float, 1);
+  }
+#undef AKVS_OFFSET
   return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------------------
 // Fused re-rotation + dequantisation + weighted correction (+ fresh rows), K and V.
-// Thread = (position t, head h, 8 lo/hi pairs). t < t_ctx: unit token; else query row.
+// Position t < t_ctx: unit token; else query row.
 // Unit holding context position t: the last i with meta[i].start <= t.
 __device__ __forceinline__ int find_chunk(const int4 *meta, int n_chunks, int t) {
   int lo = 0, hi = n_chunks - 1;
@@ -353,103 +365,124 @@ __device__ __forceinline__ int find_chunk(const int4 *meta, int n_chunks, int t)
   return lo;
 }
 
-template <typename TS>
-__global__ void k_correction(CacheLayer cache, const float *mu_k, const float *mu_v,
-                             const float *w_k, const float *w_v, const uint8_t *tok_flags,
-                             const TS *k_fresh, const TS *v_fresh, const int32_t *fresh_row,
-                             const int32_t *tok_chunk, const int32_t *tok_delta,
-                             const int4 *meta, int n_chunks, int t_ctx,
-                             int t_all, int hkv, int hd, uint32_t flags, const float2 *rope,
-                             int rope_rows, TS *k_corr, TS *v_corr) {
-  const int half = hd >> 1;
-  const int units_per_head = half >> 3;
-  const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
-  const long long per_tok = (long long)hkv * units_per_head;
-  const int t = (int)(gid / per_tok);
-  if (t >= t_all) return;
-  const int rem = (int)(gid - (long long)t * per_tok);
-  const int h = rem / units_per_head;
-  const int e0 = (rem - h * units_per_head) * 8;
-  const size_t orow = (size_t)t * hkv + h;
-  TS *ko = k_corr + orow * hd;
-  TS *vo = v_corr + orow * hd;
+// Per position: source flags, unit and rotation offset (query rows: fresh, no unit).
+struct CorrTok {
+  int chunk, delta, fr;
+  bool fresh_k, fresh_v;
+};
+
+__device__ __forceinline__ CorrTok corr_token(int t, int t_ctx, const uint8_t *tok_flags,
+                                              const int32_t *fresh_row, const int32_t *tok_chunk,
+                                              const int32_t *tok_delta, const int4 *meta,
+                                              int n_chunks, int rope_rows, uint32_t flags) {
+  CorrTok c{0, 0, -1, true, true};
   const uint8_t f = (t < t_ctx) ? (tok_flags ? tok_flags[t] : 0) : 3;
-  int chunk = 0, delta = 0;
   if (t < t_ctx) {
     if (tok_chunk) {
-      chunk = tok_chunk[t];
-      delta = tok_delta[t];
+      c.chunk = tok_chunk[t];
+      c.delta = tok_delta[t];
     } else if (meta) {
-      chunk = find_chunk(meta, n_chunks, t);
-      delta = meta[chunk].x;
+      c.chunk = find_chunk(meta, n_chunks, t);
+      c.delta = meta[c.chunk].x;
     } else {
-      delta = tok_delta[t];
+      c.delta = tok_delta[t];
     }
-    if (delta < 0 || delta >= rope_rows) delta = 0;
-    if (chunk < 0 || chunk >= n_chunks) chunk = 0;
+    if (c.delta < 0 || c.delta >= rope_rows) c.delta = 0;
+    if (c.chunk < 0 || c.chunk >= n_chunks) c.chunk = 0;
   }
   const bool any = f != 0 && (flags & AKVS_F_FRESH_IF_RECOMPUTED);
-  const bool fresh_k = (f & 1) || any;
-  const bool fresh_v = (f & 2) || any;
-  const int fr = (fresh_k || fresh_v) ? fresh_row[t] : -1;
-  float lo[8], hi[8];
-  // ---- K
-  if (fresh_k) {
+  c.fresh_k = (f & 1) || any;
+  c.fresh_v = (f & 2) || any;
+  c.fr = (c.fresh_k || c.fresh_v) ? fresh_row[t] : -1;
+  return c;
+}
+
+// One side (K: rotated) of one position: the 8 lo/hi pairs e0.. of head h.
+template <typename TS>
+__device__ __forceinline__ void corr_side(bool fresh, int fr, const TS *__restrict__ fresh_buf,
+                                          const void *cb, const _Float16 *cm, int dtype,
+                                          size_t orow, int hkv, int h, int hd, int e0,
+                                          const float2 *rrow, const float *mu, float w,
+                                          float (&lo)[8], float (&hi)[8]) {
+  const int half = hd >> 1;
+  if (fresh) {
     if (fr >= 0) {
-      const TS *src = k_fresh + ((size_t)fr * hkv + h) * hd;
+      const TS *src = fresh_buf + ((size_t)fr * hkv + h) * hd;
       load8(src + e0, lo);
       load8(src + e0 + half, hi);
     } else {
 #pragma unroll
       for (int i = 0; i < 8; ++i) lo[i] = hi[i] = 0.f;
     }
-  } else {
-    cache_load8(cache.k, cache.k_meta, cache.dtype, orow, hd, e0, lo);
-    cache_load8(cache.k, cache.k_meta, cache.dtype, orow, hd, e0 + half, hi);
-    rotate8(rope + (size_t)delta * half, e0, lo, hi);
-    if (mu_k) {
-      const float w = w_k[t];
-      const float *mu = mu_k + (size_t)chunk * hkv * hd + h * hd;
-      float ml[8], mh[8];
-      load8(mu + e0, ml);
-      load8(mu + e0 + half, mh);
+    return;
+  }
+  cache_load8(cb, cm, dtype, orow, hd, e0, lo);
+  cache_load8(cb, cm, dtype, orow, hd, e0 + half, hi);
+  if (rrow) rotate8(rrow, e0, lo, hi);
+  if (mu) {
+    float ml[8], mh[8];
+    load8(mu + e0, ml);
+    load8(mu + e0 + half, mh);
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        lo[i] = fmaf(w, ml[i], lo[i]);
-        hi[i] = fmaf(w, mh[i], hi[i]);
-      }
+    for (int i = 0; i < 8; ++i) {
+      lo[i] = fmaf(w, ml[i], lo[i]);
+      hi[i] = fmaf(w, mh[i], hi[i]);
     }
   }
-  store8(ko + e0, lo);
-  store8(ko + e0 + half, hi);
-  // ---- V
-  if (fresh_v) {
-    if (fr >= 0) {
-      const TS *src = v_fresh + ((size_t)fr * hkv + h) * hd;
-      load8(src + e0, lo);
-      load8(src + e0 + half, hi);
-    } else {
+}
+
+// Thread = (CORR_T consecutive positions, head h, 8 lo/hi pairs): with Hkv*hd/16 = 64 a
+// wave covers whole K and V rows. (Two positions per thread measured slower than one:
+// fewer waves in flight outweigh the longer per-lane load queue.)
+constexpr int CORR_T = 1;
+template <typename TS>
+__global__ __launch_bounds__(256) void k_correction(CacheLayer cache, const float *mu_k,
+                                                    const float *mu_v, const float *w_k,
+                                                    const float *w_v, const uint8_t *tok_flags,
+                                                    const TS *__restrict__ k_fresh,
+                                                    const TS *__restrict__ v_fresh,
+                                                    const int32_t *fresh_row,
+                                                    const int32_t *tok_chunk,
+                                                    const int32_t *tok_delta, const int4 *meta,
+                                                    int n_chunks, int t_ctx, int t_all, int hkv,
+                                                    int hd, uint32_t flags, const float2 *rope,
+                                                    int rope_rows, TS *__restrict__ k_corr,
+                                                    TS *__restrict__ v_corr) {
+  const int half = hd >> 1;
+  const int units = hkv * (half >> 3);
+  const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  const long long grp = gid / units;
+  const int u = (int)(gid - grp * units);
+  const int t0 = (int)(grp * CORR_T);
+  if (t0 >= t_all) return;
+  const int h = u / (half >> 3);
+  const int e0 = (u - h * (half >> 3)) * 8;
+  float klo[CORR_T][8], khi[CORR_T][8], vlo[CORR_T][8], vhi[CORR_T][8];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) lo[i] = hi[i] = 0.f;
-    }
-  } else {
-    cache_load8(cache.v, cache.v_meta, cache.dtype, orow, hd, e0, lo);
-    cache_load8(cache.v, cache.v_meta, cache.dtype, orow, hd, e0 + half, hi);
-    if (mu_v) {
-      const float w = w_v[t];
-      const float *mu = mu_v + (size_t)chunk * hkv * hd + h * hd;
-      float ml[8], mh[8];
-      load8(mu + e0, ml);
-      load8(mu + e0 + half, mh);
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        lo[i] = fmaf(w, ml[i], lo[i]);
-        hi[i] = fmaf(w, mh[i], hi[i]);
-      }
-    }
+  for (int i = 0; i < CORR_T; ++i) {
+    const int t = min(t0 + i, t_all - 1);  // a repeated last position is computed twice
+    const CorrTok c = corr_token(t, t_ctx, tok_flags, fresh_row, tok_chunk, tok_delta, meta,
+                                 n_chunks, rope_rows, flags);
+    const size_t orow = (size_t)t * hkv + h;
+    const size_t mo = (size_t)c.chunk * hkv * hd + (size_t)h * hd;
+    corr_side(c.fresh_k, c.fr, k_fresh, cache.k, cache.k_meta, cache.dtype, orow, hkv, h, hd, e0,
+              rope + (size_t)c.delta * half, mu_k ? mu_k + mo : nullptr, mu_k ? w_k[t] : 0.f,
+              klo[i], khi[i]);
+    corr_side(c.fresh_v, c.fr, v_fresh, cache.v, cache.v_meta, cache.dtype, orow, hkv, h, hd, e0,
+              nullptr, mu_v ? mu_v + mo : nullptr, mu_v ? w_v[t] : 0.f, vlo[i], vhi[i]);
   }
-  store8(vo + e0, lo);
-  store8(vo + e0 + half, hi);
+#pragma unroll
+  for (int i = 0; i < CORR_T; ++i) {
+    const int t = t0 + i;
+    if (t >= t_all) break;
+    const size_t orow = (size_t)t * hkv + h;
+    TS *ko = k_corr + orow * hd;
+    TS *vo = v_corr + orow * hd;
+    store8(ko + e0, klo[i]);
+    store8(ko + e0 + half, khi[i]);
+    store8(vo + e0, vlo[i]);
+    store8(vo + e0 + half, vhi[i]);
+  }
 }
 
 hipError_t launch_correction(CacheLayer cache, const float *mu_k, const float *mu_v,
@@ -461,7 +494,7 @@ hipError_t launch_correction(CacheLayer cache, const float *mu_k, const float *m
                              int rope_rows, void *k_corr, void *v_corr, int out_dtype,
                              hipStream_t s) {
   const int4 *m4 = reinterpret_cast<const int4 *>(meta);
-  const long long threads = (long long)t_all * hkv * (hd / 16);
+  const long long threads = ((long long)t_all + CORR_T - 1) / CORR_T * hkv * (hd / 16);
   if (threads == 0) return hipSuccess;
   dim3 g((unsigned)((threads + 255) / 256)), b(256);
   const float2 *r = reinterpret_cast<const float2 *>(rope);
