@@ -21,11 +21,14 @@ namespace akvs {
 __device__ __forceinline__ int vt_col(int r, int g) { return (g ^ ((r ^ (r >> 3)) & 15)) * 4; }
 
 // Block shape for G query heads per KV head: heads per block gh (G split into G / gh
-// groups, gh <= 8) and 32-row blocks per block nrb, so that 4 <= gh * nrb <= 8 waves.
+// groups) and 32-row blocks per block nrb, 4 <= gh * nrb <= 8 waves, of which the first
+// four stage the K / V tiles. Heads of one KV head share a block (and its K / V tiles)
+// when that still gives two blocks per compute unit; with fewer rows (the recomputed
+// probe rows) each block takes one head and 128 rows, so that the blocks fill the GPU.
 struct AttnShape {
   int gh, n_groups, nrb;
 };
-static inline AttnShape attn_shape(int G) {
+static inline AttnShape attn_shape(int G, int rows, int hkv) {
   AttnShape a{0, 0, 0};
   if (G < 1) return a;
   int n = (G + 7) / 8;
@@ -33,6 +36,12 @@ static inline AttnShape attn_shape(int G) {
   a.n_groups = n;
   a.gh = G / n;
   a.nrb = 8 / a.gh < 4 ? 8 / a.gh : 4;
+  const long long blocks = (long long)((rows + 32 * a.nrb - 1) / (32 * a.nrb)) * hkv * n;
+  if (blocks < 512) {
+    a.gh = 1;
+    a.n_groups = G;
+    a.nrb = 4;
+  }
   return a;
 }
 
@@ -58,8 +67,9 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
   constexpr int KST = HD + 8;          // K tile row stride (bf16)
   constexpr int VST = 64;              // V^T tile row stride (bf16), swizzled by vt_col
   constexpr int CPK = HD / 8;          // 16-byte chunks per key row
-  constexpr int KCH = 64 * CPK / 256;  // K chunks per loading thread
-  constexpr int VKEYS = CPK / 4;       // keys per loading thread in the V transpose
+  constexpr int LT = 256;              // loading threads (waves 0-3)
+  constexpr int KCH = 64 * CPK / LT;   // K chunks per loading thread
+  constexpr int VKEYS = 64 * CPK / LT; // keys per loading thread in the V transpose
   constexpr int KBUF = 64 * KST, VBUF = HD * VST;
   __shared__ __attribute__((aligned(16))) bf16_t Ks[2 * KBUF];
   __shared__ __attribute__((aligned(16))) bf16_t Vt[2 * VBUF];
@@ -133,7 +143,7 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
 #define AKVS_KV_LOAD(KEY0)                                                                  \
   {                                                                                         \
     _Pragma("unroll") for (int i = 0; i < KCH; ++i) {                                       \
-      const int c = tid + 256 * i, kr = c / CPK, e0 = (c - kr * CPK) * 8;                   \
+      const int c = tid + LT * i, kr = c / CPK, e0 = (c - kr * CPK) * 8;                    \
       const int key = min((KEY0) + kr, klast);                                              \
       kreg[i] = *reinterpret_cast<const u32x4_t *>(Kc + ((size_t)key * hkv + kvh) * HD + e0); \
     }                                                                                       \
@@ -147,19 +157,22 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
     bf16_t *ks_ = Ks + (BUFI) * KBUF;                                                       \
     bf16_t *vt_ = Vt + (BUFI) * VBUF;                                                       \
     _Pragma("unroll") for (int i = 0; i < KCH; ++i) {                                       \
-      const int c = tid + 256 * i, kr = c / CPK, e0 = (c - kr * CPK) * 8;                   \
+      const int c = tid + LT * i, kr = c / CPK, e0 = (c - kr * CPK) * 8;                    \
       *reinterpret_cast<u32x4_t *>(ks_ + kr * KST + e0) = kreg[i];                          \
     }                                                                                       \
     _Pragma("unroll") for (int d = 0; d < 8; ++d) {                                         \
       const int word = d >> 1;                                                              \
       const bool hi_ = (d & 1) != 0;                                                        \
-      if (VKEYS == 4) {                                                                     \
-        const uint32_t a0 = vreg[0][word], a1 = vreg[1][word];                              \
-        const uint32_t a2 = vreg[VKEYS > 2 ? 2 : 0][word], a3 = vreg[VKEYS > 3 ? 3 : 0][word]; \
-        uint2 v2;                                                                           \
-        v2.x = hi_ ? ((a0 >> 16) | (a1 & 0xffff0000u)) : ((a0 & 0xffffu) | (a1 << 16));    \
-        v2.y = hi_ ? ((a2 >> 16) | (a3 & 0xffff0000u)) : ((a2 & 0xffffu) | (a3 << 16));    \
-        *reinterpret_cast<uint2 *>(vt_ + (ve0 + d) * VST + vt_col(ve0 + d, vkg)) = v2;     \
+      if (VKEYS >= 4) {                                                                     \
+        _Pragma("unroll") for (int qd = 0; qd < VKEYS / 4; ++qd) {                         \
+          const uint32_t a0 = vreg[4 * qd][word], a1 = vreg[4 * qd + 1][word];              \
+          const uint32_t a2 = vreg[4 * qd + 2][word], a3 = vreg[4 * qd + 3][word];          \
+          uint2 v2;                                                                         \
+          v2.x = hi_ ? ((a0 >> 16) | (a1 & 0xffff0000u)) : ((a0 & 0xffffu) | (a1 << 16));  \
+          v2.y = hi_ ? ((a2 >> 16) | (a3 & 0xffff0000u)) : ((a2 & 0xffffu) | (a3 << 16));  \
+          *reinterpret_cast<uint2 *>(vt_ + (ve0 + d) * VST +                                \
+                                     vt_col(ve0 + d, vkg * (VKEYS / 4) + qd)) = v2;         \
+        }                                                                                   \
       } else {                                                                              \
         const uint32_t a0 = vreg[0][word], a1 = vreg[VKEYS > 1 ? 1 : 0][word];              \
         *reinterpret_cast<uint32_t *>(vt_ + (ve0 + d) * VST + vt_col(ve0 + d, vkg >> 1) +     \
@@ -362,11 +375,12 @@ __global__ __launch_bounds__(64) void k_attn_f32(const float *__restrict__ Q, co
 }
 
 int attn_splits(int rows, int hq, int hkv, int n_keys) {
-  const AttnShape a = attn_shape(hq / hkv);
+  const AttnShape a = attn_shape(hq / hkv, rows, hkv);
   if (a.gh == 0 || rows <= 0) return 1;
   const int rb = 32 * a.nrb;
   const long long base = (long long)((rows + rb - 1) / rb) * hkv * a.n_groups;
-  long long sp = (512 + base - 1) / base;           // aim at ~512 blocks
+  if (base >= 512) return 1;                        // two blocks per compute unit already
+  long long sp = (768 + base - 1) / base;           // else aim at ~768 blocks (measured)
   const long long cap = (n_keys + 255) / 256;        // at least 256 keys per split
   if (sp > cap) sp = cap;
   if (sp > 64) sp = 64;
@@ -389,7 +403,7 @@ hipError_t launch_attention(const void *q, const int32_t *pos, int pos0, int row
     const bf16_t *K = reinterpret_cast<const bf16_t *>(k);
     const bf16_t *V = reinterpret_cast<const bf16_t *>(v);
     bf16_t *O = reinterpret_cast<bf16_t *>(out);
-    const AttnShape a = attn_shape(hq / hkv);
+    const AttnShape a = attn_shape(hq / hkv, rows, hkv);
     if (a.gh == 0) return hipErrorInvalidValue;
     const int rb = 32 * a.nrb;
     const int n_tiles = (rows + rb - 1) / rb;
