@@ -15,10 +15,14 @@
 
 namespace akvs {
 
-// Column (bf16 element) of key group g (4 keys) in row r of the V^T tile (rows of 64
-// elements, no padding). The XOR swizzle makes every 16-lane pass of both the transposed
-// 8-byte writes and the 8-byte fragment reads touch 32 distinct 4-byte banks.
-__device__ __forceinline__ int vt_col(int r, int g) { return (g ^ ((r ^ (r >> 3)) & 15)) * 4; }
+// V^T tile: row r = head dim, 64 keys in 16 groups of 4 (8 bytes), rows padded to 72
+// elements (144 bytes, a 4-bank shift per row). Group g of row r sits at column
+// (g ^ ((r >> 3) & 1)) * 4: the one-bit swizzle separates rows r and r + 8, so 16 lanes
+// reading 16 consecutive rows at one group, or writing 16 groups of one row, touch 32
+// distinct banks; and since it only flips bit 0 of the group, a lane's reads of groups
+// 4t + c (c < 4) are one base address plus compile-time offsets.
+constexpr int VT_ST = 72;
+__device__ __forceinline__ int vt_col(int r, int g) { return (g ^ ((r >> 3) & 1)) * 4; }
 
 // Block shape for G query heads per KV head: heads per block gh (G split into G / gh
 // groups) and 32-row blocks per block nrb, 4 <= gh * nrb <= 8 waves, of which the first
@@ -65,11 +69,12 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
   constexpr int KS = HD / 16;          // contraction steps of S
   constexpr int DB = HD / 32;          // 32-wide head-dim blocks of O
   constexpr int KST = HD + 8;          // K tile row stride (bf16)
-  constexpr int VST = 64;              // V^T tile row stride (bf16), swizzled by vt_col
+  constexpr int VST = VT_ST;           // V^T tile row stride (bf16), swizzled by vt_col
   constexpr int CPK = HD / 8;          // 16-byte chunks per key row
   constexpr int LT = 256;              // loading threads (waves 0-3)
   constexpr int KCH = 64 * CPK / LT;   // K chunks per loading thread
   constexpr int VKEYS = 64 * CPK / LT; // keys per loading thread in the V transpose
+  constexpr int VQ = 64 / VKEYS;       // key groups per tile in the V transpose
   constexpr int KBUF = 64 * KST, VBUF = HD * VST;
   __shared__ __attribute__((aligned(16))) bf16_t Ks[2 * KBUF];
   __shared__ __attribute__((aligned(16))) bf16_t Vt[2 * VBUF];
@@ -138,8 +143,10 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
   // One K / V tile in the loading waves' registers. Keys past kv_end are clamped to the
   // last key: finite data that the score mask gives probability 0.
   u32x4_t kreg[KCH], vreg[VKEYS];
-  const int vkg = tid / CPK, ve0 = (tid - vkg * CPK) * 8;  // V: keys vkg*VKEYS.., dims ve0..
+  // V: keys vkg*VKEYS.., dims ve0..; the 16 (32) lanes of an LDS write phase share ve0
+  const int vkg = tid % VQ, ve0 = (tid / VQ) * 8;
   const int klast = kv_end - 1;
+  const int vsw = (hi ^ (((lane & 31) >> 3) & 1)) * 4;  // this lane's swizzled column offset
 #define AKVS_KV_LOAD(KEY0)                                                                  \
   {                                                                                         \
     _Pragma("unroll") for (int i = 0; i < KCH; ++i) {                                       \
@@ -243,13 +250,12 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
           for (int j = 0; j < 4; ++j) pw[j] = pack_bf2(pv[8 * t + 2 * j], pv[8 * t + 2 * j + 1]);
           bf16x8_t pb;
           __builtin_memcpy(&pb, pw, 16);
-          const int kg = st * 8 + 4 * t + hi;  // key groups kg and kg + 2 of the tile
 #pragma unroll
           for (int db = 0; db < DB; ++db) {
-            const int vr = db * 32 + (lane & 31);
-            const bf16_t *vrow = vt_ + vr * VST;
-            const uint2 x0 = *reinterpret_cast<const uint2 *>(vrow + vt_col(vr, kg));
-            const uint2 x1 = *reinterpret_cast<const uint2 *>(vrow + vt_col(vr, kg + 2));
+            // groups kg and kg + 2 of row db*32 + lane%32: vt_col = (st*8 + 4t (+2)) * 4 + vsw
+            const bf16_t *vrow = vt_ + (db * 32 + (lane & 31)) * VST + vsw;
+            const uint2 x0 = *reinterpret_cast<const uint2 *>(vrow + (st * 8 + 4 * t) * 4);
+            const uint2 x1 = *reinterpret_cast<const uint2 *>(vrow + (st * 8 + 4 * t + 2) * 4);
             uint32_t vw[4] = {x0.x, x0.y, x1.x, x1.y};
             bf16x8_t va;
             __builtin_memcpy(&va, vw, 16);
