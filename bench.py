@@ -8,8 +8,10 @@ by the library's own full prefill of each unit at position 0 (not timed).
 
 Prints one JSON line: reuse-prefill tokens/s, the full-prefill baseline on the same
 tokens and the speedup, the roofline figure of the dominant kernel (the bf16 MFMA GEMM,
-timed with HIP events on its launch stream during the timed steps) and the CPU oracle
-timed on a bounded sample of the same workload.
+timed with HIP events on its launch stream during the timed eager steps) and the CPU
+oracle timed on a bounded sample of the same workload. The headline step time is the
+whole call replayed from a HIP graph (every kernel runs; only the host launch overhead
+of ~300 launches per step is gone); the eager time is reported beside it.
 """
 from __future__ import annotations
 
@@ -41,6 +43,7 @@ def parse():
     p.add_argument("--seed", type=int, default=0)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-full", action="store_true", help="skip the full-prefill baseline leg")
+    p.add_argument("--no-graph", action="store_true", help="skip the graph-replay leg")
     p.add_argument("--random-caches", action="store_true",
                    help="unit caches drawn at random instead of prefilled (counter runs)")
     p.add_argument("--calibrate-copy", action="store_true",
@@ -313,41 +316,61 @@ def main():
     print(f"# reuse: {ms_step:.3f} ms/step (wall {1e3 * wall / args.steps:.3f}), M={m_rows}",
           file=sys.stderr, flush=True)
 
-    # full-prefill baseline on the same tokens (same kernels)
-    ms_full = None
-    if not args.no_full:
-        eng.full_prefill(toks, want_h=True)
+    def timed(fn):
         for _ in range(args.warmup):
-            eng.full_prefill(toks, want_h=True)
+            fn()
         torch.cuda.synchronize()
         t0.record(stream)
         for _ in range(args.steps):
-            eng.full_prefill(toks, want_h=True)
+            fn()
         t1.record(stream)
         torch.cuda.synchronize()
-        ms_full = t0.elapsed_time(t1) / args.steps
+        return t0.elapsed_time(t1) / args.steps
+
+    # The same calls replayed from HIP graphs (the launch overhead of ~300 kernels per step
+    # removed): the headline figures. The eager timings above give the per-kernel events.
+    from paper_2607_21604_amd.runtime import ReuseGraph, FullGraph
+    ms_graph = None
+    if not args.no_graph:
+        rg = ReuseGraph(eng, toks, wl.chunk_lens, wl.query_len, k_cache, v_cache, (num, den),
+                        args.check_layer, 0, **qkw)
+        ms_graph = timed(rg.replay)
+        print(f"# reuse (graph replay): {ms_graph:.3f} ms/step", file=sys.stderr, flush=True)
+        del rg
+
+    # full-prefill baseline on the same tokens (same kernels)
+    ms_full = ms_full_graph = None
+    if not args.no_full:
+        eng.full_prefill(toks, want_h=True)
+        ms_full = timed(lambda: eng.full_prefill(toks, want_h=True))
         print(f"# full prefill: {ms_full:.3f} ms/step", file=sys.stderr, flush=True)
+        if not args.no_graph:
+            fg = FullGraph(eng, toks)
+            ms_full_graph = timed(fg.replay)
+            print(f"# full prefill (graph replay): {ms_full_graph:.3f} ms/step", file=sys.stderr,
+                  flush=True)
+            del fg
 
     sweep = {}
     extra = args.refresh_sweep
     if extra == "auto":
         extra = {"3b": "1/10,3/10", "32b": "1/10,3/10"}.get(wl.name, "none")
+    full_ref = ms_full_graph or ms_full
     for r in ([] if extra == "none" else extra.split(",")):
         rn, rd = (int(x) for x in r.split("/"))
-        o2 = reuse(refresh=(rn, rd))
-        for _ in range(args.warmup):
-            reuse(o2, refresh=(rn, rd))
-        torch.cuda.synchronize()
-        t0.record(stream)
-        for _ in range(args.steps):
-            reuse(o2, refresh=(rn, rd))
-        t1.record(stream)
-        torch.cuda.synchronize()
-        ms_r = t0.elapsed_time(t1) / args.steps
+        if args.no_graph:
+            o2 = reuse(refresh=(rn, rd))
+            ms_r = timed(lambda: reuse(o2, refresh=(rn, rd)))
+        else:
+            rg = ReuseGraph(eng, toks, wl.chunk_lens, wl.query_len, k_cache, v_cache, (rn, rd),
+                            args.check_layer, 0, **qkw)
+            o2 = rg.out
+            ms_r = timed(rg.replay)
+            del rg
         m_r = int(o2["n_rows"].item())
         sweep[f"{rn}/{rd}"] = {"tokens_per_s": wl.n_tokens / (ms_r * 1e-3), "ms_per_step": ms_r,
                                "recomputed_rows": m_r,
-                               "speedup_vs_full_prefill": ms_full / ms_r if ms_full else None}
+                               "speedup_vs_full_prefill": full_ref / ms_r if full_ref else None}
         print(f"# reuse at r={rn}/{rd}: {ms_r:.3f} ms/step, M={m_r}", file=sys.stderr, flush=True)
         del o2
 
@@ -384,10 +407,12 @@ def main():
         print("# timing the CPU oracle sample", file=sys.stderr, flush=True)
         cpu = cpu_baseline(wl, (num, den), args.check_layer, args.seed, m_rows)
     T = wl.n_tokens
+    ms_head = ms_graph or ms_step
+    full_head = ms_full_graph or ms_full
     line = {
         "metric": "reuse-prefill tokens/s at 20% refresh + speedup vs full prefill, 1 GPU",
-        "value": T / (ms_step * 1e-3), "unit": "tokens/s", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
+        "value": T / (ms_head * 1e-3), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_head,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic: uniform token ids, N(0,0.02^2) random-init weights, unit caches "
                 "from the library's standalone prefill of each unit",
@@ -398,9 +423,12 @@ def main():
                    "tokens": T, "context_tokens": wl.n_ctx, "query_tokens": wl.query_len,
                    "refresh": f"{num}/{den}", "check_layer": args.check_layer,
                    "recomputed_rows": m_rows, "recomputed_fraction": m_rows / T},
-        "speedup_vs_full_prefill": ms_full / ms_step if ms_full else None,
-        "full_prefill_tokens_per_s": T / (ms_full * 1e-3) if ms_full else None,
-        "ms_full_prefill": ms_full,
+        "timing": "HIP-graph replay of the whole call" if ms_graph else "eager calls",
+        "ms_per_step_eager": ms_step,
+        "speedup_vs_full_prefill": full_head / ms_head if full_head else None,
+        "full_prefill_tokens_per_s": T / (full_head * 1e-3) if full_head else None,
+        "ms_full_prefill": full_head,
+        "ms_full_prefill_eager": ms_full,
         "roofline": roofline,
         "kernels": kernels,
         "refresh_sweep": sweep,

@@ -105,3 +105,44 @@ def quantize_cache(x: torch.Tensor, bits: int):
     meta = torch.empty(x.shape[:-1] + (hd // 64, 2), dtype=torch.float16, device=x.device)
     akvs.akvs_quantize_cache(x.contiguous(), rows, hd, bits, codes, meta)
     return codes, meta
+
+
+class ReuseGraph:
+    """One reuse-prefill call captured in a HIP graph (torch.cuda.CUDAGraph).
+
+    The call is made once eagerly (which sizes the workspace and allocates the outputs),
+    then captured; replay() reruns every kernel on the same buffers, so new token ids or
+    cache contents are written into the captured tensors in place. The library's calls
+    are capture-safe: kernel launches only (host tables travel as kernel arguments), no
+    allocation, copy, memset or synchronisation. Kernel timing (akvs_profile_enable) must
+    be off while capturing."""
+
+    def __init__(self, engine: Engine, *args, **kw):
+        kw.pop("outputs", None)
+        self.out = engine.reuse_prefill(*args, **kw)
+        torch.cuda.synchronize(engine.device)
+        self.graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(self.graph):
+            engine.reuse_prefill(*args, outputs=self.out, **kw)
+        torch.cuda.synchronize(engine.device)
+
+    def replay(self):
+        self.graph.replay()
+        return self.out
+
+
+class FullGraph:
+    """akvs_full_prefill over fixed token buffers captured in a HIP graph (the baseline
+    counterpart of ReuseGraph); the outputs live in the graph's memory pool."""
+
+    def __init__(self, engine: Engine, tokens: torch.Tensor, pos0: int = 0, want_h: bool = True):
+        engine.full_prefill(tokens, pos0, want_h)  # sizes the workspace
+        torch.cuda.synchronize(engine.device)
+        self.graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(self.graph):
+            self.out = engine.full_prefill(tokens, pos0, want_h)
+        torch.cuda.synchronize(engine.device)
+
+    def replay(self):
+        self.graph.replay()
+        return self.out
