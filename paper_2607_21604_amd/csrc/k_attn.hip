@@ -297,31 +297,53 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
 }
 
 // Merge of the key splits of one (row, head): weights 2^(m_s - max m), fixed split order.
+// Thread = 4 consecutive head dims of one (row, head); the (m, l) pairs and the partial
+// outputs of four splits are requested at a time.
 __global__ __launch_bounds__(256) void k_attn_combine(const float *__restrict__ part_o,
                                                       const float *__restrict__ part_ml,
                                                       int n_splits, int rows,
                                                       const int32_t *rows_dev, int hq, int hd,
                                                       bf16_t *__restrict__ out) {
-  const int item = blockIdx.x * 4 + (threadIdx.x >> 6);  // (row, head), one wave each
-  const int lane = threadIdx.x & 63;
+  const int per = hd >> 2;  // threads per (row, head)
+  const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  const long long item = gid / per;
+  const int e0 = (int)(gid - item * per) * 4;
   int R = rows;
   if (rows_dev) R = min(R, *rows_dev);
-  if (item >= R * hq) return;
+  if (item >= (long long)R * hq) return;
+  const size_t stride = (size_t)rows * hq;  // items per split
   float mx = -INFINITY;
-  for (int sp = 0; sp < n_splits; ++sp) mx = fmaxf(mx, part_ml[2 * ((size_t)sp * rows * hq + item)]);
+  for (int sp = 0; sp < n_splits; ++sp) mx = fmaxf(mx, part_ml[2 * (sp * stride + item)]);
   const float moff = mx == -INFINITY ? 0.f : mx;
-  float l = 0.f, a0 = 0.f, a1 = 0.f;
-  for (int sp = 0; sp < n_splits; ++sp) {
-    const size_t pi = (size_t)sp * rows * hq + item;
-    const float w = exp2f(part_ml[2 * pi] - moff);
-    l += w * part_ml[2 * pi + 1];
-    const float *po = part_o + pi * hd;
-    a0 += w * po[lane];
-    if (hd > 64) a1 += w * po[lane + 64];
+  float l = 0.f;
+  float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
+  int sp = 0;
+  for (; sp + 4 <= n_splits; sp += 4) {
+    float2 ml[4];
+    float4 o[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const size_t pi = (sp + u) * stride + item;
+      ml[u] = *reinterpret_cast<const float2 *>(part_ml + 2 * pi);
+      o[u] = *reinterpret_cast<const float4 *>(part_o + pi * hd + e0);
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const float w = exp2f(ml[u].x - moff);
+      l += w * ml[u].y;
+      a.x += w * o[u].x; a.y += w * o[u].y; a.z += w * o[u].z; a.w += w * o[u].w;
+    }
+  }
+  for (; sp < n_splits; ++sp) {
+    const size_t pi = sp * stride + item;
+    const float2 ml = *reinterpret_cast<const float2 *>(part_ml + 2 * pi);
+    const float4 o = *reinterpret_cast<const float4 *>(part_o + pi * hd + e0);
+    const float w = exp2f(ml.x - moff);
+    l += w * ml.y;
+    a.x += w * o.x; a.y += w * o.y; a.z += w * o.z; a.w += w * o.w;
   }
   const float inv = 1.0f / l;
-  out[(size_t)item * hd + lane] = f2bf(a0 * inv);
-  if (hd > 64) out[(size_t)item * hd + lane + 64] = f2bf(a1 * inv);
+  store4(out + item * hd + e0, a.x * inv, a.y * inv, a.z * inv, a.w * inv);
 }
 
 // fp32 path (small models): one wave per (row, head), keys in tiles of 64, online softmax.
@@ -427,8 +449,8 @@ hipError_t launch_attention(const void *q, const int32_t *pos, int pos0, int row
     if (n_splits > 1) {
       hipError_t e = hipGetLastError();
       if (e != hipSuccess) return e;
-      const long long items = (long long)rows * hq;
-      hipLaunchKernelGGL(k_attn_combine, dim3((unsigned)((items + 3) / 4)), dim3(256), 0, s,
+      const long long threads = (long long)rows * hq * (hd / 4);
+      hipLaunchKernelGGL(k_attn_combine, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, s,
                          part_o, part_ml, n_splits, rows, rows_dev, hq, hd, O);
     }
   } else {
