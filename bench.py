@@ -39,6 +39,9 @@ def parse():
     p.add_argument("--refresh-sweep", default="auto",
                    help="extra refresh ratios timed after the headline one, comma separated "
                         "('auto': the workload's listed ratios, 'none': skip)")
+    p.add_argument("--batch-sweep", default="auto",
+                   help="comma-separated batch sizes for the batched reuse prefill leg "
+                        "(auto: 4,8 for 3b; none elsewhere)")
     p.add_argument("--check-layer", type=int, default=1)
     p.add_argument("--seed", type=int, default=0)
     p.add_argument("--no-cpu-baseline", action="store_true")
@@ -376,6 +379,40 @@ def main():
         print(f"# reuse at r={rn}/{rd}: {ms_r:.3f} ms/step, M={m_r}", file=sys.stderr, flush=True)
         del o2
 
+    # batched reuse prefill: B requests of this workload's shape (same unit lengths, their
+    # own token ids and unit caches) in one call, whose projections run over all requests'
+    # recomputed rows at once
+    batch = {}
+    bs = args.batch_sweep
+    if bs == "auto":
+        bs = {"3b": "4,8"}.get(wl.name, "none")
+    if bs != "none" and wl.cache_bits == 16 and not args.random_caches:
+        from paper_2607_21604_amd.runtime import BatchGraph, reuse_prefill_batch
+        sizes = [int(x) for x in bs.split(",")]
+        reqs = [{"tokens": toks, "chunk_lens": wl.chunk_lens, "query_len": wl.query_len,
+                 "k_cache": k_cache, "v_cache": v_cache}]
+        for i in range(1, max(sizes)):
+            ti = torch.tensor(synthetic.make_tokens(wl.n_tokens, shape.vocab, args.seed + 100 + i),
+                              dtype=torch.int32, device=dev)
+            ki, vi = eng.cache_units(ti, wl.chunk_lens)
+            reqs.append({"tokens": ti, "chunk_lens": wl.chunk_lens, "query_len": wl.query_len,
+                         "k_cache": ki, "v_cache": vi})
+        one = ms_graph or ms_step
+        for B in sizes:
+            if args.no_graph:
+                ob = reuse_prefill_batch(eng, reqs[:B], (num, den), args.check_layer, 0)
+                ms_b = timed(lambda: reuse_prefill_batch(eng, reqs[:B], (num, den),
+                                                         args.check_layer, 0, outputs=ob))
+            else:
+                bg = BatchGraph(eng, reqs[:B], (num, den), args.check_layer, 0)
+                ms_b = timed(bg.replay)
+                del bg
+            batch[str(B)] = {"tokens_per_s": B * wl.n_tokens / (ms_b * 1e-3), "ms_per_step": ms_b,
+                             "throughput_vs_single": B * one / ms_b}
+            print(f"# batch of {B}: {ms_b:.3f} ms/step ({B * one / ms_b:.2f}x the one-request "
+                  f"rate)", file=sys.stderr, flush=True)
+        del reqs
+
     flops_step = gemm_flops(shape, wl.n_tokens, wl.n_ctx, m_rows, args.check_layer)
     achieved = flops_step * args.steps / (g_ms * 1e-3) / 1e12 if g_ms > 0 else None
     per_launch = flops_step * args.steps / max(g_launches, 1)
@@ -434,6 +471,7 @@ def main():
         "roofline": roofline,
         "kernels": kernels,
         "refresh_sweep": sweep,
+        "batch_sweep": batch,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line))

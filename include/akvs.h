@@ -258,6 +258,25 @@ akvs_status akvs_reuse_prefill(const int32_t *tokens, const void *embed, const a
                                const akvs_reuse_out *out, void *ws, size_t ws_bytes,
                                hipStream_t stream);
 
+/* Batched reuse prefill (the paper's batch axis, Sec. 4.4 / Table 3: B requests served
+ * together). Request b is exactly the call akvs_reuse_prefill(tokens[b], ..., &cfgs[b],
+ * &caches[b], &outs[b]) — its own units, query, unit caches, outputs and probe sets —
+ * but from the check layer on the recomputed rows of all requests form one row block,
+ * so every projection GEMM reads its weights once per layer for the whole batch;
+ * offsets, correction and attention stay per request. tokens, cfgs, caches and outs are
+ * host arrays of `batch` entries (device pointers inside, as for akvs_reuse_prefill).
+ * Every cfg must use the same check_layer and AKVS_F_NO_PREFIX_RECOMPUTE setting
+ * (AKVS_EINVAL otherwise). ws: akvs_batch_workspace_size bytes. */
+akvs_status akvs_reuse_prefill_batch(const int32_t *const *tokens, int32_t batch,
+                                     const void *embed, const akvs_layer_w *lw,
+                                     const void *final_norm, const akvs_model_cfg *m,
+                                     const akvs_reuse_cfg *cfgs, const akvs_cache *caches,
+                                     const akvs_reuse_out *outs, void *ws, size_t ws_bytes,
+                                     hipStream_t stream);
+/* Workspace bytes of akvs_reuse_prefill_batch (0 for an invalid configuration). */
+size_t akvs_batch_workspace_size(const akvs_model_cfg *m, const akvs_reuse_cfg *cfgs,
+                                 int32_t batch);
+
 /* Full prefill (the no-reuse baseline; also the standalone caching of a unit with
  * pos0 = 0, Sec. 3.1). tokens: device [n] ids at positions pos0..pos0+n-1. h_out:
  * [n][D] fp32 final-normed hidden states (may be NULL); k_out, v_out: [L][n][Hkv][hd]

@@ -100,6 +100,12 @@ _SIGS = {
     "akvs_reuse_prefill": (_I, [_P, _P, ctypes.POINTER(LayerW), _P, ctypes.POINTER(ModelCfg),
                                 ctypes.POINTER(ReuseCfg), ctypes.POINTER(Cache),
                                 ctypes.POINTER(ReuseOut), _P, ctypes.c_size_t, _P]),
+    "akvs_reuse_prefill_batch": (_I, [ctypes.POINTER(ctypes.c_void_p), _I, _P,
+                                      ctypes.POINTER(LayerW), _P, ctypes.POINTER(ModelCfg),
+                                      ctypes.POINTER(ReuseCfg), ctypes.POINTER(Cache),
+                                      ctypes.POINTER(ReuseOut), _P, ctypes.c_size_t, _P]),
+    "akvs_batch_workspace_size": (ctypes.c_size_t, [ctypes.POINTER(ModelCfg),
+                                                    ctypes.POINTER(ReuseCfg), _I]),
     "akvs_full_prefill": (_I, [_P, _I, _I, _P, ctypes.POINTER(LayerW), _P, ctypes.POINTER(ModelCfg),
                                _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "akvs_profile_enable": (_I, [_I]),
@@ -296,6 +302,32 @@ def akvs_reuse_prefill(tokens, embed, layers: ctypes.Array, final_norm, m: Model
                                      ctypes.byref(m), ctypes.byref(cfg), ctypes.byref(cache),
                                      ctypes.byref(out), ptr(ws), ws.numel() * ws.element_size(),
                                      stream_handle(stream)), "akvs_reuse_prefill")
+
+
+def batch_arrays(cfgs, caches, outs):
+    """ctypes arrays of per-request descriptors; they keep the descriptors (and what those
+    keep alive) referenced."""
+    n = len(cfgs)
+    ca = (ReuseCfg * n)(*cfgs)
+    cc = (Cache * n)(*caches)
+    co = (ReuseOut * n)(*outs)
+    ca._keep, cc._keep, co._keep = list(cfgs), list(caches), list(outs)
+    return ca, cc, co
+
+
+def akvs_batch_workspace_size(m: ModelCfg, cfgs: ctypes.Array, batch: int) -> int:
+    return load().akvs_batch_workspace_size(ctypes.byref(m), cfgs, int(batch))
+
+
+def akvs_reuse_prefill_batch(tokens, embed, layers: ctypes.Array, final_norm, m: ModelCfg,
+                             cfgs: ctypes.Array, caches: ctypes.Array, outs: ctypes.Array, ws,
+                             stream=None):
+    n = len(tokens)
+    tp = (ctypes.c_void_p * n)(*[ptr(t) for t in tokens])
+    _check(load().akvs_reuse_prefill_batch(tp, n, ptr(embed), layers, ptr(final_norm),
+                                           ctypes.byref(m), cfgs, caches, outs, ptr(ws),
+                                           ws.numel() * ws.element_size(), stream_handle(stream)),
+           "akvs_reuse_prefill_batch")
 
 
 def akvs_full_prefill(tokens, n_tokens, pos0, embed, layers: ctypes.Array, final_norm, m: ModelCfg,

@@ -250,6 +250,7 @@ struct Carver {
 struct LayerBufs {
   void *x, *q, *att, *act;  // model dtype
   float *part_o, *part_ml;  // attention key-split partials (bf16 models)
+  long long part_rows;      // splits x rows that part_o / part_ml hold
   float *gpart;             // GEMM K-split partials (bf16 models)
 };
 
@@ -266,11 +267,16 @@ size_t layer_gemm_part(const akvs_model_cfg *m, long long rows) {
   return w;
 }
 
-// rows: the largest row count a layer pass uses; attn_rows[0..1]: the row counts its
-// attention calls use over n_keys keys (for the key-split partials of bf16 models).
-void carve_layer_bufs(Carver &cv, const akvs_model_cfg *m, long long rows, long long attn_rows0,
-                      long long attn_rows1, long long attn_rows2, long long n_keys,
-                      LayerBufs &b) {
+// One attention call of a layer pass: its row count and key count.
+struct AttnUse {
+  long long rows, n_keys;
+};
+
+// rows: the largest row count a layer pass uses; uses: the (rows, keys) of its attention
+// calls, which are also the row counts of its projections (sizing the GEMM K-split
+// partials and the attention key-split partials of bf16 models).
+void carve_layer_bufs(Carver &cv, const akvs_model_cfg *m, long long rows,
+                      const std::vector<AttnUse> &uses, LayerBufs &b) {
   const size_t es = es_of(m->dtype);
   b.x = cv.take<char>((size_t)rows * m->d_model * es);
   b.q = cv.take<char>((size_t)rows * m->n_q_heads * m->head_dim * es);
@@ -278,22 +284,21 @@ void carve_layer_bufs(Carver &cv, const akvs_model_cfg *m, long long rows, long 
   b.act = cv.take<char>((size_t)rows * m->ffn_dim * es);
   b.part_o = nullptr;
   b.part_ml = nullptr;
+  b.part_rows = 0;
   b.gpart = nullptr;
-  {
-    const size_t g = std::max(std::max(layer_gemm_part(m, attn_rows0), layer_gemm_part(m, attn_rows1)),
-                              layer_gemm_part(m, attn_rows2));
-    if (g) b.gpart = cv.take<float>(g);
+  size_t g = 0;
+  long long worst = 0;
+  for (const AttnUse &u : uses) {
+    g = std::max(g, layer_gemm_part(m, u.rows));
+    if (m->dtype != AKVS_BF16 || u.rows <= 0) continue;
+    const long long sp = attn_splits((int)u.rows, m->n_q_heads, m->n_kv_heads, (int)u.n_keys);
+    if (sp > 1 && sp * u.rows > worst) worst = sp * u.rows;
   }
-  if (m->dtype == AKVS_BF16) {
-    long long worst = 0;
-    for (long long r : {attn_rows0, attn_rows1, attn_rows2}) {
-      const long long sp = attn_splits((int)r, m->n_q_heads, m->n_kv_heads, (int)n_keys);
-      if (sp > 1 && sp * r > worst) worst = sp * r;
-    }
-    if (worst > 0) {
-      b.part_o = cv.take<float>((size_t)worst * m->n_q_heads * m->head_dim);
-      b.part_ml = cv.take<float>((size_t)worst * m->n_q_heads * 2);
-    }
+  if (g) b.gpart = cv.take<float>(g);
+  if (worst > 0) {
+    b.part_o = cv.take<float>((size_t)worst * m->n_q_heads * m->head_dim);
+    b.part_ml = cv.take<float>((size_t)worst * m->n_q_heads * 2);
+    b.part_rows = worst;
   }
 }
 
@@ -324,7 +329,7 @@ size_t carve_reuse(void *ws, const akvs_model_cfg *m, const akvs_reuse_cfg *c, c
   b.tok_delta = cv.take<int32_t>((size_t)Tc);
   b.tok_chunk = cv.take<int32_t>((size_t)Tc);
   b.h_full = cv.take<float>((size_t)T * m->d_model);
-  carve_layer_bufs(cv, m, T, T, cap, c->query_len, T, b.lb);
+  carve_layer_bufs(cv, m, T, {{T, T}, {cap, T}, {c->query_len, T}}, b.lb);
   b.k_chk = cv.take<char>((size_t)Tc * kvw * es);
   b.v_chk = cv.take<char>((size_t)Tc * kvw * es);
   b.d_k = cv.take<float>((size_t)Tc);
@@ -357,7 +362,7 @@ size_t carve_full(void *ws, const akvs_model_cfg *m, long long n, FullBufs &b) {
   Carver cv(ws);
   b.rope = cv.take<float>((size_t)n * m->head_dim);
   b.h = cv.take<float>((size_t)n * m->d_model);
-  carve_layer_bufs(cv, m, n, n, n, n, n, b.lb);
+  carve_layer_bufs(cv, m, n, {{n, n}}, b.lb);
   return cv.off;
 }
 
@@ -456,8 +461,135 @@ akvs_status full_layer(const akvs_model_cfg *m, const akvs_layer_w &w, float *h,
                                   stream, lb.gpart);
   LAUNCH(AKVS_K_ATTENTION, launch_attention(lb.q, nullptr, 0, n, nullptr, k_dst, v_dst, n,
                                             m->n_q_heads, m->n_kv_heads, m->head_dim, m->dtype,
-                                            lb.att, lb.part_o, lb.part_ml, stream));
+                                            lb.att, lb.part_o, lb.part_ml, lb.part_rows, stream));
   return out_mlp(m, w, h, n, nullptr, lb.att, lb.x, lb.act, lb.gpart, stream);
+}
+
+// ---- batched reuse prefill ---------------------------------------------------------------
+// Per request: its unit bookkeeping, selection and correction inputs. Shared: the buffers
+// of the per-request prefix layers and check layer (used one request after another), and
+// the combined row block of all requests' recomputed rows for the layers from the check
+// layer on, where request b owns rows row_off[b] .. row_off[b] + n_rows[b].
+struct BatchReq {
+  int32_t *meta, *tok_delta, *tok_chunk;
+  float *h_full;
+  float *d_k, *d_v, *w_k, *w_v;
+  uint8_t *flags;
+  int32_t *chunk_rows, *rows, *fresh_row, *probe_k, *probe_v;
+  float *mu_k, *mu_v;
+};
+
+struct BatchBufs {
+  float *rope;
+  LayerBufs lb_full;  // prefix / check layer of one request at a time
+  void *k_chk, *v_chk;
+  int32_t *n_rows, *row_off, *pos;  // [B], [B + 1], [sum caps]
+  float *h_probe;                   // [sum caps][D]
+  void *k_fresh, *v_fresh;          // [sum caps][kvw]
+  LayerBufs lb;                     // combined rows (x, q, att, act, partials)
+  float *h_last;                    // [sum q][D]
+  void *q_last;                     // [sum q][Hq hd]
+  std::vector<BatchReq> req;
+};
+
+struct BatchPlan {
+  std::vector<Meta> mt;
+  long long t_max = 0, tc_max = 0, cap_sum = 0, q_sum = 0, min_sum = 0;
+};
+
+size_t carve_batch(void *ws, const akvs_model_cfg *m, const akvs_reuse_cfg *cfgs, int B,
+                   const BatchPlan &pl, BatchBufs &b) {
+  Carver cv(ws);
+  const size_t es = es_of(m->dtype);
+  const int kvw = m->n_kv_heads * m->head_dim, hqw = m->n_q_heads * m->head_dim;
+  const int D = m->d_model;
+  b.rope = cv.take<float>((size_t)pl.t_max * m->head_dim);
+  {  // each request's prefix layers use the buffers the single-request call would
+    std::vector<AttnUse> uses;
+    for (int i = 0; i < B; ++i) uses.push_back({pl.mt[i].t_all, pl.mt[i].t_all});
+    carve_layer_bufs(cv, m, pl.t_max, uses, b.lb_full);
+  }
+  b.k_chk = cv.take<char>((size_t)pl.tc_max * kvw * es);
+  b.v_chk = cv.take<char>((size_t)pl.tc_max * kvw * es);
+  b.n_rows = cv.take<int32_t>((size_t)B);
+  b.row_off = cv.take<int32_t>((size_t)B + 1);
+  b.pos = cv.take<int32_t>((size_t)pl.cap_sum);
+  b.h_probe = cv.take<float>((size_t)pl.cap_sum * D);
+  b.k_fresh = cv.take<char>((size_t)pl.cap_sum * kvw * es);
+  b.v_fresh = cv.take<char>((size_t)pl.cap_sum * kvw * es);
+  // combined row buffers; the attention partials are sized for the largest request call
+  b.lb.x = cv.take<char>((size_t)pl.cap_sum * D * es);
+  b.lb.q = cv.take<char>((size_t)pl.cap_sum * hqw * es);
+  b.lb.att = cv.take<char>((size_t)pl.cap_sum * hqw * es);
+  b.lb.act = cv.take<char>((size_t)pl.cap_sum * m->ffn_dim * es);
+  b.lb.gpart = nullptr;
+  b.lb.part_o = b.lb.part_ml = nullptr;
+  b.lb.part_rows = 0;
+  {
+    const size_t g = std::max(layer_gemm_part(m, pl.cap_sum), layer_gemm_part(m, pl.q_sum));
+    if (g) b.lb.gpart = cv.take<float>(g);
+  }
+  if (m->dtype == AKVS_BF16) {  // attention runs per request: its largest split partials
+    long long worst = 0;
+    for (int i = 0; i < B; ++i) {
+      for (long long r : {pl.mt[i].row_cap, (long long)cfgs[i].query_len}) {
+        const long long sp = attn_splits((int)r, m->n_q_heads, m->n_kv_heads, (int)pl.mt[i].t_all);
+        if (sp > 1 && sp * r > worst) worst = sp * r;
+      }
+    }
+    if (worst > 0) {
+      b.lb.part_o = cv.take<float>((size_t)worst * hqw);
+      b.lb.part_ml = cv.take<float>((size_t)worst * m->n_q_heads * 2);
+      b.lb.part_rows = worst;
+    }
+  }
+  b.h_last = cv.take<float>((size_t)pl.q_sum * D);
+  b.q_last = cv.take<char>((size_t)pl.q_sum * hqw * es);
+  b.req.resize(B);
+  for (int i = 0; i < B; ++i) {
+    const Meta &mt = pl.mt[i];
+    BatchReq &r = b.req[i];
+    const int nch = cfgs[i].n_chunks;
+    r.meta = cv.take<int32_t>((size_t)nch * 4);
+    r.tok_delta = cv.take<int32_t>((size_t)mt.t_ctx);
+    r.tok_chunk = cv.take<int32_t>((size_t)mt.t_ctx);
+    r.h_full = cv.take<float>((size_t)mt.t_all * D);
+    r.d_k = cv.take<float>((size_t)mt.t_ctx);
+    r.d_v = cv.take<float>((size_t)mt.t_ctx);
+    r.w_k = cv.take<float>((size_t)mt.t_ctx);
+    r.w_v = cv.take<float>((size_t)mt.t_ctx);
+    r.flags = cv.take<uint8_t>((size_t)mt.t_ctx);
+    r.chunk_rows = cv.take<int32_t>((size_t)nch);
+    r.rows = cv.take<int32_t>((size_t)mt.t_all);
+    r.fresh_row = cv.take<int32_t>((size_t)mt.t_all);
+    r.probe_k = cv.take<int32_t>((size_t)mt.sum_b + 1);
+    r.probe_v = cv.take<int32_t>((size_t)mt.sum_b + 1);
+    r.mu_k = cv.take<float>((size_t)nch * kvw);
+    r.mu_v = cv.take<float>((size_t)nch * kvw);
+  }
+  return cv.off;
+}
+
+akvs_status batch_plan(const akvs_model_cfg *m, const akvs_reuse_cfg *cfgs, int B,
+                       BatchPlan *pl) {
+  REQUIRE(B >= 1 && B <= 1024, AKVS_EINVAL, "batch %d outside [1, 1024]", B);
+  REQUIRE(cfgs, AKVS_EINVAL, "cfgs is NULL");
+  pl->mt.assign(B, Meta());
+  for (int i = 0; i < B; ++i) {
+    akvs_status st = check_reuse(&cfgs[i], m->n_layers, &pl->mt[i]);
+    if (st) return st;
+    REQUIRE(cfgs[i].check_layer == cfgs[0].check_layer &&
+                (cfgs[i].flags & AKVS_F_NO_PREFIX_RECOMPUTE) ==
+                    (cfgs[0].flags & AKVS_F_NO_PREFIX_RECOMPUTE),
+            AKVS_EINVAL, "request %d: every request needs the same check layer and prefix mode", i);
+    pl->t_max = std::max(pl->t_max, pl->mt[i].t_all);
+    pl->tc_max = std::max(pl->tc_max, pl->mt[i].t_ctx);
+    pl->cap_sum += pl->mt[i].row_cap;
+    pl->q_sum += cfgs[i].query_len;
+    pl->min_sum += pl->mt[i].row_min;
+  }
+  REQUIRE(pl->cap_sum < (1LL << 28), AKVS_ESHAPE, "batch too large");
+  return AKVS_OK;
 }
 
 }  // namespace
@@ -723,6 +855,7 @@ akvs_status akvs_sparse_query_attention(const void *q, const int32_t *positions,
   REQUIRE(aligned16(q) && aligned16(k) && aligned16(v) && aligned16(out) && aligned16(ws),
           AKVS_EINVAL, "misaligned argument");
   float *part_o = nullptr, *part_ml = nullptr;
+  long long part_rows = 0;
   if (ws) {
     size_t ml;
     const size_t o = attention_part_floats(m, n_rows, n_keys, &ml);
@@ -732,11 +865,12 @@ akvs_status akvs_sparse_query_attention(const void *q, const int32_t *positions,
       Carver cv(ws);
       part_o = cv.take<float>(o);
       part_ml = cv.take<float>(ml);
+      part_rows = (long long)(o / ((size_t)m->n_q_heads * m->head_dim));
     }
   }
   LAUNCH(AKVS_K_ATTENTION, launch_attention(q, positions, 0, n_rows, nullptr, k, v, n_keys,
                                             m->n_q_heads, m->n_kv_heads, m->head_dim, m->dtype,
-                                            out, part_o, part_ml, stream));
+                                            out, part_o, part_ml, part_rows, stream));
   return AKVS_OK;
 }
 
@@ -902,7 +1036,8 @@ akvs_status akvs_reuse_prefill(const int32_t *tokens, const void *embed, const a
     if (l + 1 < L) {
       LAUNCH(AKVS_K_ATTENTION, launch_attention(b.lb.q, b.rows, 0, cap, b.n_rows, kl, vl, T,
                                                 m->n_q_heads, hkv, hd, m->dtype, b.lb.att,
-                                                b.lb.part_o, b.lb.part_ml, stream));
+                                                b.lb.part_o, b.lb.part_ml, b.lb.part_rows,
+                                                stream));
       st = out_mlp(m, lw[l], b.h_probe, cap, b.n_rows, b.lb.att, b.lb.x, b.lb.act, b.lb.gpart,
                    stream, (int)mt.row_min);
       if (st) return st;
@@ -917,12 +1052,178 @@ akvs_status akvs_reuse_prefill(const int32_t *tokens, const void *embed, const a
                                                stream));
     LAUNCH(AKVS_K_ATTENTION, launch_attention(b.q_last, nullptr, Tc, q, nullptr, kl, vl, T,
                                               m->n_q_heads, hkv, hd, m->dtype, b.lb.att,
-                                              b.lb.part_o, b.lb.part_ml, stream));
+                                              b.lb.part_o, b.lb.part_ml, b.lb.part_rows, stream));
     st = out_mlp(m, lw[l], b.h_last, q, nullptr, b.lb.att, b.lb.x, b.lb.act, b.lb.gpart, stream);
     if (st) return st;
   }
   LAUNCH(AKVS_K_NORM, launch_rmsnorm(b.h_last, D, cfg->query_len, nullptr, nullptr, final_norm,
                                      m->dtype, D, m->rms_eps, out->h_query, AKVS_F32, D, stream));
+  return AKVS_OK;
+}
+
+size_t akvs_batch_workspace_size(const akvs_model_cfg *m, const akvs_reuse_cfg *cfgs,
+                                 int32_t batch) {
+  if (check_model(m) != AKVS_OK) return 0;
+  BatchPlan pl;
+  if (batch_plan(m, cfgs, batch, &pl) != AKVS_OK) return 0;
+  BatchBufs b;
+  return carve_batch(nullptr, m, cfgs, batch, pl, b);
+}
+
+akvs_status akvs_reuse_prefill_batch(const int32_t *const *tokens, int32_t batch,
+                                     const void *embed, const akvs_layer_w *lw,
+                                     const void *final_norm, const akvs_model_cfg *m,
+                                     const akvs_reuse_cfg *cfgs, const akvs_cache *caches,
+                                     const akvs_reuse_out *outs, void *ws, size_t ws_bytes,
+                                     hipStream_t stream) {
+  akvs_status st = check_model(m);
+  if (st) return st;
+  if ((st = check_layers(m, lw))) return st;
+  BatchPlan pl;
+  if ((st = batch_plan(m, cfgs, batch, &pl))) return st;
+  REQUIRE(tokens && caches && outs && embed && final_norm, AKVS_EINVAL, "NULL argument");
+  REQUIRE(aligned16(embed) && aligned16(final_norm) && aligned16(ws), AKVS_EINVAL,
+          "misaligned argument");
+  for (int i = 0; i < batch; ++i) {
+    if ((st = check_cache(&caches[i], m))) return st;
+    const akvs_reuse_out &o = outs[i];
+    REQUIRE(tokens[i], AKVS_EINVAL, "request %d: tokens are NULL", i);
+    REQUIRE(o.h_query && o.k_corr && o.v_corr, AKVS_EINVAL,
+            "request %d: h_query, k_corr and v_corr are required outputs", i);
+    REQUIRE(aligned16(o.h_query) && aligned16(o.k_corr) && aligned16(o.v_corr), AKVS_EINVAL,
+            "request %d: misaligned output", i);
+    REQUIRE(!(cfgs[i].flags & AKVS_F_GIVEN_PROBES) || (o.probe_k && o.probe_v), AKVS_EINVAL,
+            "request %d: AKVS_F_GIVEN_PROBES needs out->probe_k and out->probe_v", i);
+  }
+  BatchBufs b;
+  const size_t need = carve_batch(nullptr, m, cfgs, batch, pl, b);
+  REQUIRE(ws && ws_bytes >= need, AKVS_ENOSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+  carve_batch(ws, m, cfgs, batch, pl, b);
+  for (int i = 0; i < batch; ++i) {  // caller-visible outputs replace their workspace twins
+    const akvs_reuse_out &o = outs[i];
+    BatchReq &r = b.req[i];
+    if (o.probe_k) r.probe_k = o.probe_k;
+    if (o.probe_v) r.probe_v = o.probe_v;
+    if (o.d_k) r.d_k = o.d_k;
+    if (o.d_v) r.d_v = o.d_v;
+    if (o.rows) r.rows = o.rows;
+  }
+
+  const int L = m->n_layers, D = m->d_model, hkv = m->n_kv_heads, hd = m->head_dim;
+  const int kvw = hkv * hd, hqw = m->n_q_heads * hd, qkvw = hqw + 2 * kvw;
+  const bool no_prefix = (cfgs[0].flags & AKVS_F_NO_PREFIX_RECOMPUTE) != 0;
+  const int c = no_prefix ? 0 : cfgs[0].check_layer;
+  const size_t es = es_of(m->dtype);
+  const int T_max = (int)pl.t_max, cap_sum = (int)pl.cap_sum, q_sum = (int)pl.q_sum;
+  const int32_t *M_dev = b.row_off + batch;  // all requests' recomputed rows
+
+  LAUNCH(AKVS_K_OTHER, launch_rope_table(0, T_max, hd, (double)m->rope_theta, b.rope, stream));
+  // per request: bookkeeping, prefix layers, check layer, selection
+  for (int i = 0; i < batch; ++i) {
+    const Meta &mt = pl.mt[i];
+    BatchReq &r = b.req[i];
+    const akvs_reuse_cfg &cf = cfgs[i];
+    const int T = (int)mt.t_all, Tc = (int)mt.t_ctx, nch = cf.n_chunks;
+    const size_t corr_layer = (size_t)T * kvw * es;
+    char *k_corr = reinterpret_cast<char *>(outs[i].k_corr);
+    char *v_corr = reinterpret_cast<char *>(outs[i].v_corr);
+    LAUNCH(AKVS_K_OTHER, put_ints(mt.m.data(), mt.m.size(), r.meta, stream));
+    LAUNCH(AKVS_K_OTHER, launch_token_setup(r.meta, nch, r.tok_delta, r.tok_chunk, stream));
+    LAUNCH(AKVS_K_OTHER, launch_embed(tokens[i], T, embed, m->dtype, m->vocab, D, r.h_full, stream));
+    for (int l = 0; l < c; ++l) {
+      st = full_layer(m, lw[l], r.h_full, T, 0, b.rope, b.lb_full, k_corr + l * corr_layer,
+                      v_corr + l * corr_layer, stream);
+      if (st) return st;
+    }
+    if (!no_prefix) {
+      LAUNCH(AKVS_K_NORM, launch_rmsnorm(r.h_full, D, Tc, nullptr, nullptr, lw[c].attn_norm,
+                                         m->dtype, D, m->rms_eps, b.lb_full.x, m->dtype, D,
+                                         stream));
+      Epi e = qkv_epi(m, nullptr, b.k_chk, b.v_chk, nullptr, 0, 0, b.rope, T_max, 0);
+      e.n_off = hqw;
+      const char *wkv = reinterpret_cast<const char *>(lw[c].w_qkv) + (size_t)hqw * D * es;
+      GEMM(b.lb_full.x, D, wkv, D, Tc, 2 * kvw, D, nullptr, m->dtype, e, stream);
+      LAUNCH(AKVS_K_DIVERGENCE,
+             launch_divergence(b.k_chk, b.v_chk, m->dtype, cache_layer(&caches[i], c, Tc, hkv, hd),
+                               Tc, hkv, hd, r.tok_delta, b.rope, T_max, r.d_k, r.d_v, stream));
+    }
+    LAUNCH(AKVS_K_SELECT, launch_select(r.d_k, r.d_v, r.meta, nch, Tc, cf.query_len, cf.flags,
+                                        r.probe_k, r.probe_v, r.w_k, r.w_v, r.flags, r.chunk_rows,
+                                        r.rows, b.n_rows + i, r.fresh_row, stream));
+  }
+  // the combined row block: request i owns rows row_off[i] .. row_off[i] + n_rows[i]
+  LAUNCH(AKVS_K_OTHER, launch_batch_layout(b.n_rows, batch, b.row_off, stream));
+  for (int i = 0; i < batch; ++i) {
+    const Meta &mt = pl.mt[i];
+    const int cap = (int)mt.row_cap;
+    LAUNCH(AKVS_K_OTHER, launch_gather_rows(b.req[i].h_full, (int)mt.t_all, b.req[i].rows, cap,
+                                            b.n_rows + i, D, b.h_probe, stream, b.row_off + i));
+    LAUNCH(AKVS_K_OTHER, launch_copy_ints_at(b.req[i].rows, cap, b.n_rows + i, b.pos,
+                                             b.row_off + i, stream));
+  }
+  for (int l = c; l < L; ++l) {
+    LAUNCH(AKVS_K_NORM, launch_rmsnorm(b.h_probe, D, cap_sum, M_dev, nullptr, lw[l].attn_norm,
+                                       m->dtype, D, m->rms_eps, b.lb.x, m->dtype, D, stream));
+    GEMM(b.lb.x, D, lw[l].w_qkv, D, cap_sum, qkvw, D, M_dev, m->dtype,
+         qkv_epi(m, b.lb.q, b.k_fresh, b.v_fresh, b.pos, 0, 0, b.rope, T_max, 0), stream,
+         b.lb.gpart, (int)pl.min_sum);
+    const bool last = l + 1 == L;
+    int q_off = 0;
+    for (int i = 0; i < batch; ++i) {
+      const Meta &mt = pl.mt[i];
+      BatchReq &r = b.req[i];
+      const akvs_reuse_cfg &cf = cfgs[i];
+      const int T = (int)mt.t_all, Tc = (int)mt.t_ctx, nch = cf.n_chunks, cap = (int)mt.row_cap;
+      const size_t corr_layer = (size_t)T * kvw * es;
+      CacheLayer cl = cache_layer(&caches[i], l, Tc, hkv, hd);
+      LAUNCH(AKVS_K_OFFSET,
+             launch_chunk_offset(b.k_fresh, b.v_fresh, m->dtype, r.fresh_row, cl, r.meta, nch,
+                                 r.probe_k, r.probe_v, cf.flags, hkv, hd, b.rope, T_max, r.mu_k,
+                                 r.mu_v, stream, b.row_off + i));
+      void *kl = reinterpret_cast<char *>(outs[i].k_corr) + l * corr_layer;
+      void *vl = reinterpret_cast<char *>(outs[i].v_corr) + l * corr_layer;
+      LAUNCH(AKVS_K_CORRECTION,
+             launch_correction(cl, r.mu_k, r.mu_v, r.w_k, r.w_v, r.flags, b.k_fresh, b.v_fresh,
+                               r.fresh_row, r.tok_chunk, r.tok_delta, r.meta, nch, Tc, T, hkv, hd,
+                               cf.flags, b.rope, T_max, kl, vl, m->dtype, stream, b.row_off + i));
+      if (!last) {
+        LAUNCH(AKVS_K_ATTENTION,
+               launch_attention(b.lb.q, b.pos, 0, cap, b.n_rows + i, kl, vl, T, m->n_q_heads, hkv,
+                                hd, m->dtype, b.lb.att, b.lb.part_o, b.lb.part_ml,
+                                b.lb.part_rows, stream, b.row_off + i));
+        continue;
+      }
+      // last layer: only the query rows (the last q of each request's rows) go on
+      const int q = cf.query_len;
+      char *ql = reinterpret_cast<char *>(b.q_last) + (size_t)q_off * hqw * es;
+      LAUNCH(AKVS_K_OTHER, launch_copy_tail_rows(b.lb.q, (size_t)hqw * es, q, b.n_rows + i, ql,
+                                                 stream, b.row_off + i));
+      LAUNCH(AKVS_K_OTHER, launch_copy_tail_rows(b.h_probe, (size_t)D * 4, q, b.n_rows + i,
+                                                 b.h_last + (size_t)q_off * D, stream,
+                                                 b.row_off + i));
+      LAUNCH(AKVS_K_ATTENTION,
+             launch_attention(ql, nullptr, Tc, q, nullptr, kl, vl, T, m->n_q_heads, hkv, hd,
+                              m->dtype, reinterpret_cast<char *>(b.lb.att) + (size_t)q_off * hqw * es,
+                              b.lb.part_o, b.lb.part_ml, b.lb.part_rows, stream));
+      q_off += q;
+    }
+    if (!last) {
+      st = out_mlp(m, lw[l], b.h_probe, cap_sum, M_dev, b.lb.att, b.lb.x, b.lb.act, b.lb.gpart,
+                   stream, (int)pl.min_sum);
+    } else {
+      st = out_mlp(m, lw[l], b.h_last, q_sum, nullptr, b.lb.att, b.lb.x, b.lb.act, b.lb.gpart,
+                   stream);
+    }
+    if (st) return st;
+  }
+  int q_off = 0;
+  for (int i = 0; i < batch; ++i) {
+    LAUNCH(AKVS_K_NORM, launch_rmsnorm(b.h_last + (size_t)q_off * D, D, cfgs[i].query_len, nullptr,
+                                       nullptr, final_norm, m->dtype, D, m->rms_eps, outs[i].h_query,
+                                       AKVS_F32, D, stream));
+    if (outs[i].n_rows) LAUNCH(AKVS_K_OTHER, launch_copy_int(b.n_rows + i, outs[i].n_rows, stream));
+    q_off += cfgs[i].query_len;
+  }
   return AKVS_OK;
 }
 

@@ -65,7 +65,8 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
                                                    int split_keys, float scale_log2,
                                                    bf16_t *__restrict__ out,
                                                    float *__restrict__ part_o,
-                                                   float *__restrict__ part_ml) {
+                                                   float *__restrict__ part_ml,
+                                                   const int32_t *row_base) {
   constexpr int KS = HD / 16;          // contraction steps of S
   constexpr int DB = HD / 32;          // 32-wide head-dim blocks of O
   constexpr int KST = HD + 8;          // K tile row stride (bf16)
@@ -79,6 +80,12 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
   __shared__ __attribute__((aligned(16))) bf16_t Ks[2 * KBUF];
   __shared__ __attribute__((aligned(16))) bf16_t Vt[2 * VBUF];
   __shared__ int s_max[8];
+  if (row_base) {  // this call's rows start at row *row_base of q, pos and out
+    const int rb0 = *row_base;
+    Q += (size_t)rb0 * hq * HD;
+    out += (size_t)rb0 * hq * HD;
+    if (pos) pos += rb0;
+  }
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int nw = blockDim.x >> 6;
   const bool loader = wave < 4;
@@ -297,14 +304,18 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
 }
 
 // Merge of the key splits of one (row, head): weights 2^(m_s - max m), fixed split order.
+// A split whose keys all lie past the row (causal mask) holds m = -inf and no output: it
+// is skipped, never multiplied in (its part_o slot holds whatever the workspace held).
 // Thread = 4 consecutive head dims of one (row, head); the (m, l) pairs and the partial
 // outputs of four splits are requested at a time.
 __global__ __launch_bounds__(256) void k_attn_combine(const float *__restrict__ part_o,
                                                       const float *__restrict__ part_ml,
                                                       int n_splits, int rows,
                                                       const int32_t *rows_dev, int hq, int hd,
-                                                      bf16_t *__restrict__ out) {
+                                                      bf16_t *__restrict__ out,
+                                                      const int32_t *row_base) {
   const int per = hd >> 2;  // threads per (row, head)
+  if (row_base) out += (size_t)*row_base * hq * hd;
   const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
   const long long item = gid / per;
   const int e0 = (int)(gid - item * per) * 4;
@@ -329,6 +340,7 @@ __global__ __launch_bounds__(256) void k_attn_combine(const float *__restrict__ 
     }
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
+      if (ml[u].x == -INFINITY) continue;  // no visible key: its part_o was never written
       const float w = exp2f(ml[u].x - moff);
       l += w * ml[u].y;
       a.x += w * o[u].x; a.y += w * o[u].y; a.z += w * o[u].z; a.w += w * o[u].w;
@@ -337,6 +349,7 @@ __global__ __launch_bounds__(256) void k_attn_combine(const float *__restrict__ 
   for (; sp < n_splits; ++sp) {
     const size_t pi = sp * stride + item;
     const float2 ml = *reinterpret_cast<const float2 *>(part_ml + 2 * pi);
+    if (ml.x == -INFINITY) continue;
     const float4 o = *reinterpret_cast<const float4 *>(part_o + pi * hd + e0);
     const float w = exp2f(ml.x - moff);
     l += w * ml.y;
@@ -352,12 +365,19 @@ __global__ __launch_bounds__(64) void k_attn_f32(const float *__restrict__ Q, co
                                                  int pos0, int rows, const int32_t *rows_dev,
                                                  const float *__restrict__ Kc,
                                                  const float *__restrict__ Vc, int n_keys, int hq,
-                                                 int hkv, float scale, float *__restrict__ out) {
+                                                 int hkv, float scale, float *__restrict__ out,
+                                                 const int32_t *row_base) {
   constexpr int PER = HD / 64;
   __shared__ float qs[HD];
   __shared__ float ps[64];
   const int lane = threadIdx.x;
   const int r = blockIdx.x, head = blockIdx.y;
+  if (row_base) {
+    const int rb0 = *row_base;
+    Q += (size_t)rb0 * hq * HD;
+    out += (size_t)rb0 * hq * HD;
+    if (pos) pos += rb0;
+  }
   int R = rows;
   if (rows_dev) R = min(R, *rows_dev);
   if (r >= R) return;
@@ -423,7 +443,8 @@ int attn_split_keys(int n_keys, int n_splits) {
 hipError_t launch_attention(const void *q, const int32_t *pos, int pos0, int rows,
                             const int32_t *rows_dev, const void *k, const void *v, int n_keys,
                             int hq, int hkv, int hd, int dtype, void *out, float *part_o,
-                            float *part_ml, hipStream_t s) {
+                            float *part_ml, long long part_rows, hipStream_t s,
+                            const int32_t *row_base) {
   if (rows == 0) return hipSuccess;
   if (dtype == AKVS_BF16) {
     const float scale_log2 = 1.4426950408889634f / sqrtf((float)hd);
@@ -435,23 +456,24 @@ hipError_t launch_attention(const void *q, const int32_t *pos, int pos0, int row
     if (a.gh == 0) return hipErrorInvalidValue;
     const int rb = 32 * a.nrb;
     const int n_tiles = (rows + rb - 1) / rb;
-    const int n_splits = part_o ? attn_splits(rows, hq, hkv, n_keys) : 1;
+    int n_splits = part_o && part_ml ? attn_splits(rows, hq, hkv, n_keys) : 1;
+    if ((long long)n_splits * rows > part_rows) n_splits = (int)std::max(1LL, part_rows / rows);
     const int split_keys = attn_split_keys(n_keys, n_splits);
     dim3 g(n_tiles * hkv * a.n_groups * n_splits), b(64 * a.nrb * a.gh);
     if (hd == 128)
       hipLaunchKernelGGL(k_attn_bf16<128>, g, b, 0, s, Q, pos, pos0, rows, rows_dev, K, V, n_keys,
                          hq, hkv, a.gh, a.n_groups, a.nrb, n_tiles, n_splits, split_keys,
-                         scale_log2, O, part_o, part_ml);
+                         scale_log2, O, part_o, part_ml, row_base);
     else
       hipLaunchKernelGGL(k_attn_bf16<64>, g, b, 0, s, Q, pos, pos0, rows, rows_dev, K, V, n_keys,
                          hq, hkv, a.gh, a.n_groups, a.nrb, n_tiles, n_splits, split_keys,
-                         scale_log2, O, part_o, part_ml);
+                         scale_log2, O, part_o, part_ml, row_base);
     if (n_splits > 1) {
       hipError_t e = hipGetLastError();
       if (e != hipSuccess) return e;
       const long long threads = (long long)rows * hq * (hd / 4);
       hipLaunchKernelGGL(k_attn_combine, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, s,
-                         part_o, part_ml, n_splits, rows, rows_dev, hq, hd, O);
+                         part_o, part_ml, n_splits, rows, rows_dev, hq, hd, O, row_base);
     }
   } else {
     const float scale = 1.0f / sqrtf((float)hd);
@@ -462,10 +484,10 @@ hipError_t launch_attention(const void *q, const int32_t *pos, int pos0, int row
     float *O = reinterpret_cast<float *>(out);
     if (hd == 128)
       hipLaunchKernelGGL(k_attn_f32<128>, g, b, 0, s, Q, pos, pos0, rows, rows_dev, K, V, n_keys,
-                         hq, hkv, scale, O);
+                         hq, hkv, scale, O, row_base);
     else
       hipLaunchKernelGGL(k_attn_f32<64>, g, b, 0, s, Q, pos, pos0, rows, rows_dev, K, V, n_keys,
-                         hq, hkv, scale, O);
+                         hq, hkv, scale, O, row_base);
   }
   return hipGetLastError();
 }

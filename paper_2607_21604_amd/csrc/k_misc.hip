@@ -122,43 +122,88 @@ hipError_t launch_rmsnorm(const float *h, int ldh, int rows, const int32_t *rows
 }
 
 __global__ void k_gather_rows(const float *src, int n_src, const int32_t *idx, int cap,
-                              const int32_t *n_dev, int D, float *dst) {
+                              const int32_t *n_dev, int D, float *dst, const int32_t *dst_base) {
   const int i = blockIdx.x;
   if (i >= cap || i >= *n_dev) return;
   const int j = idx[i];
   const bool ok = j >= 0 && j < n_src;
   const float *a = src + (size_t)(ok ? j : 0) * D;
-  float *b = dst + (size_t)i * D;
+  float *b = dst + ((size_t)(dst_base ? *dst_base : 0) + i) * D;
   for (int e = threadIdx.x * 4; e < D; e += blockDim.x * 4)
     *reinterpret_cast<float4 *>(b + e) =
         ok ? *reinterpret_cast<const float4 *>(a + e) : make_float4(0.f, 0.f, 0.f, 0.f);
 }
 
 hipError_t launch_gather_rows(const float *src, int n_src, const int32_t *idx, int cap,
-                              const int32_t *n_dev, int D, float *dst, hipStream_t s) {
+                              const int32_t *n_dev, int D, float *dst, hipStream_t s,
+                              const int32_t *dst_base) {
   if (cap == 0) return hipSuccess;
   hipLaunchKernelGGL(k_gather_rows, dim3(cap), dim3(256), 0, s, src, n_src, idx, cap, n_dev, D,
-                     dst);
+                     dst, dst_base);
   return hipGetLastError();
 }
 
-// dst[i] = src[*n_dev - n + i] for i < n (rows of row_bytes bytes, a multiple of 16).
+// dst[i] = src[base + *n_dev - n + i] for i < n (rows of row_bytes bytes, a multiple of 16).
 __global__ void k_copy_tail_rows(const char *src, size_t row_bytes, int n, const int32_t *n_dev,
-                                 char *dst) {
+                                 char *dst, const int32_t *src_base) {
   const int i = blockIdx.x;
   const int j = *n_dev - n + i;
   if (i >= n || j < 0) return;
-  const uint4 *a = reinterpret_cast<const uint4 *>(src + (size_t)j * row_bytes);
+  const size_t row = (size_t)(src_base ? *src_base : 0) + j;
+  const uint4 *a = reinterpret_cast<const uint4 *>(src + row * row_bytes);
   uint4 *b = reinterpret_cast<uint4 *>(dst + (size_t)i * row_bytes);
   for (size_t e = threadIdx.x; e < row_bytes / 16; e += blockDim.x) b[e] = a[e];
 }
 
 hipError_t launch_copy_tail_rows(const void *src, size_t row_bytes, int n, const int32_t *n_dev,
-                                 void *dst, hipStream_t s) {
+                                 void *dst, hipStream_t s, const int32_t *src_base) {
   if (n == 0) return hipSuccess;
   hipLaunchKernelGGL(k_copy_tail_rows, dim3(n), dim3(256), 0, s,
                      reinterpret_cast<const char *>(src), row_bytes, n, n_dev,
-                     reinterpret_cast<char *>(dst));
+                     reinterpret_cast<char *>(dst), src_base);
+  return hipGetLastError();
+}
+
+// row_off[b] = n_rows[0] + ... + n_rows[b-1], b <= B (one thread: B is small).
+__global__ void k_batch_layout(const int32_t *n_rows, int B, int32_t *row_off) {
+  if (blockIdx.x != 0 || threadIdx.x != 0) return;
+  int32_t acc = 0;
+  for (int b = 0; b < B; ++b) {
+    row_off[b] = acc;
+    acc += n_rows[b];
+  }
+  row_off[B] = acc;
+}
+
+hipError_t launch_batch_layout(const int32_t *n_rows, int B, int32_t *row_off, hipStream_t s) {
+  hipLaunchKernelGGL(k_batch_layout, dim3(1), dim3(64), 0, s, n_rows, B, row_off);
+  return hipGetLastError();
+}
+
+// dst[*dst_base + i] = src[i], i < min(cap, *n_dev)
+__global__ void k_copy_ints_at(const int32_t *src, int cap, const int32_t *n_dev, int32_t *dst,
+                               const int32_t *dst_base) {
+  const int n = min(cap, *n_dev);
+  const int base = *dst_base;
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x)
+    dst[base + i] = src[i];
+}
+
+hipError_t launch_copy_ints_at(const int32_t *src, int cap, const int32_t *n_dev, int32_t *dst,
+                               const int32_t *dst_base, hipStream_t s) {
+  if (cap == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_copy_ints_at, dim3((cap + 255) / 256), dim3(256), 0, s, src, cap, n_dev,
+                     dst, dst_base);
+  return hipGetLastError();
+}
+
+// one 32-bit value: dst[0] = src[0]
+__global__ void k_copy_int(const int32_t *src, int32_t *dst) {
+  if (blockIdx.x == 0 && threadIdx.x == 0) dst[0] = src[0];
+}
+
+hipError_t launch_copy_int(const int32_t *src, int32_t *dst, hipStream_t s) {
+  hipLaunchKernelGGL(k_copy_int, dim3(1), dim3(64), 0, s, src, dst);
   return hipGetLastError();
 }
 

@@ -251,7 +251,8 @@ __global__ __launch_bounds__(UP == 1 ? 1024 : 512) void k_chunk_offset(const TF 
                                                        const int4 *meta, const int32_t *probe_k,
                                                        const int32_t *probe_v, uint32_t flags,
                                                        int hkv, int hd, const float2 *rope,
-                                                       int rope_rows, float *mu_k, float *mu_v) {
+                                                       int rope_rows, float *mu_k, float *mu_v,
+                                                       const int32_t *fresh_base) {
   __shared__ float s_part[OFF_LDS];
   const int c = blockIdx.x;
   const int side = blockIdx.y;  // 0 = K, 1 = V
@@ -281,8 +282,9 @@ __global__ __launch_bounds__(UP == 1 ? 1024 : 512) void k_chunk_offset(const TF 
   for (int k = wave; k < b; k += nw) {
     const int j = probes[k];
     const bool inside = j >= mc.x && j < mc.x + mc.y;  // a token of this unit
-    const int r = inside ? fresh_row[j] : -1;
+    int r = inside ? fresh_row[j] : -1;
     if (r < 0) continue;  // uniform over the wave
+    if (fresh_base) r += *fresh_base;
 #pragma unroll
     for (int q = 0; q < UP; ++q) {
       const int u = lane + 64 * q;
@@ -329,7 +331,8 @@ hipError_t launch_chunk_offset(const void *k_fresh, const void *v_fresh, int fre
                                const int32_t *fresh_row, CacheLayer cache, const int32_t *meta,
                                int n_chunks, const int32_t *probe_k, const int32_t *probe_v,
                                uint32_t flags, int hkv, int hd, const float *rope, int rope_rows,
-                               float *mu_k, float *mu_v, hipStream_t s) {
+                               float *mu_k, float *mu_v, hipStream_t s,
+                               const int32_t *fresh_base) {
   const int kvw = hkv * hd;
   if (kvw > 2048 || hd % 16) return hipErrorInvalidValue;
   int nw = OFF_LDS / kvw;
@@ -341,7 +344,7 @@ hipError_t launch_chunk_offset(const void *k_fresh, const void *v_fresh, int fre
 #define AKVS_OFFSET(TF, UP)                                                                    \
   hipLaunchKernelGGL((k_chunk_offset<TF, UP>), g, b, 0, s, as<TF>(k_fresh), as<TF>(v_fresh),      \
                      fresh_row, cache, m4, probe_k, probe_v, flags, hkv, hd, r, rope_rows, mu_k, \
-                     mu_v)
+                     mu_v, fresh_base)
   const bool wide = kvw > 1024;
   if (fresh_dtype == AKVS_BF16) {
     if (wide) AKVS_OFFSET(bf16_t, 2); else AKVS_OFFSET(bf16_t, 1);
@@ -374,7 +377,8 @@ struct CorrTok {
 __device__ __forceinline__ CorrTok corr_token(int t, int t_ctx, const uint8_t *tok_flags,
                                               const int32_t *fresh_row, const int32_t *tok_chunk,
                                               const int32_t *tok_delta, const int4 *meta,
-                                              int n_chunks, int rope_rows, uint32_t flags) {
+                                              int n_chunks, int rope_rows, uint32_t flags,
+                                              int fresh_off) {
   CorrTok c{0, 0, -1, true, true};
   const uint8_t f = (t < t_ctx) ? (tok_flags ? tok_flags[t] : 0) : 3;
   if (t < t_ctx) {
@@ -394,6 +398,7 @@ __device__ __forceinline__ CorrTok corr_token(int t, int t_ctx, const uint8_t *t
   c.fresh_k = (f & 1) || any;
   c.fresh_v = (f & 2) || any;
   c.fr = (c.fresh_k || c.fresh_v) ? fresh_row[t] : -1;
+  if (c.fr >= 0) c.fr += fresh_off;
   return c;
 }
 
@@ -447,9 +452,11 @@ __global__ __launch_bounds__(256) void k_correction(CacheLayer cache, const floa
                                                     int n_chunks, int t_ctx, int t_all, int hkv,
                                                     int hd, uint32_t flags, const float2 *rope,
                                                     int rope_rows, TS *__restrict__ k_corr,
-                                                    TS *__restrict__ v_corr) {
+                                                    TS *__restrict__ v_corr,
+                                                    const int32_t *fresh_base) {
   const int half = hd >> 1;
   const int units = hkv * (half >> 3);
+  const int fresh_off = fresh_base ? *fresh_base : 0;
   const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
   const long long grp = gid / units;
   const int u = (int)(gid - grp * units);
@@ -462,7 +469,7 @@ __global__ __launch_bounds__(256) void k_correction(CacheLayer cache, const floa
   for (int i = 0; i < CORR_T; ++i) {
     const int t = min(t0 + i, t_all - 1);  // a repeated last position is computed twice
     const CorrTok c = corr_token(t, t_ctx, tok_flags, fresh_row, tok_chunk, tok_delta, meta,
-                                 n_chunks, rope_rows, flags);
+                                 n_chunks, rope_rows, flags, fresh_off);
     const size_t orow = (size_t)t * hkv + h;
     const size_t mo = (size_t)c.chunk * hkv * hd + (size_t)h * hd;
     corr_side(c.fresh_k, c.fr, k_fresh, cache.k, cache.k_meta, cache.dtype, orow, hkv, h, hd, e0,
@@ -492,7 +499,8 @@ hipError_t launch_correction(CacheLayer cache, const float *mu_k, const float *m
                              const int32_t *meta, int n_chunks, int t_ctx,
                              int t_all, int hkv, int hd, uint32_t flags, const float *rope,
                              int rope_rows, void *k_corr, void *v_corr, int out_dtype,
-                             hipStream_t s) {
+                             hipStream_t s,
+                             const int32_t *fresh_base) {
   const int4 *m4 = reinterpret_cast<const int4 *>(meta);
   const long long threads = ((long long)t_all + CORR_T - 1) / CORR_T * hkv * (hd / 16);
   if (threads == 0) return hipSuccess;
@@ -502,12 +510,14 @@ hipError_t launch_correction(CacheLayer cache, const float *mu_k, const float *m
     hipLaunchKernelGGL(k_correction<bf16_t>, g, b, 0, s, cache, mu_k, mu_v, w_k, w_v, tok_flags,
                        as<bf16_t>(k_fresh), as<bf16_t>(v_fresh), fresh_row, tok_chunk, tok_delta,
                        m4, n_chunks, t_ctx, t_all, hkv, hd, flags, r, rope_rows,
-                       reinterpret_cast<bf16_t *>(k_corr), reinterpret_cast<bf16_t *>(v_corr));
+                       reinterpret_cast<bf16_t *>(k_corr), reinterpret_cast<bf16_t *>(v_corr),
+                       fresh_base);
   else
     hipLaunchKernelGGL(k_correction<float>, g, b, 0, s, cache, mu_k, mu_v, w_k, w_v, tok_flags,
                        as<float>(k_fresh), as<float>(v_fresh), fresh_row, tok_chunk, tok_delta,
                        m4, n_chunks, t_ctx, t_all, hkv, hd, flags, r, rope_rows,
-                       reinterpret_cast<float *>(k_corr), reinterpret_cast<float *>(v_corr));
+                       reinterpret_cast<float *>(k_corr), reinterpret_cast<float *>(v_corr),
+                       fresh_base);
   return hipGetLastError();
 }
 

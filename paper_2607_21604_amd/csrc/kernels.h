@@ -17,12 +17,22 @@ hipError_t launch_embed(const int32_t *tok, int n, const void *embed, int dtype,
 hipError_t launch_rmsnorm(const float *h, int ldh, int rows, const int32_t *rows_dev,
                           const int32_t *base_dev, const void *gain, int gain_dtype, int D,
                           float eps, void *out, int out_dtype, int ldo, hipStream_t s);
-// dst[i] = src[idx[i]], i < *n_dev (rows of D floats); indices outside [0, n_src) give 0.
+// dst[base + i] = src[idx[i]], i < *n_dev (rows of D floats; base = *dst_base or 0);
+// indices outside [0, n_src) give 0.
 hipError_t launch_gather_rows(const float *src, int n_src, const int32_t *idx, int cap,
-                              const int32_t *n_dev, int D, float *dst, hipStream_t s);
-// dst row i = src row (*n_dev - n + i), i < n: the last n of *n_dev rows.
+                              const int32_t *n_dev, int D, float *dst, hipStream_t s,
+                              const int32_t *dst_base = nullptr);
+// dst row i = src row (base + *n_dev - n + i), i < n: the last n of *n_dev rows that start
+// at row base = *src_base (or 0).
 hipError_t launch_copy_tail_rows(const void *src, size_t row_bytes, int n, const int32_t *n_dev,
-                                 void *dst, hipStream_t s);
+                                 void *dst, hipStream_t s, const int32_t *src_base = nullptr);
+// row_off[b] = n_rows[0] + ... + n_rows[b-1] for b = 0..B (a batch's row segments).
+hipError_t launch_batch_layout(const int32_t *n_rows, int B, int32_t *row_off, hipStream_t s);
+// dst[*dst_base + i] = src[i] for i < min(cap, *n_dev).
+hipError_t launch_copy_ints_at(const int32_t *src, int cap, const int32_t *n_dev, int32_t *dst,
+                               const int32_t *dst_base, hipStream_t s);
+// dst[0] = src[0] on the device.
+hipError_t launch_copy_int(const int32_t *src, int32_t *dst, hipStream_t s);
 // per unit token t < T_c: tok_delta[t] = s_i, tok_chunk[t] = i.
 hipError_t launch_token_setup(const int32_t *meta, int n_chunks, int32_t *tok_delta,
                               int32_t *tok_chunk, hipStream_t s);
@@ -40,7 +50,8 @@ hipError_t launch_chunk_offset(const void *k_fresh, const void *v_fresh, int fre
                                const int32_t *fresh_row, CacheLayer cache, const int32_t *meta,
                                int n_chunks, const int32_t *probe_k, const int32_t *probe_v,
                                uint32_t flags, int hkv, int hd, const float *rope, int rope_rows,
-                               float *mu_k, float *mu_v, hipStream_t s);
+                               float *mu_k, float *mu_v, hipStream_t s,
+                               const int32_t *fresh_base = nullptr);
 // Corrected (or, with mu == nullptr and tok_flags == nullptr, just re-rotated) cache rows.
 // A token's unit and offset come from tok_chunk / tok_delta when given, else from a
 // binary search of meta (n_chunks entries).
@@ -51,7 +62,8 @@ hipError_t launch_correction(CacheLayer cache, const float *mu_k, const float *m
                              const int32_t *meta, int n_chunks, int t_ctx,
                              int t_all, int hkv, int hd, uint32_t flags, const float *rope,
                              int rope_rows, void *k_corr, void *v_corr, int out_dtype,
-                             hipStream_t s);
+                             hipStream_t s,
+                             const int32_t *fresh_base = nullptr);
 hipError_t launch_quantize(const void *x, int x_dtype, int n_rows, int hd, int bits,
                            uint8_t *codes, _Float16 *meta, hipStream_t s);
 
@@ -94,11 +106,14 @@ int gemm_cu_count();
 
 // ---- k_attn.hip ---------------------------------------------------------------------
 // With part_o / part_ml (bf16 path), the key range is split for parallelism:
-// part_o [splits][rows][hq][hd] fp32, part_ml [splits][rows][hq][2] fp32, splits as below.
+// part_o [splits][rows][hq][hd] fp32, part_ml [splits][rows][hq][2] fp32, splits as below,
+// lowered so that splits x rows stays within part_rows (what the buffers hold).
+// row_base (device, may be null): rows start at row *row_base of q, pos and out.
 hipError_t launch_attention(const void *q, const int32_t *pos, int pos0, int rows,
                             const int32_t *rows_dev, const void *k, const void *v, int n_keys,
                             int hq, int hkv, int hd, int dtype, void *out, float *part_o,
-                            float *part_ml, hipStream_t s);
+                            float *part_ml, long long part_rows, hipStream_t s,
+                            const int32_t *row_base = nullptr);
 // number of key splits launch_attention uses for `rows` rows over n_keys keys
 int attn_splits(int rows, int hq, int hkv, int n_keys);
 int attn_split_keys(int n_keys, int n_splits);

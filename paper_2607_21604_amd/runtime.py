@@ -97,6 +97,53 @@ class Engine:
         return outputs
 
 
+def _reuse_outputs(engine, query_len, tc, sum_b, t_all):
+    sh, dev = engine.shape, engine.device
+    out = {
+        "h_query": torch.empty((query_len, sh.d_model), dtype=torch.float32, device=dev),
+        "k_corr": torch.empty((engine.n_layers, t_all, sh.n_kv_heads, sh.head_dim),
+                              dtype=engine.dtype, device=dev),
+        "probe_k": torch.empty(max(sum_b, 1), dtype=torch.int32, device=dev),
+        "probe_v": torch.empty(max(sum_b, 1), dtype=torch.int32, device=dev),
+        "d_k": torch.empty(tc, dtype=torch.float32, device=dev),
+        "d_v": torch.empty(tc, dtype=torch.float32, device=dev),
+        "rows": torch.empty(t_all, dtype=torch.int32, device=dev),
+        "n_rows": torch.empty(1, dtype=torch.int32, device=dev),
+    }
+    out["v_corr"] = torch.empty_like(out["k_corr"])
+    out["_sum_b"] = sum_b
+    return out
+
+
+def reuse_prefill_batch(engine: Engine, requests, refresh=(1, 5), check_layer: int = 1,
+                        flags: int = 0, outputs=None):
+    """Batched reuse prefill (akvs_reuse_prefill_batch). `requests`: list of dicts with
+    tokens, chunk_lens, query_len, k_cache, v_cache (and optional k_meta, v_meta,
+    cache_dtype). Returns one output dict per request (as Engine.reuse_prefill);
+    `outputs` may pass a previous result list to reuse its buffers."""
+    cfgs, caches, outs = [], [], []
+    if outputs is None:
+        outputs = []
+        for r in requests:
+            cfg = akvs.reuse_cfg(r["chunk_lens"], r["query_len"], refresh, check_layer, flags)
+            _, (tc, sum_b, _, t_all) = akvs.akvs_chunk_meta(cfg)
+            outputs.append(_reuse_outputs(engine, r["query_len"], tc, sum_b, t_all))
+    for r, o in zip(requests, outputs):
+        cfgs.append(akvs.reuse_cfg(r["chunk_lens"], r["query_len"], refresh, check_layer, flags))
+        dt = r.get("cache_dtype")
+        caches.append(akvs.cache_struct(r["k_cache"], r["v_cache"], r.get("k_meta"), r.get("v_meta"),
+                                        dt if dt is not None else akvs.dtype_code(r["k_cache"])))
+        outs.append(akvs.ReuseOut(*(akvs.ptr(o[k]) for k in ("h_query", "k_corr", "v_corr",
+                                                            "probe_k", "probe_v", "d_k", "d_v",
+                                                            "rows", "n_rows"))))
+    ca, cc, co = akvs.batch_arrays(cfgs, caches, outs)
+    ws = engine.workspace(akvs.akvs_batch_workspace_size(engine.m, ca, len(requests)))
+    akvs.akvs_reuse_prefill_batch([r["tokens"] for r in requests], engine.weights["embed"],
+                                  engine.layers, engine.weights["final_norm"], engine.m, ca, cc,
+                                  co, ws)
+    return outputs
+
+
 def quantize_cache(x: torch.Tensor, bits: int):
     """Group-64 quantised copy of a cache [..][hd] (codes uint8, meta fp16 (scale, zero))."""
     hd = x.shape[-1]
@@ -105,6 +152,25 @@ def quantize_cache(x: torch.Tensor, bits: int):
     meta = torch.empty(x.shape[:-1] + (hd // 64, 2), dtype=torch.float16, device=x.device)
     akvs.akvs_quantize_cache(x.contiguous(), rows, hd, bits, codes, meta)
     return codes, meta
+
+
+class BatchGraph:
+    """One batched reuse-prefill call (reuse_prefill_batch) captured in a HIP graph, as
+    ReuseGraph does for a single request: an eager call sizes the workspace and allocates
+    the outputs, the capture reruns it on the same buffers, replay() reruns every kernel."""
+
+    def __init__(self, engine: Engine, requests, *args, **kw):
+        kw.pop("outputs", None)
+        self.out = reuse_prefill_batch(engine, requests, *args, **kw)
+        torch.cuda.synchronize(engine.device)
+        self.graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(self.graph):
+            reuse_prefill_batch(engine, requests, *args, outputs=self.out, **kw)
+        torch.cuda.synchronize(engine.device)
+
+    def replay(self):
+        self.graph.replay()
+        return self.out
 
 
 class ReuseGraph:

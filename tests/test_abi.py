@@ -159,3 +159,27 @@ def test_attention_workspace(lib):
     st = lib.akvs_sparse_query_attention(4096, 4096, 1400, 4096, 4096, 4516, ctypes.byref(m), 4096,
                                          4096, need - 256, None)
     assert st == akvs.AKVS_ENOSPACE
+
+
+def test_batch_workspace_and_validation(lib):
+    """Batched reuse prefill: the workspace covers each request's single-call buffers;
+    requests that disagree on the check layer, and an empty batch, are refused before any
+    device work."""
+    m = akvs.ModelCfg(4, 3072, 24, 8, 128, 8192, 16, 1e6, 1e-6, akvs.AKVS_BF16)
+    a = akvs.reuse_cfg([300, 280, 256], 64, (1, 5), 1, 0)
+    b = akvs.reuse_cfg([512, 100], 32, (1, 5), 1, 0)
+    ca, _, _ = akvs.batch_arrays([a, b], [], [])
+    both = akvs.akvs_batch_workspace_size(m, ca, 2)
+    one = akvs.akvs_batch_workspace_size(m, ca, 1)
+    assert both > one > 0
+    c = akvs.reuse_cfg([512, 100], 32, (1, 5), 2, 0)
+    cm, _, _ = akvs.batch_arrays([a, c], [], [])
+    assert akvs.akvs_batch_workspace_size(m, cm, 2) == 0
+    tp = (ctypes.c_void_p * 2)(4096, 4096)
+    lw = (akvs.LayerW * 4)(*[akvs.LayerW(*([4096] * 6)) for _ in range(4)])
+    st = lib.akvs_reuse_prefill_batch(tp, 2, 4096, lw, 4096, ctypes.byref(m), cm, None, None,
+                                      4096, 1 << 30, None)
+    assert st == akvs.AKVS_EINVAL and b"check layer" in lib.akvs_last_error()
+    st = lib.akvs_reuse_prefill_batch(tp, 0, 4096, lw, 4096, ctypes.byref(m), ca, None, None,
+                                      4096, 1 << 30, None)
+    assert st == akvs.AKVS_EINVAL and b"batch 0" in lib.akvs_last_error()

@@ -64,3 +64,24 @@ def test_graph_replay_with_new_tokens_in_place():
     torch.cuda.synchronize()
     assert_same(got, eager)
     assert not torch.equal(got["h_query"], first["h_query"])
+
+
+def test_batch_graph_replays_match_eager():
+    """The batched call captured once: each replay equals the eager batch bit for bit,
+    with eager single-request work between replays."""
+    from paper_2607_21604_amd.runtime import BatchGraph, reuse_prefill_batch
+    from tests.test_gpu_batch import make_requests
+    c = Case("3b", n_layers=3, n_units=4)
+    reqs = make_requests(c, [([200, 230, 192, 256], 64, 0), ([250, 199], 64, 5)])
+    eager = [snapshot(o) for o in reuse_prefill_batch(c.eng, reqs, (1, 5), 1, 0)]
+    g = BatchGraph(c.eng, reqs, (1, 5), 1, 0)
+    for i in range(3):
+        got = [snapshot(o) for o in g.replay()]
+        torch.cuda.synchronize()
+        for a, b in zip(got, eager):
+            assert_same(a, b)
+        r = reqs[1]
+        other = c.eng.reuse_prefill(r["tokens"], r["chunk_lens"], r["query_len"], r["k_cache"],
+                                    r["v_cache"], (1, 1), 1, 0)
+        torch.cuda.synchronize()
+        assert int(other["n_rows"][0]) == sum(r["chunk_lens"]) + r["query_len"]

@@ -301,6 +301,7 @@ def test_constant_residual_is_recovered_on_gpu():
 
 @pytest.mark.parametrize("dtype,hq,hkv,hd,n_rows,n_keys", [
     ("bf16", 6, 2, 128, 77, 300), ("bf16", 28, 4, 128, 130, 1000), ("bf16", 4, 4, 64, 64, 64),
+    ("bf16", 24, 8, 128, 600, 2400),
     ("f32", 4, 4, 64, 50, 288), ("f32", 6, 3, 128, 9, 70)])
 def test_sparse_query_attention(dtype, hq, hkv, hd, n_rows, n_keys):
     tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
@@ -312,11 +313,17 @@ def test_sparse_query_attention(dtype, hq, hkv, hd, n_rows, n_keys):
     m = akvs.ModelCfg(1, 64, hq, hkv, hd, 64, 16, 1e4, 1e-6, akvs.dtype_code(q))
     ref = oracle.attention(f64(q), pos, f64(k), f64(v), np.arange(n_keys)).reshape(n_rows, -1)
     nbytes = akvs.akvs_attention_workspace_size(m, n_rows, n_keys)
-    for ws in (None, torch.empty(max(nbytes, 1), dtype=torch.uint8, device=DEV)):
+    # the key-split workspace starts as all-ones bytes (NaN floats): splits whose keys all
+    # lie past a row's position must not carry any of it into the merge
+    outs = []
+    for ws in (None, torch.full((max(nbytes, 1),), 255, dtype=torch.uint8, device=DEV),
+               torch.zeros(max(nbytes, 1), dtype=torch.uint8, device=DEV)):
         out = torch.empty((n_rows, hq * hd), dtype=tdt, device=DEV)
         akvs.akvs_sparse_query_attention(to_dev(q), to_dev(pos), n_rows, to_dev(k), to_dev(v), n_keys,
                                          m, out, ws)
         assert max_rel(f64(out), ref) < (1e-2 if dtype == "bf16" else 1e-5)
+        outs.append(out)
+    assert torch.equal(outs[1], outs[2])
 
 
 def gemm_case(shape, n_rows, seed):
