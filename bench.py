@@ -37,11 +37,12 @@ def parse():
     p.add_argument("--workload", default="3b")
     p.add_argument("--refresh", default="1/5")
     p.add_argument("--refresh-sweep", default="auto",
-                   help="extra refresh ratios timed after the headline one, comma separated "
+                   help="extra refresh ratios timed after the headline one, comma separated; "
+                        "a ':select' suffix times the select-only mode (offsets forced to 0) "
                         "('auto': the workload's listed ratios, 'none': skip)")
     p.add_argument("--batch-sweep", default="auto",
                    help="comma-separated batch sizes for the batched reuse prefill leg "
-                        "(auto: 4,8 for 3b; none elsewhere)")
+                        "(auto: 4,8,16 for 3b; none elsewhere)")
     p.add_argument("--check-layer", type=int, default=1)
     p.add_argument("--seed", type=int, default=0)
     p.add_argument("--no-cpu-baseline", action="store_true")
@@ -359,24 +360,30 @@ def main():
     sweep = {}
     extra = args.refresh_sweep
     if extra == "auto":
-        extra = {"3b": "1/10,3/10", "32b": "1/10,3/10"}.get(wl.name, "none")
+        extra = {"3b": "1/100,1/20,1/10,3/10,1/2,3/4,1/5:select",
+                 "32b": "1/10,3/10"}.get(wl.name, "none")
     full_ref = ms_full_graph or ms_full
     for r in ([] if extra == "none" else extra.split(",")):
-        rn, rd = (int(x) for x in r.split("/"))
+        ratio, _, mode = r.partition(":")
+        rn, rd = (int(x) for x in ratio.split("/"))
+        fl = akvs.AKVS_F_NO_CORRECTION if mode == "select" else 0
         if args.no_graph:
-            o2 = reuse(refresh=(rn, rd))
-            ms_r = timed(lambda: reuse(o2, refresh=(rn, rd)))
+            o2 = eng.reuse_prefill(toks, wl.chunk_lens, wl.query_len, k_cache, v_cache, (rn, rd),
+                                   args.check_layer, fl, **qkw)
+            ms_r = timed(lambda: eng.reuse_prefill(toks, wl.chunk_lens, wl.query_len, k_cache,
+                                                   v_cache, (rn, rd), args.check_layer, fl,
+                                                   outputs=o2, **qkw))
         else:
             rg = ReuseGraph(eng, toks, wl.chunk_lens, wl.query_len, k_cache, v_cache, (rn, rd),
-                            args.check_layer, 0, **qkw)
+                            args.check_layer, fl, **qkw)
             o2 = rg.out
             ms_r = timed(rg.replay)
             del rg
         m_r = int(o2["n_rows"].item())
-        sweep[f"{rn}/{rd}"] = {"tokens_per_s": wl.n_tokens / (ms_r * 1e-3), "ms_per_step": ms_r,
-                               "recomputed_rows": m_r,
-                               "speedup_vs_full_prefill": full_ref / ms_r if full_ref else None}
-        print(f"# reuse at r={rn}/{rd}: {ms_r:.3f} ms/step, M={m_r}", file=sys.stderr, flush=True)
+        sweep[r] = {"tokens_per_s": wl.n_tokens / (ms_r * 1e-3), "ms_per_step": ms_r,
+                    "recomputed_rows": m_r,
+                    "speedup_vs_full_prefill": full_ref / ms_r if full_ref else None}
+        print(f"# reuse at r={r}: {ms_r:.3f} ms/step, M={m_r}", file=sys.stderr, flush=True)
         del o2
 
     # batched reuse prefill: B requests of this workload's shape (same unit lengths, their
@@ -385,7 +392,7 @@ def main():
     batch = {}
     bs = args.batch_sweep
     if bs == "auto":
-        bs = {"3b": "4,8"}.get(wl.name, "none")
+        bs = {"3b": "4,8,16"}.get(wl.name, "none")
     if bs != "none" and wl.cache_bits == 16 and not args.random_caches:
         from paper_2607_21604_amd.runtime import BatchGraph, reuse_prefill_batch
         sizes = [int(x) for x in bs.split(",")]
