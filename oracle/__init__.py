@@ -3,7 +3,7 @@
 TEST INFRASTRUCTURE ONLY. This package is a plain, slow, fp64 NumPy statement of
 what the reuse-prefill path computes (the decoder, full prefill, standalone unit
 caching, the probe-guided residual correction of Sec. 3.3 / Algorithm 1, and the
-group-64 cache quantiser). Only the tests, the smoke check and the benchmark's
+group-64 cache quantisers: 2/4-bit integer and FP8 E4M3). Only the tests, the smoke check and the benchmark's
 CPU-baseline leg may import it; the library path never does, and it shares no
 code with the HIP kernels.
 
@@ -16,4 +16,5 @@ from .reuse import (F_NO_CORRECTION, F_UNIT_WEIGHTS, F_FRESH_IF_RECOMPUTED,
                     F_NO_PREFIX_RECOMPUTE, probe_budget, chunk_starts, rerotate,
                     divergence, select_top, correction_weights, probe_offset,
                     correct_chunk, reuse_prefill)
-from .quant import quantize_g64, dequantize_g64, pack_codes, unpack_codes
+from .quant import (quantize_g64, dequantize_g64, pack_codes, unpack_codes, E4M3_MAX,
+                    e4m3_value, e4m3_code, quantize_e4m3_g64, dequantize_e4m3_g64)
