@@ -279,13 +279,13 @@ def main():
         k_cache, v_cache = eng.cache_units(toks, wl.chunk_lens)
     qkw = {}
     if wl.cache_bits < 16:
-        from paper_2607_21604_amd.runtime import quantize_cache
+        from paper_2607_21604_amd.runtime import cache_dtype_for_bits, quantize_cache
         kq, km = quantize_cache(k_cache, wl.cache_bits)
         vq, vm = quantize_cache(v_cache, wl.cache_bits)
         del k_cache, v_cache
         k_cache, v_cache = kq, vq
         qkw = {"k_meta": km, "v_meta": vm,
-               "cache_dtype": akvs.AKVS_U4G64 if wl.cache_bits == 4 else akvs.AKVS_U2G64}
+               "cache_dtype": cache_dtype_for_bits(wl.cache_bits)}
     torch.cuda.synchronize()
     print("# unit caches built", file=sys.stderr, flush=True)
 

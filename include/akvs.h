@@ -30,7 +30,8 @@
  *    bitwise identical outputs.
  *  - dtypes: AKVS_F32 model = fp32 weights, activations and K/V; AKVS_BF16 model =
  *    bf16 weights and K/V, fp32 residual stream and accumulation. Quantised caches
- *    (AKVS_U4G64 / AKVS_U2G64) are only valid as cache inputs of a bf16 model.
+ *    (AKVS_U4G64 / AKVS_U2G64 / AKVS_E4M3G64) are only valid as cache inputs of a bf16
+ *    model.
  *
  * Layouts (L layers, D model width, Hq / Hkv heads, hd head dim, F FFN width,
  * kvw = Hkv*hd, T_c = sum of unit lengths, q = query length, T = T_c + q)
@@ -68,7 +69,7 @@ enum {
   AKVS_EHIP = 6          /* HIP runtime error while enqueueing                   */
 };
 
-enum { AKVS_F32 = 0, AKVS_BF16 = 1, AKVS_U4G64 = 2, AKVS_U2G64 = 3 };
+enum { AKVS_F32 = 0, AKVS_BF16 = 1, AKVS_U4G64 = 2, AKVS_U2G64 = 3, AKVS_E4M3G64 = 4 };
 
 /* akvs_reuse_cfg.flags */
 enum {
@@ -103,7 +104,8 @@ typedef struct akvs_reuse_cfg {
 typedef struct akvs_cache {
   const void *k, *v;
   const void *k_meta, *v_meta;
-  int32_t dtype; /* AKVS_F32 (f32 model), AKVS_BF16, AKVS_U4G64, AKVS_U2G64 (bf16 model) */
+  int32_t dtype; /* AKVS_F32 (f32 model), AKVS_BF16, AKVS_U4G64, AKVS_U2G64, AKVS_E4M3G64
+                    (bf16 model) */
 } akvs_cache;
 
 /* Outputs of akvs_reuse_prefill. h_query, k_corr, v_corr are required; the others
@@ -237,11 +239,16 @@ akvs_status akvs_probe_out_mlp(float *h, int32_t n_rows, const void *attn_out,
                                const akvs_model_cfg *m, const akvs_layer_w *lw, void *ws,
                                size_t ws_bytes, hipStream_t stream);
 
-/* Group-64 asymmetric quantiser of a cache (Sec. 4.5 composition with KV quantisation):
- * for each group of 64 head-dim elements: zero = fp16(min), scale = fp16((max-min) /
- * (2^bits - 1)) computed in fp32, code = clamp(rne((x - zero) / scale), 0, 2^bits - 1)
- * (0 when scale == 0). x: [n_rows][hd] of x_dtype (F32 or BF16), hd a multiple of 64;
- * codes: [n_rows][hd*bits/8]; meta: [n_rows][hd/64][2] fp16. bits: 2 or 4. */
+/* Group-64 quantiser of a cache (Sec. 4.5 composition with KV quantisation). For each
+ * group of 64 head-dim elements:
+ *   bits 2 / 4 (AKVS_U2G64 / AKVS_U4G64, asymmetric integer codes): zero = fp16(min),
+ *     scale = fp16((max-min) / (2^bits - 1)) computed in fp32,
+ *     code = clamp(rne((x - zero) / scale), 0, 2^bits - 1) (0 when scale == 0);
+ *   bits 8 (AKVS_E4M3G64, FP8 E4M3 codes): scale = fp16(max|x| / 448) computed in fp32,
+ *     zero = 0, code = E4M3 of clamp(x / scale, -448, 448) rounded half to even (OCP FP8
+ *     E4M3: bias 7, no infinity, 448 the largest finite value; 0 when scale == 0).
+ * x: [n_rows][hd] of x_dtype (F32 or BF16), hd a multiple of 64; codes:
+ * [n_rows][hd*bits/8]; meta: [n_rows][hd/64][2] fp16 (scale, zero). */
 akvs_status akvs_quantize_cache(const void *x, int32_t x_dtype, int32_t n_rows, int32_t head_dim,
                                 int32_t bits, uint8_t *codes, void *meta, hipStream_t stream);
 

@@ -19,7 +19,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libakvs.so")
 
 AKVS_OK, AKVS_EINVAL, AKVS_ESHAPE, AKVS_EDTYPE, AKVS_EUNSUPPORTED, AKVS_ENOSPACE, AKVS_EHIP = range(7)
-AKVS_F32, AKVS_BF16, AKVS_U4G64, AKVS_U2G64 = range(4)
+AKVS_F32, AKVS_BF16, AKVS_U4G64, AKVS_U2G64, AKVS_E4M3G64 = range(5)
 AKVS_F_NO_CORRECTION = 1
 AKVS_F_UNIT_WEIGHTS = 2
 AKVS_F_FRESH_IF_RECOMPUTED = 4

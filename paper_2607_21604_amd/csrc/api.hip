@@ -204,10 +204,11 @@ akvs_status check_cache(const akvs_cache *c, const akvs_model_cfg *m) {
   if (m->dtype == AKVS_F32) {
     REQUIRE(c->dtype == AKVS_F32, AKVS_EDTYPE, "an fp32 model needs an AKVS_F32 cache");
   } else {
-    REQUIRE(c->dtype == AKVS_BF16 || c->dtype == AKVS_U4G64 || c->dtype == AKVS_U2G64,
-            AKVS_EDTYPE, "a bf16 model needs an AKVS_BF16 / U4G64 / U2G64 cache");
+    REQUIRE(c->dtype == AKVS_BF16 || c->dtype == AKVS_U4G64 || c->dtype == AKVS_U2G64 ||
+                c->dtype == AKVS_E4M3G64,
+            AKVS_EDTYPE, "a bf16 model needs an AKVS_BF16 / U4G64 / U2G64 / E4M3G64 cache");
   }
-  if (c->dtype == AKVS_U4G64 || c->dtype == AKVS_U2G64) {
+  if (c->dtype == AKVS_U4G64 || c->dtype == AKVS_U2G64 || c->dtype == AKVS_E4M3G64) {
     REQUIRE(c->k_meta && c->v_meta, AKVS_EINVAL, "quantised cache needs k_meta and v_meta");
     REQUIRE(aligned16(c->k_meta) && aligned16(c->v_meta), AKVS_EINVAL, "meta not aligned");
   }
@@ -222,6 +223,7 @@ CacheLayer cache_layer(const akvs_cache *c, int l, long long t_ctx, int hkv, int
   if (c->dtype == AKVS_F32) row_bytes = (size_t)hd * 4;
   else if (c->dtype == AKVS_BF16) row_bytes = (size_t)hd * 2;
   else if (c->dtype == AKVS_U4G64) row_bytes = (size_t)hd / 2;
+  else if (c->dtype == AKVS_E4M3G64) row_bytes = (size_t)hd;
   else row_bytes = (size_t)hd / 4;
   const size_t lb = (size_t)rows * row_bytes;
   v.k = reinterpret_cast<const char *>(c->k) + (size_t)l * lb;
@@ -898,7 +900,7 @@ akvs_status akvs_probe_out_mlp(float *h, int32_t n_rows, const void *attn_out,
 akvs_status akvs_quantize_cache(const void *x, int32_t x_dtype, int32_t n_rows, int32_t head_dim,
                                 int32_t bits, uint8_t *codes, void *meta, hipStream_t stream) {
   REQUIRE(x_dtype == AKVS_F32 || x_dtype == AKVS_BF16, AKVS_EDTYPE, "x dtype");
-  REQUIRE(bits == 2 || bits == 4, AKVS_EINVAL, "bits must be 2 or 4");
+  REQUIRE(bits == 2 || bits == 4 || bits == 8, AKVS_EINVAL, "bits must be 2, 4 or 8 (E4M3)");
   REQUIRE(n_rows >= 0 && head_dim >= 64 && head_dim % 64 == 0, AKVS_EINVAL,
           "head_dim must be a positive multiple of 64");
   REQUIRE(x && codes && meta, AKVS_EINVAL, "NULL argument");

@@ -87,8 +87,18 @@ __device__ __forceinline__ float wave_min(float v) {
 struct CacheLayer {
   const void *k, *v;
   const _Float16 *k_meta, *v_meta;
-  int dtype;  // AKVS_F32 / AKVS_BF16 / AKVS_U4G64 / AKVS_U2G64
+  int dtype;  // AKVS_F32 / AKVS_BF16 / AKVS_U4G64 / AKVS_U2G64 / AKVS_E4M3G64
 };
+
+// Four E4M3 bytes of w, decoded by the gfx950 conversion (OCP FP8 E4M3), times scale.
+__device__ __forceinline__ void e4m3x4(uint32_t w, float scale, float *o) {
+  const f32x2_t a = __builtin_amdgcn_cvt_pk_f32_fp8((int)w, false);
+  const f32x2_t b = __builtin_amdgcn_cvt_pk_f32_fp8((int)w, true);
+  o[0] = a[0] * scale;
+  o[1] = a[1] * scale;
+  o[2] = b[0] * scale;
+  o[3] = b[1] * scale;
+}
 
 // 8 consecutive elements e0..e0+7 (e0 % 8 == 0) of row `row` (= token*Hkv + head).
 __device__ __forceinline__ void cache_load8(const void *base, const _Float16 *meta, int dtype,
@@ -101,7 +111,12 @@ __device__ __forceinline__ void cache_load8(const void *base, const _Float16 *me
     const size_t g = row * (size_t)(hd / 64) + (size_t)(e0 / 64);
     const float scale = (float)meta[2 * g];
     const float zero = (float)meta[2 * g + 1];
-    if (dtype == AKVS_U4G64) {
+    if (dtype == AKVS_E4M3G64) {
+      const uint2 w = *reinterpret_cast<const uint2 *>(reinterpret_cast<const uint8_t *>(base) +
+                                                       row * hd + e0);
+      e4m3x4(w.x, scale, o);
+      e4m3x4(w.y, scale, o + 4);
+    } else if (dtype == AKVS_U4G64) {
       const uint8_t *c = reinterpret_cast<const uint8_t *>(base) + row * (hd / 2) + e0 / 2;
       const uint32_t w = *reinterpret_cast<const uint32_t *>(c);
 #pragma unroll
@@ -123,6 +138,8 @@ __device__ __forceinline__ float cache_load1(const void *base, const _Float16 *m
   const float scale = (float)meta[2 * g];
   const float zero = (float)meta[2 * g + 1];
   const uint8_t *c = reinterpret_cast<const uint8_t *>(base);
+  if (dtype == AKVS_E4M3G64)
+    return __builtin_amdgcn_cvt_pk_f32_fp8((int)c[row * hd + e], false)[0] * scale;
   uint32_t code;
   if (dtype == AKVS_U4G64)
     code = (c[row * (hd / 2) + e / 2] >> (4 * (e & 1))) & 15u;

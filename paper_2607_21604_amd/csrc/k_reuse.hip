@@ -533,6 +533,22 @@ __global__ void k_quantize(const TX *x, int n_rows, int hd, int bits, uint8_t *c
   const long long row = gid / groups;
   const int grp = (int)(gid - row * groups);
   const float v = load1(x + row * hd + grp * 64 + lane);
+  if (bits == 8) {  // E4M3: symmetric, one fp16 scale per group
+    const float amax = wave_max(fabsf(v));
+    const _Float16 s16 = (_Float16)__fdiv_rn(amax, 448.f);
+    const float scale = (float)s16;
+    int code = 0;
+    if (scale != 0.f) {
+      const float t = fminf(fmaxf(__fdiv_rn(v, scale), -448.f), 448.f);
+      code = __builtin_amdgcn_cvt_pk_fp8_f32(t, 0.f, 0, false) & 0xff;
+    }
+    codes[row * hd + grp * 64 + lane] = (uint8_t)code;
+    if (lane == 0) {
+      meta[2 * gid] = s16;
+      meta[2 * gid + 1] = (_Float16)0.f;
+    }
+    return;
+  }
   const float mn = wave_min(v), mx = wave_max(v);
   const float levels = (float)((1 << bits) - 1);
   const _Float16 z16 = (_Float16)mn;

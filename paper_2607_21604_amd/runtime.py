@@ -144,8 +144,14 @@ def reuse_prefill_batch(engine: Engine, requests, refresh=(1, 5), check_layer: i
     return outputs
 
 
+def cache_dtype_for_bits(bits: int) -> int:
+    """Cache dtype code of a group-64 format: 4 / 2-bit integer or 8-bit FP8 E4M3."""
+    return {4: akvs.AKVS_U4G64, 2: akvs.AKVS_U2G64, 8: akvs.AKVS_E4M3G64}[bits]
+
+
 def quantize_cache(x: torch.Tensor, bits: int):
-    """Group-64 quantised copy of a cache [..][hd] (codes uint8, meta fp16 (scale, zero))."""
+    """Group-64 quantised copy of a cache [..][hd] (codes uint8, meta fp16 (scale, zero));
+    bits 4 / 2: integer codes, 8: FP8 E4M3 codes."""
     hd = x.shape[-1]
     rows = x.numel() // hd
     codes = torch.empty(x.shape[:-1] + (hd * bits // 8,), dtype=torch.uint8, device=x.device)

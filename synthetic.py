@@ -55,7 +55,7 @@ class Workload:
     chunk_lens: tuple
     query_len: int
     refresh: tuple          # refresh ratios as (num, den) pairs; first one is the headline
-    cache_bits: int = 16    # 16 = plain cache; 4 / 2 = group-64 quantised cache
+    cache_bits: int = 16    # 16 = plain cache; 4 / 2 = group-64 integer, 8 = group-64 FP8 E4M3
 
     @property
     def n_ctx(self) -> int:
@@ -81,7 +81,7 @@ def chunk_lengths(name: str, seed: int = 0) -> tuple:
     if name == "3b":
         rng = np.random.default_rng(seed + 2)
         return tuple(int(x) for x in rng.integers(192, 257, size=20))
-    if name in ("7b", "7b-q4", "7b-q2"):
+    if name in ("7b", "7b-q4", "7b-q2", "7b-fp8"):
         return (200,) * 40
     if name == "32b":
         return (200,) * 80
@@ -99,9 +99,9 @@ def workload(name: str, seed: int = 0) -> Workload:
     if name == "32b":
         return Workload(name, SHAPES["32b"], chunk_lengths(name, seed), 128,
                         ((1, 10), (3, 10)))
-    if name in ("7b-q4", "7b-q2"):
+    if name in ("7b-q4", "7b-q2", "7b-fp8"):
         return Workload(name, SHAPES["7b"], chunk_lengths(name, seed), 128, ((1, 5),),
-                        cache_bits=4 if name == "7b-q4" else 2)
+                        cache_bits={"7b-q4": 4, "7b-q2": 2, "7b-fp8": 8}[name])
     raise KeyError(name)
 
 

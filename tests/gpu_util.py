@@ -66,3 +66,15 @@ def check_valid_top_b(d_ref, d_gpu, probes_gpu, starts, lens, budgets, slack):
             assert tied_in.max() < tied_out.min()
         dr = np.asarray(d_ref[s:s + n])
         assert dr[inside].min() >= dr[~inside].max() - slack
+
+
+def oracle_quantized(x64, bits):
+    """A cache quantised by the oracle: (storage bytes, meta, dequantised values, dtype code)
+    for bits 4 / 2 (integer groups) or 8 (FP8 E4M3 groups)."""
+    from paper_2607_21604_amd import akvs
+    if bits == 8:
+        codes, meta = oracle.quantize_e4m3_g64(x64)
+        return codes, meta, oracle.dequantize_e4m3_g64(codes, meta), akvs.AKVS_E4M3G64
+    codes, meta = oracle.quantize_g64(x64, bits)
+    return (oracle.pack_codes(codes, bits), meta, oracle.dequantize_g64(codes, meta),
+            akvs.AKVS_U4G64 if bits == 4 else akvs.AKVS_U2G64)

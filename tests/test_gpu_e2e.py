@@ -7,7 +7,7 @@ import oracle
 import synthetic
 from paper_2607_21604_amd import akvs
 from paper_2607_21604_amd.runtime import Engine
-from tests.gpu_util import (DEV, to_dev, dev_weights, f64, max_rel, oracle_caches,
+from tests.gpu_util import (DEV, oracle_quantized, to_dev, dev_weights, f64, max_rel, oracle_caches,
                             check_valid_top_b)
 from tests.libutil import ensure_built
 
@@ -186,19 +186,15 @@ def test_7b_width_reuse_prefill(w7b):
     print("7b-width errors", errs)
 
 
-@pytest.mark.parametrize("bits", [4, 2])
+@pytest.mark.parametrize("bits", [4, 2, 8])
 def test_7b_width_quantised_cache(w7b, bits):
-    codes_k, meta_k = oracle.quantize_g64(f64(w7b.k_all), bits)
-    codes_v, meta_v = oracle.quantize_g64(f64(w7b.v_all), bits)
-    deq_k = oracle.dequantize_g64(codes_k, meta_k)
-    deq_v = oracle.dequantize_g64(codes_v, meta_v)
+    codes_k, meta_k, deq_k, dt = oracle_quantized(f64(w7b.k_all), bits)
+    codes_v, meta_v, deq_v, _ = oracle_quantized(f64(w7b.v_all), bits)
     kc = [deq_k[:, s:s + n] for s, n in zip(w7b.starts, w7b.lens)]
     vc = [deq_v[:, s:s + n] for s, n in zip(w7b.starts, w7b.lens)]
     ref = w7b.oracle(kc=kc, vc=vc)
     out = w7b.gpu(probes=(ref["probe_k"], ref["probe_v"]),
-                  k_cache=to_dev(oracle.pack_codes(codes_k, bits)),
-                  v_cache=to_dev(oracle.pack_codes(codes_v, bits)),
-                  k_meta=to_dev(meta_k), v_meta=to_dev(meta_v),
-                  cache_dtype=akvs.AKVS_U4G64 if bits == 4 else akvs.AKVS_U2G64)
+                  k_cache=to_dev(codes_k), v_cache=to_dev(codes_v),
+                  k_meta=to_dev(meta_k), v_meta=to_dev(meta_v), cache_dtype=dt)
     errs = w7b.compare(out, ref)
     print(f"7b-width {bits}-bit errors", errs)

@@ -6,7 +6,7 @@ import torch
 import oracle
 import synthetic
 from paper_2607_21604_amd import akvs
-from tests.gpu_util import DEV, to_dev, f64, max_rel, storage_round
+from tests.gpu_util import DEV, to_dev, f64, max_rel, storage_round, oracle_quantized
 from tests.libutil import ensure_built
 
 pytestmark = pytest.mark.gpu
@@ -59,19 +59,17 @@ def test_rerotate_keys(dtype, hkv, hd):
     assert torch.equal(kd.cpu(), k)
 
 
-@pytest.mark.parametrize("bits", [4, 2])
+@pytest.mark.parametrize("bits", [4, 2, 8])
 def test_rerotate_quantised_cache(bits):
     lens = [64, 70]
     starts, delta = unit_layout(lens)
     n, hkv, hd = 134, 4, 128
     x = storage_round(synthetic.random_array((2, n, hkv, hd), 3), torch.bfloat16)
-    codes, meta = oracle.quantize_g64(f64(x), bits)
-    packed = oracle.pack_codes(codes, bits)
-    deq = oracle.dequantize_g64(codes, meta)
+    packed, meta, deq, dt = oracle_quantized(f64(x), bits)
     tab = rope(n, hd, 1e6)
     kd = torch.empty((n, hkv, hd), dtype=torch.bfloat16, device=DEV)
     vd = torch.empty_like(kd)
-    cache = akvs.Cache(0, 0, 0, 0, akvs.AKVS_U4G64 if bits == 4 else akvs.AKVS_U2G64)
+    cache = akvs.Cache(0, 0, 0, 0, dt)
     kq, vq = to_dev(packed[0]), to_dev(packed[1])
     km, vm = to_dev(meta[0]), to_dev(meta[1])
     cache.k, cache.v, cache.k_meta, cache.v_meta = kq.data_ptr(), vq.data_ptr(), km.data_ptr(), vm.data_ptr()
@@ -362,6 +360,42 @@ def test_probe_qkv_and_out_mlp(name, n_rows):
     akvs.akvs_probe_out_mlp(h_dev, n_rows, to_dev(att), m, lws, ws)
     ref = oracle.model.output_and_mlp(h32.astype(np.float64), f64(att), sw, dims)
     assert max_rel(f64(h_dev), ref) < tol
+
+
+def test_e4m3_cache_decodes_every_byte():
+    """All 256 E4M3 bytes through the library's cache reader (the V copy of the
+    re-rotation entry, scale 1): each gives the value of the format's definition."""
+    hkv, hd, n = 1, 128, 2
+    codes = np.arange(256, dtype=np.uint8).reshape(n, hkv, hd)
+    meta = np.zeros((n, hkv, 2, 2), np.float16)
+    meta[..., 0] = 1.0
+    cache = akvs.Cache(0, 0, 0, 0, akvs.AKVS_E4M3G64)
+    kq, vq, km = to_dev(codes), to_dev(codes), to_dev(meta)
+    cache.k, cache.v, cache.k_meta, cache.v_meta = kq.data_ptr(), vq.data_ptr(), km.data_ptr(), km.data_ptr()
+    kd = torch.empty((n, hkv, hd), dtype=torch.bfloat16, device=DEV)  # holds E4M3 values exactly
+    vd = torch.empty_like(kd)
+    akvs.akvs_rerotate_keys(cache, n, hkv, hd, to_dev(np.zeros(n, np.int32)), rope(n, hd, 1e6), n,
+                            kd, vd, akvs.AKVS_BF16)
+    got = vd.float().cpu().numpy().reshape(-1).astype(np.float64)
+    ref = oracle.e4m3_value(np.arange(256))
+    np.testing.assert_array_equal(np.isnan(got), np.isnan(ref))
+    np.testing.assert_array_equal(got[~np.isnan(ref)], ref[~np.isnan(ref)])
+
+
+def test_quantize_e4m3_bit_exact():
+    x = storage_round(synthetic.random_array((300, 128), 48), torch.bfloat16)
+    x[7, :64] = 0.0           # all-zero group: scale 0, codes 0
+    x[9, 64:] = 1e-3          # constant group
+    pos = oracle.e4m3_value(np.arange(0x7F))
+    mids = ((pos[:-1] + pos[1:]) / 2)[-63:]     # ties between neighbours, scale exactly 1
+    x[11, :64] = torch.from_numpy(np.concatenate([[448.0], mids]))
+    x[12, :64] = -x[11, :64]
+    codes, meta = oracle.quantize_e4m3_g64(f64(x))
+    c = torch.empty((300, 128), dtype=torch.uint8, device=DEV)
+    mt = torch.empty((300, 2, 2), dtype=torch.float16, device=DEV)
+    akvs.akvs_quantize_cache(to_dev(x), 300, 128, 8, c, mt)
+    np.testing.assert_array_equal(c.cpu().numpy(), codes)
+    np.testing.assert_array_equal(mt.cpu().numpy().view(np.uint16), meta.view(np.uint16))
 
 
 @pytest.mark.parametrize("bits", [4, 2])
