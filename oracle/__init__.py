@@ -2,7 +2,7 @@
 
 TEST INFRASTRUCTURE ONLY. This package is a plain, slow, fp64 NumPy statement of
 what the reuse-prefill path computes (the decoder, full prefill, standalone unit
-caching, the probe-guided residual correction of Sec. 3.3 / Algorithm 1, and the
+caching, the first decode step over the reused caches, the probe-guided residual correction of Sec. 3.3 / Algorithm 1, and the
 group-64 cache quantisers: 2/4-bit integer and FP8 E4M3). Only the tests, the smoke check and the benchmark's
 CPU-baseline leg may import it; the library path never does, and it shares no
 code with the HIP kernels.
@@ -11,7 +11,8 @@ Every function cites the passage of the paper it follows. Readings of passages
 the paper leaves open are listed in the design notes of the repository.
 """
 from .model import (ModelDims, dims_from, rms_norm, rope_cos_sin, rotate, attention,
-                    decoder_layer, full_prefill, cache_units, split_layer)
+                    decoder_layer, full_prefill, cache_units, split_layer, lm_logits,
+                    greedy_token, decode_step)
 from .reuse import (F_NO_CORRECTION, F_UNIT_WEIGHTS, F_FRESH_IF_RECOMPUTED,
                     F_NO_PREFIX_RECOMPUTE, probe_budget, chunk_starts, rerotate,
                     divergence, select_top, correction_weights, probe_offset,

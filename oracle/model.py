@@ -196,3 +196,43 @@ def cache_units(tokens, chunk_lens, weights: dict, dims: ModelDims, layers=None)
         vc.append(v)
         s += n
     return kc, vc
+
+
+def lm_logits(h_final: np.ndarray, weights: dict, lm_head=None) -> np.ndarray:
+    """Next-token logits of final-normed rows: h W^T over the vocabulary. W is the output
+    embedding; the 3B-class decoders the paper evaluates tie it to the input embedding,
+    which is the default here (`lm_head` passes an untied [V][D] table)."""
+    w = _f64(lm_head if lm_head is not None else weights["embed"])
+    return np.asarray(h_final, dtype=np.float64) @ w.T
+
+
+def greedy_token(logits: np.ndarray) -> int:
+    """The largest logit's index (equal values: the lowest index)."""
+    return int(np.argmax(logits))
+
+
+def decode_step(token: int, k_past, v_past, weights: dict, dims: ModelDims, layers=None,
+                lm_head=None):
+    """One generated token on top of per-layer past keys/values [L][n][Hkv][hd] at
+    positions 0..n-1 (after a reuse prefill: its corrected caches). The token sits at
+    position n; in every layer it attends to the n past keys and to its own.
+
+    Returns (final-normed hidden [D], logits [V], k_new [L][Hkv][hd], v_new [L][Hkv][hd]).
+    """
+    n = np.asarray(k_past[0]).shape[0]
+    if layers is None:
+        layers = [split_layer(lw, dims) for lw in weights["layers"][:dims.n_layers]]
+    h = embed(weights, [token])
+    pos = np.array([n])
+    key_pos = np.arange(n + 1)
+    ks, vs = [], []
+    for l, w in enumerate(layers):
+        q, k, v = project_qkv(h, pos, w, dims)
+        kk = np.concatenate([np.asarray(k_past[l], dtype=np.float64), k])
+        vv = np.concatenate([np.asarray(v_past[l], dtype=np.float64), v])
+        o = attention(q, pos, kk, vv, key_pos)
+        h = output_and_mlp(h, o, w, dims)
+        ks.append(k[0])
+        vs.append(v[0])
+    hf = rms_norm(h, _f64(weights["final_norm"]), dims.rms_eps)
+    return hf[0], lm_logits(hf, weights, lm_head)[0], np.stack(ks), np.stack(vs)

@@ -114,3 +114,37 @@ def test_lemma1_halved_constant_is_violated():
     halved = 1.0 * 2.0 / (2 * np.sqrt(d)) * eps
     assert err > 1.9 * halved
     assert err <= 2.0 / np.sqrt(d) * eps * (1 + 1e-6)
+
+
+def test_decode_step_is_the_next_row_of_a_full_prefill():
+    """On the caches of an ordinary prefill, one decode step gives exactly what a prefill
+    of one more token gives for that token (hidden row, logits, its K and V)."""
+    dims, w, V = small_model(seed=11)
+    toks = context(11, [17], 3, V)
+    n = len(toks) - 1
+    _, k, v = oracle.full_prefill(toks[:n], 0, w, dims)
+    h1, logits, kn, vn = oracle.decode_step(int(toks[n]), k, v, w, dims)
+    h_all, k_all, v_all = oracle.full_prefill(toks, 0, w, dims)
+    np.testing.assert_allclose(h1, h_all[n], rtol=0, atol=1e-12)
+    np.testing.assert_allclose(kn, k_all[:, n], rtol=0, atol=1e-12)
+    np.testing.assert_allclose(vn, v_all[:, n], rtol=0, atol=1e-12)
+    np.testing.assert_allclose(logits, h_all[n] @ np.asarray(w["embed"]).T, rtol=0, atol=1e-10)
+
+
+def test_decode_step_on_arbitrary_caches_matches_transformers_llama():
+    """Past K/V that no prefill produced (as after a reuse prefill): the transformers
+    Llama run with them as its cache gives the same hidden row."""
+    dims, w, V = small_model(seed=12, hq=6, hkv=2, hd=16, D=48)
+    rng = np.random.default_rng(12)
+    n = 23
+    k = rng.standard_normal((dims.n_layers, n, dims.n_kv_heads, dims.head_dim))
+    v = rng.standard_normal((dims.n_layers, n, dims.n_kv_heads, dims.head_dim))
+    tok = 5
+    h1, logits, _, _ = oracle.decode_step(tok, k, v, w, dims)
+    ref = hf_llama.continue_from(hf_llama.build(w, dims, V), k, v, [tok], n)[0]
+    close_to(h1, ref, 1e-5)
+    assert oracle.greedy_token(logits) == int(np.argmax(ref @ np.asarray(w["embed"]).T))
+
+
+def test_greedy_token_takes_the_lowest_index_of_equal_maxima():
+    assert oracle.greedy_token(np.array([0.5, 2.0, -1.0, 2.0])) == 1
