@@ -43,6 +43,7 @@ def parse():
     p.add_argument("--batch-sweep", default="auto",
                    help="comma-separated batch sizes for the batched reuse prefill leg "
                         "(auto: 4,8,16 for 3b; none elsewhere)")
+    p.add_argument("--no-decode", action="store_true", help="skip the decode-step leg")
     p.add_argument("--check-layer", type=int, default=1)
     p.add_argument("--seed", type=int, default=0)
     p.add_argument("--no-cpu-baseline", action="store_true")
@@ -386,6 +387,48 @@ def main():
         print(f"# reuse at r={r}: {ms_r:.3f} ms/step, M={m_r}", file=sys.stderr, flush=True)
         del o2
 
+    # first decode step over the corrected caches: the next token from the last query row,
+    # then one generated token through every layer (weights read once: HBM-bound)
+    decode = None
+    if not args.no_decode:
+        T = wl.n_tokens
+        out_d = eng.reuse_prefill(toks, wl.chunk_lens, wl.query_len, k_cache, v_cache, (num, den),
+                                  args.check_layer, 0, kv_rows=T + 1, **qkw)
+        _, tok0 = eng.lm_head(out_d["h_query"][-1:].contiguous())
+        lg_buf = torch.empty(shape.vocab, dtype=torch.float32, device=dev)
+        nt_buf = torch.empty(1, dtype=torch.int32, device=dev)
+
+        def dstep():
+            eng.decode_step(tok0, T, out_d["k_corr"], out_d["v_corr"], logits=lg_buf,
+                            next_token=nt_buf)
+
+        dstep()
+        torch.cuda.synchronize()
+        ms_dec_eager = timed(dstep)
+        ms_dec = None
+        if not args.no_graph:
+            g_dec = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g_dec):
+                dstep()
+            ms_dec = timed(g_dec.replay)
+            del g_dec
+        ms_d = ms_dec or ms_dec_eager
+        D, F = shape.d_model, shape.ffn_dim
+        w_bytes = 2.0 * (shape.n_layers * (shape.qkv_width * D + D * shape.n_q_heads * shape.head_dim
+                                           + 3 * F * D) + shape.vocab * D)
+        kv_bytes = 2.0 * 2 * shape.n_layers * (T + 1) * shape.kv_width
+        decode = {"ms_per_token": ms_d, "ms_per_token_eager": ms_dec_eager,
+                  "timing": "HIP-graph replay" if ms_dec else "eager calls",
+                  "hbm_bytes_per_token": w_bytes + kv_bytes,
+                  "achieved_GBps": (w_bytes + kv_bytes) / (ms_d * 1e-3) / 1e9,
+                  "peak_GBps": HBM_PEAK_GBS,
+                  "frac": (w_bytes + kv_bytes) / (ms_d * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                  "note": "weights of every layer and the tied output embedding read once, plus "
+                          "the corrected keys and values of all T tokens"}
+        print(f"# decode step over the corrected caches: {ms_d:.3f} ms/token "
+              f"({decode['achieved_GBps']:.0f} GB/s)", file=sys.stderr, flush=True)
+        del out_d
+
     # batched reuse prefill: B requests of this workload's shape (same unit lengths, their
     # own token ids and unit caches) in one call, whose projections run over all requests'
     # recomputed rows at once
@@ -479,6 +522,7 @@ def main():
         "kernels": kernels,
         "refresh_sweep": sweep,
         "batch_sweep": batch,
+        "decode_step": decode,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line))

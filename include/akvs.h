@@ -117,6 +117,8 @@ typedef struct akvs_reuse_out {
   float *d_k, *d_v;        /* [T_c] check-layer divergences                          */
   int32_t *rows;           /* [T] recomputed positions, ascending; first n_rows used  */
   int32_t *n_rows;         /* [1] number of recomputed rows M                        */
+  int32_t kv_rows;         /* rows per layer of k_corr / v_corr: 0 means T; a larger
+                              value leaves room for the tokens a decode step appends */
 } akvs_reuse_out;
 
 /* ---- library information ---------------------------------------------------- */
@@ -293,6 +295,37 @@ akvs_status akvs_full_prefill(const int32_t *tokens, int32_t n_tokens, int32_t p
                               const akvs_model_cfg *m, float *h_out, void *k_out, void *v_out,
                               void *ws, size_t ws_bytes, hipStream_t stream);
 
+/* ---- first decode step over the corrected caches -------------------------------------
+ * The consumer of a reuse prefill: the next token is predicted from the last final-normed
+ * query row, then generated tokens run through every layer attending to the corrected
+ * keys and values (Sec. 3.1: the reused states serve the generation that follows). The
+ * output embedding w_out is [vocab][D] in the model dtype; NULL means tied to the input
+ * embedding (as in the 3B-class decoders the paper evaluates). Greedy pick: the largest
+ * logit, equal values resolved to the lowest index, -1 if no logit is a number. */
+
+/* Workspace of akvs_decode_step with n_past cached tokens (also enough for akvs_lm_head
+ * when n_past >= 0). 0 for an invalid model. */
+size_t akvs_decode_workspace_size(const akvs_model_cfg *m, int32_t n_past);
+
+/* logits[r][:] = h[r] . w_out^T and tokens[r] = greedy pick, r < n_rows. h: device
+ * [n_rows][D] fp32 final-normed rows (e.g. the last row of h_query); logits (device
+ * [n_rows][vocab] fp32) or tokens (device [n_rows]) may be NULL, not both. */
+akvs_status akvs_lm_head(const float *h, int32_t n_rows, const void *w_out,
+                         const akvs_model_cfg *m, float *logits, int32_t *tokens, void *ws,
+                         size_t ws_bytes, hipStream_t stream);
+
+/* One decode step: token (device [1]) at position n_past. k_cache, v_cache: device
+ * [L][cache_rows][Hkv][hd] model dtype, rows 0..n_past-1 valid (e.g. the k_corr / v_corr
+ * of a reuse prefill written with kv_rows = cache_rows); the step writes the token's
+ * post-RoPE key and value to row n_past of every layer. Outputs logits (device [vocab]
+ * fp32, may be NULL) and next_token (device [1], may be NULL). Errors: EINVAL for
+ * n_past < 0 or cache_rows <= n_past, null or misaligned pointers; ENOSPACE. */
+akvs_status akvs_decode_step(const int32_t *token, int32_t n_past, const void *embed,
+                             const akvs_layer_w *lw, const void *final_norm, const void *w_out,
+                             const akvs_model_cfg *m, void *k_cache, void *v_cache,
+                             int32_t cache_rows, float *logits, int32_t *next_token, void *ws,
+                             size_t ws_bytes, hipStream_t stream);
+
 /* ---- kernel timing -------------------------------------------------------------------
  * akvs_profile_enable(mask): for every kernel class whose bit (1 << class) is set in
  * mask, the library brackets each launch of that class with a pair of HIP events
@@ -303,7 +336,7 @@ akvs_status akvs_full_prefill(const int32_t *tokens, int32_t n_tokens, int32_t p
 enum {
   AKVS_K_GEMM = 0, AKVS_K_ATTENTION = 1, AKVS_K_CORRECTION = 2, AKVS_K_OFFSET = 3,
   AKVS_K_DIVERGENCE = 4, AKVS_K_SELECT = 5, AKVS_K_NORM = 6, AKVS_K_OTHER = 7,
-  AKVS_K_NCLASSES = 8
+  AKVS_K_GEMV = 8, AKVS_K_NCLASSES = 9
 };
 akvs_status akvs_profile_enable(int32_t class_mask);
 akvs_status akvs_profile_read(int32_t kernel_class, int64_t *launches, double *total_ms);

@@ -26,7 +26,7 @@ AKVS_F_FRESH_IF_RECOMPUTED = 4
 AKVS_F_NO_PREFIX_RECOMPUTE = 8
 AKVS_F_GIVEN_PROBES = 16
 (AKVS_K_GEMM, AKVS_K_ATTENTION, AKVS_K_CORRECTION, AKVS_K_OFFSET, AKVS_K_DIVERGENCE,
- AKVS_K_SELECT, AKVS_K_NORM, AKVS_K_OTHER) = range(8)
+ AKVS_K_SELECT, AKVS_K_NORM, AKVS_K_OTHER, AKVS_K_GEMV) = range(9)
 KERNEL_CLASSES = ("gemm", "attention", "correction", "offset", "divergence", "select", "norm",
                   "other")
 
@@ -66,7 +66,7 @@ class ReuseOut(ctypes.Structure):
     _fields_ = [("h_query", ctypes.c_void_p), ("k_corr", ctypes.c_void_p),
                 ("v_corr", ctypes.c_void_p), ("probe_k", ctypes.c_void_p),
                 ("probe_v", ctypes.c_void_p), ("d_k", ctypes.c_void_p), ("d_v", ctypes.c_void_p),
-                ("rows", ctypes.c_void_p), ("n_rows", ctypes.c_void_p)]
+                ("rows", ctypes.c_void_p), ("n_rows", ctypes.c_void_p), ("kv_rows", ctypes.c_int32)]
 
 
 _P = ctypes.c_void_p
@@ -108,6 +108,10 @@ _SIGS = {
                                                     ctypes.POINTER(ReuseCfg), _I]),
     "akvs_full_prefill": (_I, [_P, _I, _I, _P, ctypes.POINTER(LayerW), _P, ctypes.POINTER(ModelCfg),
                                _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "akvs_decode_workspace_size": (ctypes.c_size_t, [ctypes.POINTER(ModelCfg), _I]),
+    "akvs_lm_head": (_I, [_P, _I, _P, ctypes.POINTER(ModelCfg), _P, _P, _P, ctypes.c_size_t, _P]),
+    "akvs_decode_step": (_I, [_P, _I, _P, ctypes.POINTER(LayerW), _P, _P, ctypes.POINTER(ModelCfg),
+                              _P, _P, _I, _P, _P, _P, ctypes.c_size_t, _P]),
     "akvs_profile_enable": (_I, [_I]),
     "akvs_profile_read": (_I, [_I, ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_double)]),
 }
@@ -336,6 +340,25 @@ def akvs_full_prefill(tokens, n_tokens, pos0, embed, layers: ctypes.Array, final
                                     ctypes.byref(m), ptr(h_out), ptr(k_out), ptr(v_out), ptr(ws),
                                     ws.numel() * ws.element_size(), stream_handle(stream)),
            "akvs_full_prefill")
+
+
+def akvs_decode_workspace_size(m: ModelCfg, n_past: int) -> int:
+    return load().akvs_decode_workspace_size(ctypes.byref(m), int(n_past))
+
+
+def akvs_lm_head(h, n_rows, w_out, m: ModelCfg, logits, tokens, ws, stream=None):
+    _check(load().akvs_lm_head(ptr(h), int(n_rows), ptr(w_out), ctypes.byref(m), ptr(logits),
+                               ptr(tokens), ptr(ws), ws.numel() * ws.element_size(),
+                               stream_handle(stream)), "akvs_lm_head")
+
+
+def akvs_decode_step(token, n_past, embed, layers: ctypes.Array, final_norm, w_out, m: ModelCfg,
+                     k_cache, v_cache, cache_rows, logits, next_token, ws, stream=None):
+    _check(load().akvs_decode_step(ptr(token), int(n_past), ptr(embed), layers, ptr(final_norm),
+                                   ptr(w_out), ctypes.byref(m), ptr(k_cache), ptr(v_cache),
+                                   int(cache_rows), ptr(logits), ptr(next_token), ptr(ws),
+                                   ws.numel() * ws.element_size(), stream_handle(stream)),
+           "akvs_decode_step")
 
 
 def akvs_profile_enable(class_mask: int):

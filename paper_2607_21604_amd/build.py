@@ -14,7 +14,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libakvs.so")
-SOURCES = ["api.hip", "k_misc.hip", "k_reuse.hip", "k_gemm.hip", "k_attn.hip"]
+SOURCES = ["api.hip", "k_misc.hip", "k_reuse.hip", "k_gemm.hip", "k_attn.hip", "k_decode.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 # Packed fp32 instructions are kept out of the generated code on purpose.

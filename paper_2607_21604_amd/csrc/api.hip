@@ -984,7 +984,9 @@ akvs_status akvs_reuse_prefill(const int32_t *tokens, const void *embed, const a
   const bool no_prefix = (cfg->flags & AKVS_F_NO_PREFIX_RECOMPUTE) != 0;
   const int c = no_prefix ? 0 : cfg->check_layer;
   const size_t es = es_of(m->dtype);
-  const size_t corr_layer = (size_t)T * kvw * es;
+  REQUIRE(out->kv_rows == 0 || out->kv_rows >= T, AKVS_EINVAL,
+          "kv_rows %d is below T = %d", out->kv_rows, T);
+  const size_t corr_layer = (size_t)(out->kv_rows ? out->kv_rows : T) * kvw * es;
   char *k_corr = reinterpret_cast<char *>(out->k_corr);
   char *v_corr = reinterpret_cast<char *>(out->v_corr);
 
@@ -1096,6 +1098,8 @@ akvs_status akvs_reuse_prefill_batch(const int32_t *const *tokens, int32_t batch
             "request %d: misaligned output", i);
     REQUIRE(!(cfgs[i].flags & AKVS_F_GIVEN_PROBES) || (o.probe_k && o.probe_v), AKVS_EINVAL,
             "request %d: AKVS_F_GIVEN_PROBES needs out->probe_k and out->probe_v", i);
+    REQUIRE(o.kv_rows == 0 || o.kv_rows >= pl.mt[i].t_all, AKVS_EINVAL,
+            "request %d: kv_rows below its token count", i);
   }
   BatchBufs b;
   const size_t need = carve_batch(nullptr, m, cfgs, batch, pl, b);
@@ -1126,7 +1130,7 @@ akvs_status akvs_reuse_prefill_batch(const int32_t *const *tokens, int32_t batch
     BatchReq &r = b.req[i];
     const akvs_reuse_cfg &cf = cfgs[i];
     const int T = (int)mt.t_all, Tc = (int)mt.t_ctx, nch = cf.n_chunks;
-    const size_t corr_layer = (size_t)T * kvw * es;
+    const size_t corr_layer = (size_t)(outs[i].kv_rows ? outs[i].kv_rows : T) * kvw * es;
     char *k_corr = reinterpret_cast<char *>(outs[i].k_corr);
     char *v_corr = reinterpret_cast<char *>(outs[i].v_corr);
     LAUNCH(AKVS_K_OTHER, put_ints(mt.m.data(), mt.m.size(), r.meta, stream));
@@ -1176,7 +1180,7 @@ akvs_status akvs_reuse_prefill_batch(const int32_t *const *tokens, int32_t batch
       BatchReq &r = b.req[i];
       const akvs_reuse_cfg &cf = cfgs[i];
       const int T = (int)mt.t_all, Tc = (int)mt.t_ctx, nch = cf.n_chunks, cap = (int)mt.row_cap;
-      const size_t corr_layer = (size_t)T * kvw * es;
+      const size_t corr_layer = (size_t)(outs[i].kv_rows ? outs[i].kv_rows : T) * kvw * es;
       CacheLayer cl = cache_layer(&caches[i], l, Tc, hkv, hd);
       LAUNCH(AKVS_K_OFFSET,
              launch_chunk_offset(b.k_fresh, b.v_fresh, m->dtype, r.fresh_row, cl, r.meta, nch,
@@ -1227,6 +1231,144 @@ akvs_status akvs_reuse_prefill_batch(const int32_t *const *tokens, int32_t batch
     q_off += cfgs[i].query_len;
   }
   return AKVS_OK;
+}
+
+// ---- first decode step -----------------------------------------------------------------
+
+struct DecodeBufs {
+  float *rope, *h, *hf, *logits, *part_val, *part_o, *part_ml;
+  int32_t *part_idx;
+  void *x, *q, *att, *act;
+  long long part_rows;
+};
+
+static size_t carve_decode(void *ws, const akvs_model_cfg *m, long long n_keys, DecodeBufs &b) {
+  Carver cv(ws);
+  const size_t es = es_of(m->dtype);
+  const int D = m->d_model, F = m->ffn_dim, hqw = m->n_q_heads * m->head_dim;
+  b.rope = cv.take<float>((size_t)m->head_dim);
+  b.h = cv.take<float>((size_t)D);
+  b.hf = cv.take<float>((size_t)D);
+  b.logits = cv.take<float>((size_t)m->vocab);
+  b.part_val = cv.take<float>((size_t)gemv_blocks(m->vocab));
+  b.part_idx = cv.take<int32_t>((size_t)gemv_blocks(m->vocab));
+  b.x = cv.take<char>((size_t)D * es);
+  b.q = cv.take<char>((size_t)hqw * es);
+  b.att = cv.take<char>((size_t)hqw * es);
+  b.act = cv.take<char>((size_t)F * es);
+  size_t ml;
+  const size_t o = attention_part_floats(m, 1, n_keys, &ml);
+  b.part_o = o ? cv.take<float>(o) : nullptr;
+  b.part_ml = o ? cv.take<float>(ml) : nullptr;
+  b.part_rows = o ? (long long)(o / ((size_t)m->n_q_heads * m->head_dim)) : 0;
+  return cv.off;
+}
+
+static GemvEpi gemv_epi(int mode) {
+  GemvEpi e{};
+  e.mode = mode;
+  return e;
+}
+
+// Logits and greedy token of one final-normed row (fp32 [D]).
+static akvs_status lm_head_row(const akvs_model_cfg *m, const float *hf, const void *w_out,
+                               float *logits, float *part_val, int32_t *part_idx,
+                               int32_t *token, hipStream_t stream) {
+  GemvEpi e = gemv_epi(GV_LOGITS);
+  e.out_f32 = logits;
+  e.part_val = part_val;
+  e.part_idx = part_idx;
+  LAUNCH(AKVS_K_GEMV, launch_gemv(hf, AKVS_F32, w_out, m->dtype, m->vocab, m->d_model, e, stream));
+  if (token) LAUNCH(AKVS_K_OTHER, launch_pick(part_val, part_idx, gemv_blocks(m->vocab), token, stream));
+  return AKVS_OK;
+}
+
+size_t akvs_decode_workspace_size(const akvs_model_cfg *m, int32_t n_past) {
+  if (check_model(m) != AKVS_OK || n_past < 0) return 0;
+  DecodeBufs b;
+  return carve_decode(nullptr, m, (long long)n_past + 1, b);
+}
+
+akvs_status akvs_lm_head(const float *h, int32_t n_rows, const void *w_out,
+                         const akvs_model_cfg *m, float *logits, int32_t *tokens, void *ws,
+                         size_t ws_bytes, hipStream_t stream) {
+  akvs_status st = check_model(m);
+  if (st) return st;
+  REQUIRE(n_rows >= 0, AKVS_EINVAL, "n_rows must be >= 0");
+  REQUIRE(h && w_out && (logits || tokens), AKVS_EINVAL, "NULL argument");
+  REQUIRE(aligned16(h) && aligned16(w_out) && aligned16(ws) && (!logits || aligned16(logits)),
+          AKVS_EINVAL, "misaligned argument");
+  DecodeBufs b;
+  const size_t need = carve_decode(nullptr, m, 1, b);
+  REQUIRE(ws && ws_bytes >= need, AKVS_ENOSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+  carve_decode(ws, m, 1, b);
+  for (int r = 0; r < n_rows; ++r) {
+    float *lg = logits ? logits + (size_t)r * m->vocab : b.logits;
+    st = lm_head_row(m, h + (size_t)r * m->d_model, w_out, lg, b.part_val, b.part_idx,
+                     tokens ? tokens + r : nullptr, stream);
+    if (st) return st;
+  }
+  return AKVS_OK;
+}
+
+akvs_status akvs_decode_step(const int32_t *token, int32_t n_past, const void *embed,
+                             const akvs_layer_w *lw, const void *final_norm, const void *w_out,
+                             const akvs_model_cfg *m, void *k_cache, void *v_cache,
+                             int32_t cache_rows, float *logits, int32_t *next_token, void *ws,
+                             size_t ws_bytes, hipStream_t stream) {
+  akvs_status st = check_model(m);
+  if (st) return st;
+  if ((st = check_layers(m, lw))) return st;
+  REQUIRE(n_past >= 0 && cache_rows >= n_past + 1, AKVS_EINVAL,
+          "need 0 <= n_past < cache_rows (n_past %d, cache_rows %d)", n_past, cache_rows);
+  REQUIRE(token && embed && final_norm && k_cache && v_cache, AKVS_EINVAL, "NULL argument");
+  REQUIRE(aligned16(embed) && aligned16(final_norm) && aligned16(k_cache) &&
+              aligned16(v_cache) && aligned16(ws) && (!w_out || aligned16(w_out)) &&
+              (!logits || aligned16(logits)),
+          AKVS_EINVAL, "misaligned argument");
+  DecodeBufs b;
+  const size_t need = carve_decode(nullptr, m, (long long)n_past + 1, b);
+  REQUIRE(ws && ws_bytes >= need, AKVS_ENOSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+  carve_decode(ws, m, (long long)n_past + 1, b);
+  const int D = m->d_model, F = m->ffn_dim, hkv = m->n_kv_heads, hd = m->head_dim;
+  const int hqw = m->n_q_heads * hd, kvw = hkv * hd, qkvw = hqw + 2 * kvw;
+  const size_t es = es_of(m->dtype);
+  const size_t layer_bytes = (size_t)cache_rows * kvw * es;
+  LAUNCH(AKVS_K_OTHER, launch_rope_table(n_past, 1, hd, (double)m->rope_theta, b.rope, stream));
+  LAUNCH(AKVS_K_OTHER, launch_embed(token, 1, embed, m->dtype, m->vocab, D, b.h, stream));
+  for (int l = 0; l < m->n_layers; ++l) {
+    char *kl = reinterpret_cast<char *>(k_cache) + l * layer_bytes;
+    char *vl = reinterpret_cast<char *>(v_cache) + l * layer_bytes;
+    LAUNCH(AKVS_K_NORM, launch_rmsnorm(b.h, D, 1, nullptr, nullptr, lw[l].attn_norm, m->dtype, D,
+                                       m->rms_eps, b.x, m->dtype, D, stream));
+    GemvEpi e = gemv_epi(GV_QKV);
+    e.out_dtype = m->dtype;
+    e.q_out = b.q;
+    e.k_out = kl + (size_t)n_past * kvw * es;
+    e.v_out = vl + (size_t)n_past * kvw * es;
+    e.hq_w = hqw;
+    e.kv_w = kvw;
+    e.hd = hd;
+    e.rope = reinterpret_cast<const float2 *>(b.rope);
+    LAUNCH(AKVS_K_GEMV, launch_gemv(b.x, m->dtype, lw[l].w_qkv, m->dtype, qkvw, D, e, stream));
+    LAUNCH(AKVS_K_ATTENTION, launch_attention(b.q, nullptr, n_past, 1, nullptr, kl, vl, n_past + 1,
+                                              m->n_q_heads, hkv, hd, m->dtype, b.att, b.part_o,
+                                              b.part_ml, b.part_rows, stream));
+    GemvEpi r = gemv_epi(GV_RESID);
+    r.out_f32 = b.h;
+    LAUNCH(AKVS_K_GEMV, launch_gemv(b.att, m->dtype, lw[l].w_o, m->dtype, D, hqw, r, stream));
+    LAUNCH(AKVS_K_NORM, launch_rmsnorm(b.h, D, 1, nullptr, nullptr, lw[l].mlp_norm, m->dtype, D,
+                                       m->rms_eps, b.x, m->dtype, D, stream));
+    GemvEpi g = gemv_epi(GV_SWIGLU);
+    g.out = b.act;
+    g.out_dtype = m->dtype;
+    LAUNCH(AKVS_K_GEMV, launch_gemv(b.x, m->dtype, lw[l].w_gate_up, m->dtype, 2 * F, D, g, stream));
+    LAUNCH(AKVS_K_GEMV, launch_gemv(b.act, m->dtype, lw[l].w_down, m->dtype, D, F, r, stream));
+  }
+  LAUNCH(AKVS_K_NORM, launch_rmsnorm(b.h, D, 1, nullptr, nullptr, final_norm, m->dtype, D,
+                                     m->rms_eps, b.hf, AKVS_F32, D, stream));
+  return lm_head_row(m, b.hf, w_out ? w_out : embed, logits ? logits : b.logits, b.part_val,
+                     b.part_idx, next_token, stream);
 }
 
 }  // extern "C"

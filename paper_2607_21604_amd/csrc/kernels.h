@@ -118,4 +118,33 @@ hipError_t launch_attention(const void *q, const int32_t *pos, int pos0, int row
 int attn_splits(int rows, int hq, int hkv, int n_keys);
 int attn_split_keys(int n_keys, int n_splits);
 
+// ---- k_decode.hip -------------------------------------------------------------------
+// Matrix-vector products of one token, y = W x (W [N][K], K a multiple of 8), item i of
+// a launch = one pair of rows, with these epilogues:
+//   GV_LOGITS  out_f32[n] = y[n]; part_val / part_idx [gemv_blocks(N)] get each block's
+//              greedy best (largest value, lowest index), for launch_pick;
+//   GV_RESID   out_f32[n] += y[n];
+//   GV_SWIGLU  out[j] = silu(y[j]) * y[N/2 + j], j < N/2 (gate rows first);
+//   GV_QKV     rows [q | k | v] of widths hq_w, kv_w, kv_w: q and k get the rotary map
+//              with `rope` = the (cos, sin) row [hd/2] of the token's position, then
+//              q -> q_out, k -> k_out, v -> v_out (out_dtype).
+enum { GV_LOGITS = 0, GV_RESID = 1, GV_SWIGLU = 2, GV_QKV = 3 };
+struct GemvEpi {
+  int mode;
+  float *out_f32;
+  void *out;
+  int out_dtype;
+  void *q_out, *k_out, *v_out;
+  int hq_w, kv_w, hd;
+  const float2 *rope;
+  float *part_val;
+  int32_t *part_idx;
+};
+int gemv_blocks(int N);
+hipError_t launch_gemv(const void *x, int x_dtype, const void *W, int w_dtype, int N, int K,
+                       const GemvEpi &e, hipStream_t s);
+// *out = index of the best of n (value, index) partials; -1 if none is a number.
+hipError_t launch_pick(const float *part_val, const int32_t *part_idx, int n, int32_t *out,
+                       hipStream_t s);
+
 }  // namespace akvs

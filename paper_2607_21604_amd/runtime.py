@@ -42,6 +42,33 @@ class Engine:
                                self.weights["final_norm"], self.m, h, k, v, ws)
         return h, k, v
 
+    def lm_head(self, h: torch.Tensor, w_out: Optional[torch.Tensor] = None):
+        """Logits [n][vocab] fp32 and greedy tokens [n] of final-normed rows h [n][D]
+        (w_out None: tied to the input embedding)."""
+        n = int(h.shape[0])
+        logits = torch.empty((n, self.shape.vocab), dtype=torch.float32, device=self.device)
+        toks = torch.empty(n, dtype=torch.int32, device=self.device)
+        ws = self.workspace(akvs.akvs_decode_workspace_size(self.m, 0))
+        akvs.akvs_lm_head(h.contiguous(), n, w_out if w_out is not None else self.weights["embed"],
+                          self.m, logits, toks, ws)
+        return logits, toks
+
+    def decode_step(self, token: torch.Tensor, n_past: int, k_cache: torch.Tensor,
+                    v_cache: torch.Tensor, w_out: Optional[torch.Tensor] = None, logits=None,
+                    next_token=None):
+        """One decode step of `token` (device int32 [1]) at position n_past over caches
+        [L][cache_rows][Hkv][hd] (rows < n_past valid; row n_past is written). Returns
+        (logits [vocab] fp32, next token [1] int32)."""
+        if logits is None:
+            logits = torch.empty(self.shape.vocab, dtype=torch.float32, device=self.device)
+        if next_token is None:
+            next_token = torch.empty(1, dtype=torch.int32, device=self.device)
+        ws = self.workspace(akvs.akvs_decode_workspace_size(self.m, n_past))
+        akvs.akvs_decode_step(token, n_past, self.weights["embed"], self.layers,
+                              self.weights["final_norm"], w_out, self.m, k_cache, v_cache,
+                              int(k_cache.shape[1]), logits, next_token, ws)
+        return logits, next_token
+
     def cache_units(self, tokens: torch.Tensor, chunk_lens: Sequence[int]):
         """Standalone per-unit caches: each unit prefilled alone at position 0, laid out
         [L][T_c][Hkv][hd] with the units back to back."""
@@ -61,10 +88,12 @@ class Engine:
     def reuse_prefill(self, tokens: torch.Tensor, chunk_lens: Sequence[int], query_len: int,
                       k_cache: torch.Tensor, v_cache: torch.Tensor, refresh=(1, 5),
                       check_layer: int = 1, flags: int = 0, k_meta=None, v_meta=None,
-                      cache_dtype: Optional[int] = None, given_probes=None, outputs=None):
+                      cache_dtype: Optional[int] = None, given_probes=None, outputs=None,
+                      kv_rows: int = 0):
         """Run the reuse prefill. Returns a dict of device tensors (h_query, k_corr, v_corr,
         probe_k, probe_v, d_k, d_v, rows, n_rows). `outputs` may pass a previous result
-        dict to reuse its buffers."""
+        dict to reuse its buffers. kv_rows > T sizes k_corr / v_corr [L][kv_rows][Hkv][hd]
+        (rows T.. left for decode steps)."""
         sh = self.shape
         cfg = akvs.reuse_cfg(chunk_lens, query_len, refresh, check_layer, flags)
         _, (tc, sum_b, row_cap, t_all) = akvs.akvs_chunk_meta(cfg)
@@ -72,8 +101,8 @@ class Engine:
             dev = self.device
             outputs = {
                 "h_query": torch.empty((query_len, sh.d_model), dtype=torch.float32, device=dev),
-                "k_corr": torch.empty((self.n_layers, t_all, sh.n_kv_heads, sh.head_dim),
-                                      dtype=self.dtype, device=dev),
+                "k_corr": torch.empty((self.n_layers, max(kv_rows, t_all), sh.n_kv_heads,
+                                       sh.head_dim), dtype=self.dtype, device=dev),
                 "probe_k": torch.empty(max(sum_b, 1), dtype=torch.int32, device=dev),
                 "probe_v": torch.empty(max(sum_b, 1), dtype=torch.int32, device=dev),
                 "d_k": torch.empty(tc, dtype=torch.float32, device=dev),
@@ -87,7 +116,8 @@ class Engine:
             outputs["probe_v"][:sum_b].copy_(given_probes[1])
         o = outputs
         out = akvs.ReuseOut(*(akvs.ptr(o[k]) for k in ("h_query", "k_corr", "v_corr", "probe_k",
-                                                       "probe_v", "d_k", "d_v", "rows", "n_rows")))
+                                                       "probe_v", "d_k", "d_v", "rows", "n_rows")),
+                            int(o["k_corr"].shape[1]))
         cache = akvs.cache_struct(k_cache, v_cache, k_meta, v_meta,
                                   cache_dtype if cache_dtype is not None else akvs.dtype_code(k_cache))
         ws = self.workspace(akvs.akvs_workspace_size(self.m, cfg))
