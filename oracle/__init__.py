@@ -14,8 +14,9 @@ from .model import (ModelDims, dims_from, rms_norm, rope_cos_sin, rotate, attent
                     decoder_layer, full_prefill, cache_units, split_layer, lm_logits,
                     greedy_token, decode_step)
 from .reuse import (F_NO_CORRECTION, F_UNIT_WEIGHTS, F_FRESH_IF_RECOMPUTED,
-                    F_NO_PREFIX_RECOMPUTE, probe_budget, chunk_starts, rerotate,
-                    divergence, select_top, correction_weights, probe_offset,
-                    correct_chunk, reuse_prefill)
+                    F_NO_PREFIX_RECOMPUTE, F_PRE_ROPE_OFFSETS, probe_budget, chunk_starts,
+                    rerotate, divergence, select_top, correction_weights, probe_offset,
+                    probe_offset_pre_rope, correct_chunk, correct_chunk_pre_rope,
+                    reuse_prefill)
 from .quant import (quantize_g64, dequantize_g64, pack_codes, unpack_codes, E4M3_MAX,
                     e4m3_value, e4m3_code, quantize_e4m3_g64, dequantize_e4m3_g64)

@@ -31,6 +31,7 @@ F_NO_CORRECTION = 1        # offsets forced to 0: probes fresh, the rest as reus
 F_UNIT_WEIGHTS = 2         # w = 1 for every token instead of min(d, 1)
 F_FRESH_IF_RECOMPUTED = 4  # a token recomputed for either side takes fresh K and V
 F_NO_PREFIX_RECOMPUTE = 8  # no check layer at all: stale reuse (needs refresh 0)
+F_PRE_ROPE_OFFSETS = 32    # key offsets estimated and applied before the rotary map
 
 
 def probe_budget(n: int, num: int, den: int) -> int:
@@ -79,6 +80,30 @@ def probe_offset(fresh_probes: np.ndarray, reuse_probes: np.ndarray) -> np.ndarr
     return np.mean(fresh_probes - reuse_probes, axis=0)
 
 
+def probe_offset_pre_rope(fresh_probes: np.ndarray, reuse_probes: np.ndarray, positions,
+                          theta: float) -> np.ndarray:
+    """Key offset taken before the rotary map (the pre-RoPE variant of "Mean estimation",
+    Sec. 3.3; the survey's NEXT variant of reading R2): every probe's fresh-minus-reused
+    difference is rotated back by its own position, then averaged. An empty set gives 0."""
+    if fresh_probes.shape[0] == 0:
+        return np.zeros(fresh_probes.shape[1:], dtype=np.float64)
+    diff = fresh_probes - reuse_probes
+    return np.mean(rotate(diff, -np.asarray(positions, dtype=np.int64), theta), axis=0)
+
+
+def correct_chunk_pre_rope(reuse: np.ndarray, fresh: np.ndarray, is_fresh, w, mu_pre,
+                           positions, theta: float) -> np.ndarray:
+    """correct_chunk with a pre-RoPE key offset: token t gets reuse_t + w_t Rot(t) mu_pre."""
+    n = reuse.shape[0]
+    mu_t = rotate(np.broadcast_to(mu_pre, (n,) + mu_pre.shape).copy(),
+                  np.asarray(positions, dtype=np.int64), theta)
+    is_fresh = np.asarray(is_fresh, dtype=bool)
+    w = np.asarray(w, dtype=np.float64)
+    shape_w = (-1,) + (1,) * (reuse.ndim - 1)
+    corrected = reuse + w.reshape(shape_w) * mu_t
+    return np.where(is_fresh.reshape(shape_w), fresh, corrected)
+
+
 def correct_chunk(reuse: np.ndarray, fresh: np.ndarray, is_fresh, w, mu) -> np.ndarray:
     """Corrected states of one unit (Algorithm 1, inner loop).
 
@@ -94,12 +119,14 @@ def correct_chunk(reuse: np.ndarray, fresh: np.ndarray, is_fresh, w, mu) -> np.n
 
 def reuse_prefill(tokens, weights: dict, dims: ModelDims, chunk_lens, query_len: int,
                   k_cache, v_cache, refresh=(1, 5), check_layer: int = 1, flags: int = 0,
-                  probes=None, layers=None) -> dict:
+                  probes=None, layers=None, refresh_v=None) -> dict:
     """The whole reuse prefill over units U_1..U_m followed by the query.
 
     k_cache[i], v_cache[i]: unit i's standalone cache [L][n_i][Hkv][hd] (keys rotated at
     positions 0..n_i-1), already dequantised if the cache is quantised.
-    refresh: r as an integer pair (num, den). check_layer: 0-based layer index.
+    refresh: r as an integer pair (num, den). refresh_v: the value side's own ratio
+    (asymmetric K/V budgets, the Limitations' K-V asymmetry direction); None: the same
+    as the keys. check_layer: 0-based layer index.
     probes: optional (list of K-probe position arrays, list of V-probe position arrays),
     global positions per unit, used instead of the top-b selection.
 
@@ -119,7 +146,8 @@ def reuse_prefill(tokens, weights: dict, dims: ModelDims, chunk_lens, query_len:
     if layers is None:
         layers = [split_layer(lw, dims) for lw in weights["layers"][:L]]
     no_prefix = bool(flags & F_NO_PREFIX_RECOMPUTE)
-    if no_prefix and num != 0:
+    num_v, den_v = refresh_v if refresh_v is not None else refresh
+    if no_prefix and (num != 0 or num_v != 0):
         raise ValueError("stale reuse (no check layer) is defined for refresh 0 only")
     c = 0 if no_prefix else int(check_layer)
     if not 0 <= c < L:
@@ -148,6 +176,7 @@ def reuse_prefill(tokens, weights: dict, dims: ModelDims, chunk_lens, query_len:
 
     # 3. check layer: divergences, probe sets, weights
     budgets = [probe_budget(n, num, den) for n in lens]
+    budgets_v = [probe_budget(n, num_v, den_v) for n in lens]
     if no_prefix:
         d_k = d_v = None
         sk = [np.zeros(0, np.int64) for _ in range(m)]
@@ -160,14 +189,14 @@ def reuse_prefill(tokens, weights: dict, dims: ModelDims, chunk_lens, query_len:
         d_v = divergence(vf, v_reuse[c])
         if probes is None:
             sk = [select_top(d_k[s:s + n], b) + s for s, n, b in zip(starts, lens, budgets)]
-            sv = [select_top(d_v[s:s + n], b) + s for s, n, b in zip(starts, lens, budgets)]
+            sv = [select_top(d_v[s:s + n], b) + s for s, n, b in zip(starts, lens, budgets_v)]
         else:
             sk = [np.asarray(p, np.int64) for p in probes[0]]
             sv = [np.asarray(p, np.int64) for p in probes[1]]
             for i in range(m):
-                for side in (sk[i], sv[i]):
+                for side, bud in ((sk[i], budgets[i]), (sv[i], budgets_v[i])):
                     s, n = int(starts[i]), lens[i]
-                    if (len(side) != budgets[i] or len(np.unique(side)) != len(side)
+                    if (len(side) != bud or len(np.unique(side)) != len(side)
                             or (len(side) and (side.min() < s or side.max() >= s + n))):
                         raise ValueError(f"given probe set of unit {i} is not a valid top-b set")
         if flags & F_UNIT_WEIGHTS:
@@ -201,12 +230,21 @@ def reuse_prefill(tokens, weights: dict, dims: ModelDims, chunk_lens, query_len:
             if flags & F_NO_CORRECTION:
                 mu_k = np.zeros((hkv, hd))
                 mu_v = np.zeros((hkv, hd))
+            elif flags & F_PRE_ROPE_OFFSETS:
+                mu_k = probe_offset_pre_rope(k_fresh[sk[i]], k_reuse[l][sk[i]], sk[i],
+                                             dims.rope_theta)
+                mu_v = probe_offset(v_fresh[sv[i]], v_reuse[l][sv[i]])
             else:
                 mu_k = probe_offset(k_fresh[sk[i]], k_reuse[l][sk[i]])
                 mu_v = probe_offset(v_fresh[sv[i]], v_reuse[l][sv[i]])
             seg = slice(s, s + n)
-            k_corr[l, seg] = correct_chunk(k_reuse[l, seg], k_fresh[seg], fresh_k_mask[seg],
-                                           w_k[seg], mu_k)
+            if flags & F_PRE_ROPE_OFFSETS and not flags & F_NO_CORRECTION:
+                k_corr[l, seg] = correct_chunk_pre_rope(k_reuse[l, seg], k_fresh[seg],
+                                                        fresh_k_mask[seg], w_k[seg], mu_k,
+                                                        np.arange(s, s + n), dims.rope_theta)
+            else:
+                k_corr[l, seg] = correct_chunk(k_reuse[l, seg], k_fresh[seg], fresh_k_mask[seg],
+                                               w_k[seg], mu_k)
             v_corr[l, seg] = correct_chunk(v_reuse[l, seg], v_fresh[seg], fresh_v_mask[seg],
                                            w_v[seg], mu_v)
         k_corr[l, tc:] = k_fresh[tc:]
@@ -219,5 +257,5 @@ def reuse_prefill(tokens, weights: dict, dims: ModelDims, chunk_lens, query_len:
         "h_query": h_query, "k_corr": k_corr, "v_corr": v_corr,
         "d_k": d_k, "d_v": d_v, "probe_k": sk, "probe_v": sv, "rows": rows,
         "w_k": w_k, "w_v": w_v, "k_reuse": k_reuse, "v_reuse": v_reuse,
-        "budgets": budgets, "starts": starts,
+        "budgets": budgets, "budgets_v": budgets_v, "starts": starts,
     }

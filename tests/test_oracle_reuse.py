@@ -245,3 +245,70 @@ def test_correction_moves_reuse_towards_fresh_on_a_shifted_model(small):
     stale = np.abs(out["k_reuse"][1:] - kf[1:, :tc]).mean()
     corr = np.abs(out["k_corr"][1:, :tc] - kf[1:, :tc]).mean()
     assert corr < stale
+
+
+# ---- variants: pre-RoPE key offsets, asymmetric K/V budgets --------------------------------
+
+def test_pre_rope_offset_recovers_a_constant_pre_rope_shift():
+    """Fresh keys that differ from the reused ones by one constant vector before the
+    rotary map (after it: a different vector per position) are recovered exactly by the
+    pre-RoPE offset, and the corrected keys equal the fresh ones; the post-RoPE mean of
+    the same probes does not recover them."""
+    rng = np.random.default_rng(21)
+    n, H, hd, s0, theta = 24, 2, 8, 37, 10000.0
+    pos = np.arange(s0, s0 + n)
+    reuse = rng.standard_normal((n, H, hd))
+    delta = rng.standard_normal((H, hd))
+    delta *= 2.0 / np.linalg.norm(delta)
+    shift = oracle.model.rotate(np.broadcast_to(delta, (n, H, hd)).copy(), pos, theta)
+    fresh = reuse + shift
+    probes = np.array([2, 5, 11, 19])
+    mu = oracle.probe_offset_pre_rope(fresh[probes], reuse[probes], pos[probes], theta)
+    np.testing.assert_allclose(mu, delta, atol=1e-13)
+    w = oracle.correction_weights(oracle.divergence(fresh, reuse))
+    np.testing.assert_allclose(w, 1.0)
+    is_probe = np.isin(np.arange(n), probes)
+    corr = oracle.correct_chunk_pre_rope(reuse, fresh, is_probe, w, mu, pos, theta)
+    np.testing.assert_allclose(corr, fresh, atol=1e-13)
+    post = oracle.probe_offset(fresh[probes], reuse[probes])
+    assert np.abs(oracle.correct_chunk(reuse, fresh, is_probe, w, post) - fresh).max() > 1e-2
+
+
+def test_pre_rope_offset_at_position_zero_equals_post_rope():
+    """With every probe at position 0 the rotary map is the identity: both offsets agree."""
+    rng = np.random.default_rng(22)
+    f = rng.standard_normal((3, 2, 8))
+    r = rng.standard_normal((3, 2, 8))
+    np.testing.assert_allclose(oracle.probe_offset_pre_rope(f, r, [0, 0, 0], 1e4),
+                               oracle.probe_offset(f, r), atol=1e-15)
+
+
+def test_asymmetric_budgets_select_per_side(small):
+    dims, w, V, toks, kc, vc = small
+    out = oracle.reuse_prefill(toks, w, dims, LENS, Q, kc, vc, refresh=(1, 3), check_layer=1,
+                               refresh_v=(2, 3))
+    starts = oracle.chunk_starts(LENS)
+    for i, n in enumerate(LENS):
+        bk, bv = oracle.probe_budget(n, 1, 3), oracle.probe_budget(n, 2, 3)
+        assert out["budgets"][i] == bk and out["budgets_v"][i] == bv
+        assert list(out["probe_k"][i] - starts[i]) == brute_top(out["d_k"][starts[i]:starts[i] + n], bk)
+        assert list(out["probe_v"][i] - starts[i]) == brute_top(out["d_v"][starts[i]:starts[i] + n], bv)
+    # equal ratios on both sides reproduce the symmetric call
+    a = oracle.reuse_prefill(toks, w, dims, LENS, Q, kc, vc, refresh=(1, 3), check_layer=1,
+                             refresh_v=(1, 3))
+    b = oracle.reuse_prefill(toks, w, dims, LENS, Q, kc, vc, refresh=(1, 3), check_layer=1)
+    np.testing.assert_array_equal(a["h_query"], b["h_query"])
+
+
+def test_full_value_refresh_gives_fresh_values(small):
+    """r_V = 1 recomputes every value: the corrected values of every layer from the check
+    layer on are the fresh ones of that run, i.e. those of a full prefill when the keys
+    are fully refreshed too."""
+    dims, w, V, toks, kc, vc = small
+    h, kf, vf = oracle.full_prefill(toks, 0, w, dims)
+    out = oracle.reuse_prefill(toks, w, dims, LENS, Q, kc, vc, refresh=(1, 1), check_layer=1,
+                               refresh_v=(1, 1))
+    np.testing.assert_allclose(out["v_corr"], vf, atol=1e-10)
+    out2 = oracle.reuse_prefill(toks, w, dims, LENS, Q, kc, vc, refresh=(0, 1), check_layer=1,
+                                refresh_v=(1, 1))
+    assert len(out2["rows"]) == sum(LENS) + Q     # every unit token recomputed for its value
