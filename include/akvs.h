@@ -77,7 +77,10 @@ enum {
   AKVS_F_UNIT_WEIGHTS = 2u,        /* w = 1 instead of min(d, 1)                            */
   AKVS_F_FRESH_IF_RECOMPUTED = 4u, /* a token recomputed for either side takes fresh K and V */
   AKVS_F_NO_PREFIX_RECOMPUTE = 8u, /* stale reuse: no check layer; needs refresh_num == 0    */
-  AKVS_F_GIVEN_PROBES = 16u        /* probe sets come from the caller instead of top-b       */
+  AKVS_F_GIVEN_PROBES = 16u,       /* probe sets come from the caller instead of top-b       */
+  AKVS_F_PRE_ROPE_OFFSETS = 32u    /* key offsets taken before the rotary map: each probe's
+                                      difference is rotated back by its position before the
+                                      mean, the offset rotated to each corrected token's */
 };
 
 typedef struct akvs_model_cfg {
@@ -98,6 +101,8 @@ typedef struct akvs_reuse_cfg {
   int32_t refresh_num, refresh_den; /* r = num/den in [0, 1]; b_i = ceil(num*n_i/den) */
   int32_t check_layer;       /* 0-based layer of the divergence check, < n_layers    */
   uint32_t flags;            /* AKVS_F_*                                             */
+  int32_t refresh_v_num, refresh_v_den; /* value-side ratio (asymmetric K/V budgets);
+                                           den 0: the key ratio for both sides       */
 } akvs_reuse_cfg;
 
 /* A unit cache: k, v in the cache layout above; k_meta / v_meta only when quantised. */
@@ -129,10 +134,12 @@ const char *akvs_last_error(void);
 /* ---- host helpers -------------------------------------------------------------- */
 
 /* Per-unit bookkeeping (Sec. 3.3: b = ceil(r n), exact integers). Host only.
- * meta_out (host, may be NULL): [m][4] = (start s_i, length n_i, budget b_i, CSR offset
- * of the unit's probes = b_0 + ... + b_{i-1}). totals_out (host, may be NULL): [4] =
- * (T_c, sum b_i, row cap = sum min(n_i, 2 b_i) + q, T). Device copies of meta_out are
- * the `chunk_meta` argument of the step entries below. */
+ * meta_out (host, may be NULL): [2][m][4], table 0 for the keys and table 1 for the
+ * values, row i = (start s_i, length n_i, budget b_i of that side, CSR offset of the
+ * unit's probes of that side = b_0 + ... + b_{i-1}); the two tables differ only when the
+ * value side has its own ratio. totals_out (host, may be NULL): [5] = (T_c, sum b_K,i,
+ * row cap = sum min(n_i, b_K,i + b_V,i) + q, T, sum b_V,i). Device copies of meta_out
+ * are the `chunk_meta` argument of the step entries below. */
 akvs_status akvs_chunk_meta(const akvs_reuse_cfg *cfg, int32_t *meta_out, int32_t *totals_out);
 
 /* Workspace bytes of akvs_reuse_prefill (cfg != NULL) or of akvs_full_prefill over
@@ -175,13 +182,14 @@ akvs_status akvs_check_divergence(const void *k_fresh, const void *v_fresh, int3
  * tokens of largest d_k (equal values: the earlier token first), S_V,i likewise;
  * weights w = min(d, 1) (1 with AKVS_F_UNIT_WEIGHTS). With AKVS_F_GIVEN_PROBES the
  * sets are read from probe_k / probe_v (as written below) instead. Writes
- *  probe_k, probe_v [sum b_i]: global positions, ascending within each unit, unit i at
- *   CSR offset meta[i][3];
+ *  probe_k [sum b_K,i], probe_v [sum b_V,i]: global positions, ascending within each
+ *   unit, unit i at the CSR offset of its side's table (meta[0][i][3] / meta[1][i][3]);
  *  flags [T_c] uint8: bit0 = in S_K, bit1 = in S_V;  w_k, w_v [T_c] fp32;
  *  chunk_rows [m]: |S_K,i u S_V,i|;
  *  rows [row cap]: recomputed positions R = (u_i S_K,i u S_V,i) u query, ascending;
  *  n_rows [1]: |R|;  fresh_row [T]: index in R of each position, -1 if not recomputed.
- * chunk_meta: device copy of akvs_chunk_meta's meta_out. d_k, d_v must be finite. */
+ * chunk_meta: device copy of akvs_chunk_meta's meta_out. d_k, d_v must be finite. A
+ * probe array may be NULL when its side's budgets are all 0. */
 akvs_status akvs_select_probes(const float *d_k, const float *d_v, const akvs_reuse_cfg *cfg,
                                const int32_t *chunk_meta, int32_t *probe_k, int32_t *probe_v,
                                float *w_k, float *w_v, uint8_t *flags, int32_t *chunk_rows,
@@ -199,8 +207,9 @@ akvs_status akvs_probe_qkv(const float *h, int32_t n_rows, const int32_t *positi
 
 /* Per-unit offsets of one layer (Sec. 3.3 "Mean estimation"; Alg. 1):
  * mu_k[i] = (1/b_i) sum_{j in S_K,i} (k_fresh[fresh_row[j]] - Rot(s_i) deq(k_cached[j])),
- * mu_v likewise without rotation; 0 when b_i = 0 or with AKVS_F_NO_CORRECTION. Probe
- * terms are summed in ascending position order in fp32. k_fresh / v_fresh: [rows][Hkv][hd]
+ * mu_v likewise without rotation; 0 when b_i = 0 or with AKVS_F_NO_CORRECTION. With
+ * AKVS_F_PRE_ROPE_OFFSETS each key term is first rotated back by -j (the offset is then
+ * a pre-RoPE vector). Probe terms are summed in ascending position order in fp32. k_fresh / v_fresh: [rows][Hkv][hd]
  * model dtype; cache: one layer; mu_k, mu_v: [m][Hkv][hd] fp32. */
 akvs_status akvs_chunk_offset(const void *k_fresh, const void *v_fresh, const int32_t *fresh_row,
                               const akvs_cache *cache, const akvs_reuse_cfg *cfg,
@@ -211,7 +220,8 @@ akvs_status akvs_chunk_offset(const void *k_fresh, const void *v_fresh, const in
 /* Corrected cache of one layer (Alg. 1 inner loop; Sec. 3.3 "AgentKVShift correction").
  * For a unit token j of unit i: k_corr[j] = k_fresh[fresh_row[j]] if j in S_K,i (any
  * recomputed j with AKVS_F_FRESH_IF_RECOMPUTED), else Rot(s_i) deq(k_cached[j]) +
- * w_k[j] mu_k[i]; v_corr likewise with S_V and no rotation. Query positions T_c..T-1
+ * w_k[j] mu_k[i] (w_k[j] Rot(j) mu_k[i] with AKVS_F_PRE_ROPE_OFFSETS); v_corr likewise
+ * with S_V and no rotation. Query positions T_c..T-1
  * take their fresh rows. k_corr, v_corr: [T][Hkv][hd] model dtype (one layer). */
 akvs_status akvs_apply_correction(const akvs_cache *cache, const float *mu_k, const float *mu_v,
                                   const float *w_k, const float *w_v, const uint8_t *flags,

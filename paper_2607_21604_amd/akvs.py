@@ -25,6 +25,7 @@ AKVS_F_UNIT_WEIGHTS = 2
 AKVS_F_FRESH_IF_RECOMPUTED = 4
 AKVS_F_NO_PREFIX_RECOMPUTE = 8
 AKVS_F_GIVEN_PROBES = 16
+AKVS_F_PRE_ROPE_OFFSETS = 32
 (AKVS_K_GEMM, AKVS_K_ATTENTION, AKVS_K_CORRECTION, AKVS_K_OFFSET, AKVS_K_DIVERGENCE,
  AKVS_K_SELECT, AKVS_K_NORM, AKVS_K_OTHER, AKVS_K_GEMV) = range(9)
 KERNEL_CLASSES = ("gemm", "attention", "correction", "offset", "divergence", "select", "norm",
@@ -54,7 +55,8 @@ class ReuseCfg(ctypes.Structure):
     _fields_ = [("n_chunks", ctypes.c_int32), ("chunk_len", ctypes.POINTER(ctypes.c_int32)),
                 ("query_len", ctypes.c_int32), ("refresh_num", ctypes.c_int32),
                 ("refresh_den", ctypes.c_int32), ("check_layer", ctypes.c_int32),
-                ("flags", ctypes.c_uint32)]
+                ("flags", ctypes.c_uint32), ("refresh_v_num", ctypes.c_int32),
+                ("refresh_v_den", ctypes.c_int32)]
 
 
 class Cache(ctypes.Structure):
@@ -181,10 +183,12 @@ def layer_array(weights: dict) -> ctypes.Array:
 
 
 def reuse_cfg(chunk_lens: Sequence[int], query_len: int, refresh=(1, 5), check_layer: int = 1,
-              flags: int = 0):
+              flags: int = 0, refresh_v=None):
+    """refresh_v: the value side's own ratio (num, den); None: the key ratio for both."""
     lens = (ctypes.c_int32 * len(chunk_lens))(*[int(n) for n in chunk_lens])
+    rv = refresh_v if refresh_v is not None else (0, 0)
     cfg = ReuseCfg(len(chunk_lens), lens, int(query_len), int(refresh[0]), int(refresh[1]),
-                   int(check_layer), int(flags))
+                   int(check_layer), int(flags), int(rv[0]), int(rv[1]))
     cfg._keep = lens  # the length array must outlive the struct
     return cfg
 
@@ -205,9 +209,10 @@ def akvs_version() -> int:
 
 
 def akvs_chunk_meta(cfg: ReuseCfg):
-    """Returns (meta [m][4] int32 host tensor, totals (T_c, sum b, row cap, T))."""
-    meta = torch.zeros((cfg.n_chunks, 4), dtype=torch.int32)
-    tot = torch.zeros(4, dtype=torch.int32)
+    """Returns (meta [2m][4] int32 host tensor: key table then value table,
+    totals (T_c, sum b_K, row cap, T, sum b_V))."""
+    meta = torch.zeros((2 * cfg.n_chunks, 4), dtype=torch.int32)
+    tot = torch.zeros(5, dtype=torch.int32)
     _check(load().akvs_chunk_meta(ctypes.byref(cfg), meta.data_ptr(), tot.data_ptr()),
            "akvs_chunk_meta")
     return meta, tuple(int(x) for x in tot)

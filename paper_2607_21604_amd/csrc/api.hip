@@ -154,8 +154,8 @@ akvs_status check_layers(const akvs_model_cfg *m, const akvs_layer_w *lw) {
 }
 
 struct Meta {
-  std::vector<int32_t> m;  // [n][4]
-  long long t_ctx = 0, sum_b = 0, row_cap = 0, row_min = 0, t_all = 0;
+  std::vector<int32_t> m;  // [2][n][4]: key table, value table
+  long long t_ctx = 0, sum_b = 0, sum_b_v = 0, row_cap = 0, row_min = 0, t_all = 0;
 };
 
 akvs_status check_reuse(const akvs_reuse_cfg *c, int n_layers, Meta *meta) {
@@ -164,34 +164,49 @@ akvs_status check_reuse(const akvs_reuse_cfg *c, int n_layers, Meta *meta) {
   REQUIRE(c->query_len >= 1, AKVS_EINVAL, "query_len must be >= 1");
   REQUIRE(c->refresh_den >= 1 && c->refresh_num >= 0 && c->refresh_num <= c->refresh_den,
           AKVS_EINVAL, "refresh ratio must satisfy 0 <= num <= den, den >= 1");
+  const bool own_v = c->refresh_v_den != 0;
+  REQUIRE(!own_v || (c->refresh_v_den >= 1 && c->refresh_v_num >= 0 &&
+                     c->refresh_v_num <= c->refresh_v_den),
+          AKVS_EINVAL, "value refresh ratio must satisfy 0 <= num <= den, den >= 1 (or den 0)");
+  const long long vn = own_v ? c->refresh_v_num : c->refresh_num;
+  const long long vd = own_v ? c->refresh_v_den : c->refresh_den;
   const uint32_t known = AKVS_F_NO_CORRECTION | AKVS_F_UNIT_WEIGHTS | AKVS_F_FRESH_IF_RECOMPUTED |
-                         AKVS_F_NO_PREFIX_RECOMPUTE | AKVS_F_GIVEN_PROBES;
+                         AKVS_F_NO_PREFIX_RECOMPUTE | AKVS_F_GIVEN_PROBES |
+                         AKVS_F_PRE_ROPE_OFFSETS;
   REQUIRE((c->flags & ~known) == 0, AKVS_EINVAL, "unknown flag bits 0x%x", c->flags & ~known);
-  REQUIRE(!(c->flags & AKVS_F_NO_PREFIX_RECOMPUTE) || c->refresh_num == 0, AKVS_EINVAL,
-          "AKVS_F_NO_PREFIX_RECOMPUTE needs refresh_num == 0");
+  REQUIRE(!(c->flags & AKVS_F_NO_PREFIX_RECOMPUTE) || (c->refresh_num == 0 && vn == 0),
+          AKVS_EINVAL, "AKVS_F_NO_PREFIX_RECOMPUTE needs zero refresh ratios");
   if (n_layers > 0)
     REQUIRE(c->check_layer >= 0 && c->check_layer < n_layers, AKVS_EINVAL,
             "check_layer %d outside [0, %d)", c->check_layer, n_layers);
   Meta loc;
   Meta &mt = meta ? *meta : loc;
-  mt.m.assign((size_t)c->n_chunks * 4, 0);
-  long long s = 0, off = 0, cap = 0, lo = 0;
-  for (int i = 0; i < c->n_chunks; ++i) {
+  const int nc = c->n_chunks;
+  mt.m.assign((size_t)nc * 8, 0);
+  long long s = 0, off = 0, off_v = 0, cap = 0, lo = 0;
+  for (int i = 0; i < nc; ++i) {
     const long long n = c->chunk_len[i];
     REQUIRE(n >= 1, AKVS_EINVAL, "chunk %d has length %lld", i, n);
     const long long b = (c->refresh_num * n + c->refresh_den - 1) / c->refresh_den;
-    mt.m[4 * i + 0] = (int32_t)s;
-    mt.m[4 * i + 1] = (int32_t)n;
-    mt.m[4 * i + 2] = (int32_t)b;
-    mt.m[4 * i + 3] = (int32_t)off;
+    const long long bv = (vn * n + vd - 1) / vd;
+    int32_t *mk = &mt.m[4 * (size_t)i], *mv = &mt.m[4 * ((size_t)nc + i)];
+    mk[0] = mv[0] = (int32_t)s;
+    mk[1] = mv[1] = (int32_t)n;
+    mk[2] = (int32_t)b;
+    mk[3] = (int32_t)off;
+    mv[2] = (int32_t)bv;
+    mv[3] = (int32_t)off_v;
     s += n;
     off += b;
-    cap += n < 2 * b ? n : 2 * b;
-    lo += n < b ? n : b;  // the key probes alone are min(n, b) distinct rows
+    off_v += bv;
+    cap += n < b + bv ? n : b + bv;
+    const long long bmax = b > bv ? b : bv;
+    lo += n < bmax ? n : bmax;  // the larger probe set alone is min(n, b) distinct rows
     REQUIRE(s + c->query_len < (1LL << 28), AKVS_ESHAPE, "context too long");
   }
   mt.t_ctx = s;
   mt.sum_b = off;
+  mt.sum_b_v = off_v;
   mt.row_cap = cap + c->query_len;
   mt.row_min = lo + c->query_len;
   mt.t_all = s + c->query_len;
@@ -327,7 +342,7 @@ size_t carve_reuse(void *ws, const akvs_model_cfg *m, const akvs_reuse_cfg *c, c
   const long long T = mt.t_all, Tc = mt.t_ctx, cap = mt.row_cap;
   const int kvw = m->n_kv_heads * m->head_dim;
   b.rope = cv.take<float>((size_t)T * m->head_dim);
-  b.meta = cv.take<int32_t>((size_t)c->n_chunks * 4);
+  b.meta = cv.take<int32_t>((size_t)c->n_chunks * 8);
   b.tok_delta = cv.take<int32_t>((size_t)Tc);
   b.tok_chunk = cv.take<int32_t>((size_t)Tc);
   b.h_full = cv.take<float>((size_t)T * m->d_model);
@@ -344,7 +359,7 @@ size_t carve_reuse(void *ws, const akvs_model_cfg *m, const akvs_reuse_cfg *c, c
   b.n_rows = cv.take<int32_t>(1);
   b.fresh_row = cv.take<int32_t>((size_t)T);
   b.probe_k = cv.take<int32_t>((size_t)mt.sum_b + 1);
-  b.probe_v = cv.take<int32_t>((size_t)mt.sum_b + 1);
+  b.probe_v = cv.take<int32_t>((size_t)mt.sum_b_v + 1);
   b.h_probe = cv.take<float>((size_t)cap * m->d_model);
   b.k_fresh = cv.take<char>((size_t)cap * kvw * es);
   b.v_fresh = cv.take<char>((size_t)cap * kvw * es);
@@ -552,7 +567,7 @@ size_t carve_batch(void *ws, const akvs_model_cfg *m, const akvs_reuse_cfg *cfgs
     const Meta &mt = pl.mt[i];
     BatchReq &r = b.req[i];
     const int nch = cfgs[i].n_chunks;
-    r.meta = cv.take<int32_t>((size_t)nch * 4);
+    r.meta = cv.take<int32_t>((size_t)nch * 8);
     r.tok_delta = cv.take<int32_t>((size_t)mt.t_ctx);
     r.tok_chunk = cv.take<int32_t>((size_t)mt.t_ctx);
     r.h_full = cv.take<float>((size_t)mt.t_all * D);
@@ -565,7 +580,7 @@ size_t carve_batch(void *ws, const akvs_model_cfg *m, const akvs_reuse_cfg *cfgs
     r.rows = cv.take<int32_t>((size_t)mt.t_all);
     r.fresh_row = cv.take<int32_t>((size_t)mt.t_all);
     r.probe_k = cv.take<int32_t>((size_t)mt.sum_b + 1);
-    r.probe_v = cv.take<int32_t>((size_t)mt.sum_b + 1);
+    r.probe_v = cv.take<int32_t>((size_t)mt.sum_b_v + 1);
     r.mu_k = cv.take<float>((size_t)nch * kvw);
     r.mu_v = cv.take<float>((size_t)nch * kvw);
   }
@@ -626,6 +641,7 @@ akvs_status akvs_chunk_meta(const akvs_reuse_cfg *cfg, int32_t *meta_out, int32_
     totals_out[1] = (int32_t)mt.sum_b;
     totals_out[2] = (int32_t)mt.row_cap;
     totals_out[3] = (int32_t)mt.t_all;
+    totals_out[4] = (int32_t)mt.sum_b_v;
   }
   return AKVS_OK;
 }
@@ -737,8 +753,9 @@ akvs_status akvs_select_probes(const float *d_k, const float *d_v, const akvs_re
   Meta mt;
   akvs_status st = check_reuse(cfg, 0, &mt);
   if (st) return st;
-  REQUIRE(d_k && d_v && chunk_meta && probe_k && probe_v && w_k && w_v && flags && chunk_rows &&
-              rows && n_rows && fresh_row,
+  REQUIRE(d_k && d_v && chunk_meta && (probe_k || mt.sum_b == 0) &&
+              (probe_v || mt.sum_b_v == 0) && w_k && w_v && flags && chunk_rows && rows &&
+              n_rows && fresh_row,
           AKVS_EINVAL, "NULL argument");
   REQUIRE(aligned16(chunk_meta), AKVS_EINVAL, "chunk_meta misaligned");
   LAUNCH(AKVS_K_SELECT, launch_select(d_k, d_v, chunk_meta, cfg->n_chunks, (int)mt.t_ctx,
@@ -786,8 +803,8 @@ akvs_status akvs_chunk_offset(const void *k_fresh, const void *v_fresh, const in
   Meta mt;
   if ((st = check_reuse(cfg, 0, &mt))) return st;
   if ((st = check_cache(cache, m))) return st;
-  REQUIRE(k_fresh && v_fresh && fresh_row && chunk_meta && probe_k && probe_v && rope && mu_k &&
-              mu_v,
+  REQUIRE(k_fresh && v_fresh && fresh_row && chunk_meta && (probe_k || mt.sum_b == 0) &&
+              (probe_v || mt.sum_b_v == 0) && rope && mu_k && mu_v,
           AKVS_EINVAL, "NULL argument");
   REQUIRE(aligned16(chunk_meta) && aligned16(mu_k) && aligned16(mu_v) && aligned16(rope),
           AKVS_EINVAL, "misaligned argument");

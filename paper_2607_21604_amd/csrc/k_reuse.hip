@@ -16,6 +16,18 @@ __device__ __forceinline__ void rotate8(const float2 *rope_row, int e0, float (&
   }
 }
 
+// The inverse map: rotation by minus the row's angle.
+__device__ __forceinline__ void unrotate8(const float2 *rope_row, int e0, float (&lo)[8],
+                                          float (&hi)[8]) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const float2 cs = rope_row[e0 + i];
+    const float a = lo[i], b = hi[i];
+    lo[i] = a * cs.x + b * cs.y;
+    hi[i] = b * cs.x - a * cs.y;
+  }
+}
+
 template <typename T>
 __host__ __device__ __forceinline__ const T *as(const void *p) {
   return reinterpret_cast<const T *>(p);
@@ -96,13 +108,15 @@ hipError_t launch_divergence(const void *k_fresh, const void *v_fresh, int fresh
 // j is a probe iff rank(j) < b. Then the probe lists (ascending) are compacted by wave 0.
 constexpr int SEL_TILE = 1024;
 
-__global__ void k_select_rank(const float *d_k, const float *d_v, const int4 *meta, uint32_t flags,
-                              int32_t *probe_k, int32_t *probe_v, float *w_k, float *w_v,
-                              uint8_t *tok_flags, int32_t *chunk_rows) {
+__global__ void k_select_rank(const float *d_k, const float *d_v, const int4 *meta, int n_chunks,
+                              uint32_t flags, int32_t *probe_k, int32_t *probe_v, float *w_k,
+                              float *w_v, uint8_t *tok_flags, int32_t *chunk_rows) {
   __shared__ float sk[SEL_TILE], sv[SEL_TILE];
   const int c = blockIdx.x;
-  const int4 mc = meta[c];  // (start, len, budget, csr offset)
-  const int s0 = mc.x, n = mc.y, b = mc.z, off = mc.w;
+  const int4 mc = meta[c];             // keys: (start, len, budget, csr offset)
+  const int4 mcv = meta[n_chunks + c];  // values: same start and length, own budget
+  const int s0 = mc.x, n = mc.y, b = mc.z, off = mc.w, bv_ = mcv.z, offv = mcv.w;
+  const int bany = max(b, bv_);
   const bool given = (flags & AKVS_F_GIVEN_PROBES) != 0;
   const bool unit_w = (flags & AKVS_F_UNIT_WEIGHTS) != 0;
   // each thread keeps the ranks of up to 8 of its tokens in registers (n <= 8*blockDim)
@@ -113,13 +127,13 @@ __global__ void k_select_rank(const float *d_k, const float *d_v, const int4 *me
     for (int u = 0; u < 8; ++u) {
       const int j = jb + u * blockDim.x + threadIdx.x;
       rk[u] = rv[u] = 0;
-      dk[u] = (j < n && b > 0) ? d_k[s0 + j] : 0.f;
-      dv[u] = (j < n && b > 0) ? d_v[s0 + j] : 0.f;
+      dk[u] = (j < n && bany > 0) ? d_k[s0 + j] : 0.f;
+      dv[u] = (j < n && bany > 0) ? d_v[s0 + j] : 0.f;
       // a NaN divergence ranks below every number (keeps exactly b probes per side)
       if (dk[u] != dk[u]) dk[u] = -INFINITY;
       if (dv[u] != dv[u]) dv[u] = -INFINITY;
     }
-    if (!given && b > 0) {
+    if (!given && bany > 0) {
       for (int tb = 0; tb < n; tb += SEL_TILE) {
         __syncthreads();
         for (int t = threadIdx.x; t < SEL_TILE && tb + t < n; t += blockDim.x) {
@@ -148,17 +162,15 @@ __global__ void k_select_rank(const float *d_k, const float *d_v, const int4 *me
       uint8_t f;
       if (given) {
         f = 0;
-        for (int k = 0; k < b; ++k) {
-          f |= (probe_k[off + k] == s0 + j) ? 1 : 0;
-          f |= (probe_v[off + k] == s0 + j) ? 2 : 0;
-        }
+        for (int k = 0; k < b; ++k) f |= (probe_k[off + k] == s0 + j) ? 1 : 0;
+        for (int k = 0; k < bv_; ++k) f |= (probe_v[offv + k] == s0 + j) ? 2 : 0;
       } else {
-        f = (uint8_t)((rk[u] < b ? 1 : 0) | (rv[u] < b ? 2 : 0));
+        f = (uint8_t)((rk[u] < b ? 1 : 0) | (rv[u] < bv_ ? 2 : 0));
       }
       tok_flags[s0 + j] = f;
-      // w only multiplies the unit's offset, which is 0 when b == 0
+      // w only multiplies the unit's offset, which is 0 when that side's b == 0
       w_k[s0 + j] = b == 0 ? 0.f : (unit_w ? 1.f : fmaxf(fminf(dk[u], 1.f), 0.f));
-      w_v[s0 + j] = b == 0 ? 0.f : (unit_w ? 1.f : fmaxf(fminf(dv[u], 1.f), 0.f));
+      w_v[s0 + j] = bv_ == 0 ? 0.f : (unit_w ? 1.f : fmaxf(fminf(dv[u], 1.f), 0.f));
     }
   }
   __syncthreads();
@@ -175,7 +187,7 @@ __global__ void k_select_rank(const float *d_k, const float *d_v, const int4 *me
     const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
     if (!given) {
       if ((f & 1) && ck + __popcll(mk & below) < b) probe_k[off + ck + __popcll(mk & below)] = s0 + j;
-      if ((f & 2) && cv + __popcll(mv & below) < b) probe_v[off + cv + __popcll(mv & below)] = s0 + j;
+      if ((f & 2) && cv + __popcll(mv & below) < bv_) probe_v[offv + cv + __popcll(mv & below)] = s0 + j;
     }
     ck += __popcll(mk);
     cv += __popcll(mv);
@@ -227,8 +239,8 @@ hipError_t launch_select(const float *d_k, const float *d_v, const int32_t *meta
                          float *w_k, float *w_v, uint8_t *tok_flags, int32_t *chunk_rows,
                          int32_t *rows, int32_t *n_rows, int32_t *fresh_row, hipStream_t s) {
   const int4 *m4 = reinterpret_cast<const int4 *>(meta);
-  hipLaunchKernelGGL(k_select_rank, dim3(n_chunks), dim3(256), 0, s, d_k, d_v, m4, flags, probe_k,
-                     probe_v, w_k, w_v, tok_flags, chunk_rows);
+  hipLaunchKernelGGL(k_select_rank, dim3(n_chunks), dim3(256), 0, s, d_k, d_v, m4, n_chunks, flags,
+                     probe_k, probe_v, w_k, w_v, tok_flags, chunk_rows);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_select_rows, dim3(n_chunks + 1), dim3(64), 0, s, m4, n_chunks, t_ctx, q,
@@ -260,8 +272,9 @@ __global__ __launch_bounds__(UP == 1 ? 1024 : 512) void k_chunk_offset(const TF 
   const int half = hd >> 1, upr = half >> 3;  // 8-pair units per head
   const int units = hkv * upr;                // <= 64 * UP
   const int kvw = hkv * hd;
-  const int4 mc = meta[c];
+  const int4 mc = meta[side * gridDim.x + c];  // this side's table
   const int b = mc.z;
+  const bool pre_rope = side == 0 && (flags & AKVS_F_PRE_ROPE_OFFSETS);
   float *mu = (side == 0 ? mu_k : mu_v) + (size_t)c * kvw;
   if (b == 0 || (flags & AKVS_F_NO_CORRECTION)) {
     for (int e = threadIdx.x; e < kvw; e += blockDim.x) mu[e] = 0.f;
@@ -298,10 +311,17 @@ __global__ __launch_bounds__(UP == 1 ? 1024 : 512) void k_chunk_offset(const TF 
         cache_load8(cb, cm, cache.dtype, crow, hd, e0, clo);
         cache_load8(cb, cm, cache.dtype, crow, hd, e0 + half, chi);
         if (side == 0) rotate8(rrow, e0, clo, chi);
+        float dlo[8], dhi[8];
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
-          acc[q][i] += flo[i] - clo[i];
-          acc[q][8 + i] += fhi[i] - chi[i];
+          dlo[i] = flo[i] - clo[i];
+          dhi[i] = fhi[i] - chi[i];
+        }
+        if (pre_rope) unrotate8(rope + (size_t)min(j, rope_rows - 1) * half, e0, dlo, dhi);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          acc[q][i] += dlo[i];
+          acc[q][8 + i] += dhi[i];
         }
       }
     }
@@ -408,7 +428,8 @@ __device__ __forceinline__ void corr_side(bool fresh, int fr, const TS *__restri
                                           const void *cb, const _Float16 *cm, int dtype,
                                           size_t orow, int hkv, int h, int hd, int e0,
                                           const float2 *rrow, const float *mu, float w,
-                                          float (&lo)[8], float (&hi)[8]) {
+                                          float (&lo)[8], float (&hi)[8],
+                                          const float2 *mu_rot = nullptr) {
   const int half = hd >> 1;
   if (fresh) {
     if (fr >= 0) {
@@ -428,6 +449,7 @@ __device__ __forceinline__ void corr_side(bool fresh, int fr, const TS *__restri
     float ml[8], mh[8];
     load8(mu + e0, ml);
     load8(mu + e0 + half, mh);
+    if (mu_rot) rotate8(mu_rot, e0, ml, mh);  // a pre-RoPE offset at the token's position
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       lo[i] = fmaf(w, ml[i], lo[i]);
@@ -472,9 +494,12 @@ __global__ __launch_bounds__(256) void k_correction(CacheLayer cache, const floa
                                  n_chunks, rope_rows, flags, fresh_off);
     const size_t orow = (size_t)t * hkv + h;
     const size_t mo = (size_t)c.chunk * hkv * hd + (size_t)h * hd;
+    const float2 *mu_rot = (flags & AKVS_F_PRE_ROPE_OFFSETS)
+                               ? rope + (size_t)min(t, rope_rows - 1) * half
+                               : nullptr;
     corr_side(c.fresh_k, c.fr, k_fresh, cache.k, cache.k_meta, cache.dtype, orow, hkv, h, hd, e0,
               rope + (size_t)c.delta * half, mu_k ? mu_k + mo : nullptr, mu_k ? w_k[t] : 0.f,
-              klo[i], khi[i]);
+              klo[i], khi[i], mu_rot);
     corr_side(c.fresh_v, c.fr, v_fresh, cache.v, cache.v_meta, cache.dtype, orow, hkv, h, hd, e0,
               nullptr, mu_v ? mu_v + mo : nullptr, mu_v ? w_v[t] : 0.f, vlo[i], vhi[i]);
   }

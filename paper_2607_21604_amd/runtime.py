@@ -89,14 +89,14 @@ class Engine:
                       k_cache: torch.Tensor, v_cache: torch.Tensor, refresh=(1, 5),
                       check_layer: int = 1, flags: int = 0, k_meta=None, v_meta=None,
                       cache_dtype: Optional[int] = None, given_probes=None, outputs=None,
-                      kv_rows: int = 0):
+                      kv_rows: int = 0, refresh_v=None):
         """Run the reuse prefill. Returns a dict of device tensors (h_query, k_corr, v_corr,
         probe_k, probe_v, d_k, d_v, rows, n_rows). `outputs` may pass a previous result
         dict to reuse its buffers. kv_rows > T sizes k_corr / v_corr [L][kv_rows][Hkv][hd]
-        (rows T.. left for decode steps)."""
+        (rows T.. left for decode steps). refresh_v: the value side's own ratio."""
         sh = self.shape
-        cfg = akvs.reuse_cfg(chunk_lens, query_len, refresh, check_layer, flags)
-        _, (tc, sum_b, row_cap, t_all) = akvs.akvs_chunk_meta(cfg)
+        cfg = akvs.reuse_cfg(chunk_lens, query_len, refresh, check_layer, flags, refresh_v)
+        _, (tc, sum_b, row_cap, t_all, sum_bv) = akvs.akvs_chunk_meta(cfg)
         if outputs is None:
             dev = self.device
             outputs = {
@@ -104,7 +104,7 @@ class Engine:
                 "k_corr": torch.empty((self.n_layers, max(kv_rows, t_all), sh.n_kv_heads,
                                        sh.head_dim), dtype=self.dtype, device=dev),
                 "probe_k": torch.empty(max(sum_b, 1), dtype=torch.int32, device=dev),
-                "probe_v": torch.empty(max(sum_b, 1), dtype=torch.int32, device=dev),
+                "probe_v": torch.empty(max(sum_bv, 1), dtype=torch.int32, device=dev),
                 "d_k": torch.empty(tc, dtype=torch.float32, device=dev),
                 "d_v": torch.empty(tc, dtype=torch.float32, device=dev),
                 "rows": torch.empty(t_all, dtype=torch.int32, device=dev),
@@ -113,7 +113,7 @@ class Engine:
             outputs["v_corr"] = torch.empty_like(outputs["k_corr"])
         if given_probes is not None:
             outputs["probe_k"][:sum_b].copy_(given_probes[0])
-            outputs["probe_v"][:sum_b].copy_(given_probes[1])
+            outputs["probe_v"][:sum_bv].copy_(given_probes[1])
         o = outputs
         out = akvs.ReuseOut(*(akvs.ptr(o[k]) for k in ("h_query", "k_corr", "v_corr", "probe_k",
                                                        "probe_v", "d_k", "d_v", "rows", "n_rows")),
@@ -124,17 +124,19 @@ class Engine:
         akvs.akvs_reuse_prefill(tokens, self.weights["embed"], self.layers,
                                 self.weights["final_norm"], self.m, cfg, cache, out, ws)
         outputs["_sum_b"] = sum_b
+        outputs["_sum_b_v"] = sum_bv
         return outputs
 
 
-def _reuse_outputs(engine, query_len, tc, sum_b, t_all):
+def _reuse_outputs(engine, query_len, tc, sum_b, t_all, sum_bv=None):
     sh, dev = engine.shape, engine.device
     out = {
         "h_query": torch.empty((query_len, sh.d_model), dtype=torch.float32, device=dev),
         "k_corr": torch.empty((engine.n_layers, t_all, sh.n_kv_heads, sh.head_dim),
                               dtype=engine.dtype, device=dev),
         "probe_k": torch.empty(max(sum_b, 1), dtype=torch.int32, device=dev),
-        "probe_v": torch.empty(max(sum_b, 1), dtype=torch.int32, device=dev),
+        "probe_v": torch.empty(max(sum_b if sum_bv is None else sum_bv, 1), dtype=torch.int32,
+                               device=dev),
         "d_k": torch.empty(tc, dtype=torch.float32, device=dev),
         "d_v": torch.empty(tc, dtype=torch.float32, device=dev),
         "rows": torch.empty(t_all, dtype=torch.int32, device=dev),
@@ -142,6 +144,7 @@ def _reuse_outputs(engine, query_len, tc, sum_b, t_all):
     }
     out["v_corr"] = torch.empty_like(out["k_corr"])
     out["_sum_b"] = sum_b
+    out["_sum_b_v"] = sum_b if sum_bv is None else sum_bv
     return out
 
 
@@ -156,8 +159,8 @@ def reuse_prefill_batch(engine: Engine, requests, refresh=(1, 5), check_layer: i
         outputs = []
         for r in requests:
             cfg = akvs.reuse_cfg(r["chunk_lens"], r["query_len"], refresh, check_layer, flags)
-            _, (tc, sum_b, _, t_all) = akvs.akvs_chunk_meta(cfg)
-            outputs.append(_reuse_outputs(engine, r["query_len"], tc, sum_b, t_all))
+            _, (tc, sum_b, _, t_all, sum_bv) = akvs.akvs_chunk_meta(cfg)
+            outputs.append(_reuse_outputs(engine, r["query_len"], tc, sum_b, t_all, sum_bv))
     for r, o in zip(requests, outputs):
         cfgs.append(akvs.reuse_cfg(r["chunk_lens"], r["query_len"], refresh, check_layer, flags))
         dt = r.get("cache_dtype")

@@ -5,6 +5,7 @@ import os
 import subprocess
 
 import pytest
+import torch
 
 import oracle
 from paper_2607_21604_amd import akvs
@@ -45,24 +46,44 @@ def test_chunk_meta_matches_budget_table(lib):
 def test_chunk_meta_offsets_and_row_cap(lib):
     lens = [5, 1, 17, 64]
     cfg = akvs.reuse_cfg(lens, 9, (3, 10), 1, 0)
-    meta, (tc, sum_b, cap, t_all) = akvs.akvs_chunk_meta(cfg)
+    meta, (tc, sum_b, cap, t_all, sum_bv) = akvs.akvs_chunk_meta(cfg)
     b = [oracle.probe_budget(n, 3, 10) for n in lens]
     starts = oracle.chunk_starts(lens)
-    assert [int(x) for x in meta[:, 0]] == list(starts)
-    assert [int(x) for x in meta[:, 2]] == b
-    assert [int(x) for x in meta[:, 3]] == [0, b[0], b[0] + b[1], b[0] + b[1] + b[2]]
-    assert (tc, sum_b, t_all) == (87, sum(b), 96)
+    m = len(lens)
+    assert [int(x) for x in meta[:m, 0]] == list(starts)
+    assert [int(x) for x in meta[:m, 2]] == b
+    assert [int(x) for x in meta[:m, 3]] == [0, b[0], b[0] + b[1], b[0] + b[1] + b[2]]
+    assert (tc, sum_b, t_all, sum_bv) == (87, sum(b), 96, sum(b))
     assert cap == sum(min(n, 2 * bb) for n, bb in zip(lens, b)) + 9
+    assert torch.equal(meta[m:], meta[:m])   # the value table equals the key table
+
+
+def test_chunk_meta_value_side_ratio(lib):
+    """A value ratio of its own: the second table carries its budgets and CSR offsets,
+    the row cap counts both sides."""
+    lens = [5, 1, 17, 64]
+    cfg = akvs.reuse_cfg(lens, 9, (1, 10), 1, 0, refresh_v=(1, 2))
+    meta, (tc, sum_b, cap, t_all, sum_bv) = akvs.akvs_chunk_meta(cfg)
+    bk = [oracle.probe_budget(n, 1, 10) for n in lens]
+    bv = [oracle.probe_budget(n, 1, 2) for n in lens]
+    m = len(lens)
+    assert [int(x) for x in meta[:m, 2]] == bk and [int(x) for x in meta[m:, 2]] == bv
+    assert [int(x) for x in meta[m:, 3]] == [0, bv[0], bv[0] + bv[1], bv[0] + bv[1] + bv[2]]
+    assert [int(x) for x in meta[m:, 0]] == list(oracle.chunk_starts(lens))
+    assert (sum_b, sum_bv) == (sum(bk), sum(bv))
+    assert cap == sum(min(n, a + c) for n, a, c in zip(lens, bk, bv)) + 9
 
 
 @pytest.mark.parametrize("bad", [
     dict(n_chunks=0), dict(query_len=0), dict(refresh=(6, 5)), dict(refresh=(1, 0)),
     dict(flags=1 << 7), dict(lens=[4, 0, 3]), dict(flags=akvs.AKVS_F_NO_PREFIX_RECOMPUTE),
+    dict(refresh_v=(3, 2)), dict(refresh_v=(-1, 2)),
+    dict(refresh=(0, 1), refresh_v=(1, 2), flags=akvs.AKVS_F_NO_PREFIX_RECOMPUTE),
 ])
 def test_invalid_reuse_configs_are_rejected(lib, bad):
     lens = bad.get("lens", [4, 5, 3])
     cfg = akvs.reuse_cfg(lens, bad.get("query_len", 2), bad.get("refresh", (1, 5)), 1,
-                         bad.get("flags", 0))
+                         bad.get("flags", 0), bad.get("refresh_v"))
     if "n_chunks" in bad:
         cfg.n_chunks = 0
     with pytest.raises(akvs.AkvsError) as e:

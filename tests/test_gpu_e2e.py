@@ -40,12 +40,13 @@ class Case:
         self.starts = oracle.chunk_starts(self.lens)
         self.tol = 1e-4 if self.shape.dtype == "f32" else 2e-2
 
-    def oracle(self, refresh=None, check_layer=1, flags=0, probes=None, kc=None, vc=None):
+    def oracle(self, refresh=None, check_layer=1, flags=0, probes=None, kc=None, vc=None,
+               refresh_v=None):
         return oracle.reuse_prefill(self.toks, self.w, self.dims, self.lens, self.q,
                                     kc if kc is not None else self.kc,
                                     vc if vc is not None else self.vc,
                                     refresh or self.refresh, check_layer, flags, probes,
-                                    self.layers)
+                                    self.layers, refresh_v=refresh_v)
 
     def gpu(self, refresh=None, check_layer=1, flags=0, probes=None, **kw):
         given = None
@@ -198,3 +199,19 @@ def test_7b_width_quantised_cache(w7b, bits):
                   k_meta=to_dev(meta_k), v_meta=to_dev(meta_v), cache_dtype=dt)
     errs = w7b.compare(out, ref)
     print(f"7b-width {bits}-bit errors", errs)
+
+
+@pytest.mark.parametrize("flags,refresh_v", [
+    (akvs.AKVS_F_PRE_ROPE_OFFSETS, None), (0, (1, 2)), (akvs.AKVS_F_PRE_ROPE_OFFSETS, (0, 1))])
+def test_tiny_variants_pre_rope_offsets_and_value_ratio(tiny, flags, refresh_v):
+    """The pre-RoPE key offsets and a value ratio of its own, whole procedure against the
+    oracle (its probe sets handed over)."""
+    ref = tiny.oracle(flags=flags, refresh_v=refresh_v)
+    out = tiny.gpu(flags=flags, probes=(ref["probe_k"], ref["probe_v"]), refresh_v=refresh_v)
+    tiny.compare(out, ref)
+
+
+def test_3b_width_pre_rope_offsets(w3b):
+    ref = w3b.oracle(flags=akvs.AKVS_F_PRE_ROPE_OFFSETS)
+    out = w3b.gpu(flags=akvs.AKVS_F_PRE_ROPE_OFFSETS, probes=(ref["probe_k"], ref["probe_v"]))
+    w3b.compare(out, ref)

@@ -100,12 +100,12 @@ def test_check_divergence(fresh_dtype):
     np.testing.assert_allclose(f64(dv), oracle.divergence(f64(vf), f64(vc)), rtol=2e-5)
 
 
-def run_select(d_k, d_v, lens, q, refresh, flags=0, given=None):
-    cfg = akvs.reuse_cfg(lens, q, refresh, 1, flags)
-    meta, (tc, sum_b, cap, t_all) = akvs.akvs_chunk_meta(cfg)
+def run_select(d_k, d_v, lens, q, refresh, flags=0, given=None, refresh_v=None):
+    cfg = akvs.reuse_cfg(lens, q, refresh, 1, flags, refresh_v)
+    meta, (tc, sum_b, cap, t_all, sum_bv) = akvs.akvs_chunk_meta(cfg)
     out = {
         "probe_k": torch.full((max(sum_b, 1),), -7, dtype=torch.int32, device=DEV),
-        "probe_v": torch.full((max(sum_b, 1),), -7, dtype=torch.int32, device=DEV),
+        "probe_v": torch.full((max(sum_bv, 1),), -7, dtype=torch.int32, device=DEV),
         "w_k": torch.empty(tc, dtype=torch.float32, device=DEV),
         "w_v": torch.empty(tc, dtype=torch.float32, device=DEV),
         "flags": torch.empty(tc, dtype=torch.uint8, device=DEV),
@@ -116,7 +116,7 @@ def run_select(d_k, d_v, lens, q, refresh, flags=0, given=None):
     }
     if given is not None:
         out["probe_k"][:sum_b] = to_dev(np.concatenate(given[0]).astype(np.int32))
-        out["probe_v"][:sum_b] = to_dev(np.concatenate(given[1]).astype(np.int32))
+        out["probe_v"][:sum_bv] = to_dev(np.concatenate(given[1]).astype(np.int32))
     akvs.akvs_select_probes(to_dev(d_k.astype(np.float32)), to_dev(d_v.astype(np.float32)), cfg,
                             to_dev(meta), out["probe_k"], out["probe_v"], out["w_k"], out["w_v"],
                             out["flags"], out["chunk_rows"], out["rows"], out["n_rows"],
@@ -154,6 +154,34 @@ def test_select_probes_bit_exact(refresh):
         np.testing.assert_array_equal(got["w_v"], np.minimum(d_v, np.float32(1)))
 
 
+@pytest.mark.parametrize("refresh,refresh_v", [((1, 10), (1, 2)), ((1, 2), (0, 1)), ((0, 1), (3, 10))])
+def test_select_probes_value_ratio_bit_exact(refresh, refresh_v):
+    lens = [1, 7, 64, 65, 200, 1000]
+    q = 4
+    tc = sum(lens)
+    rng = np.random.default_rng(19)
+    d_k = rng.integers(0, 20, size=tc).astype(np.float32) * 0.25
+    d_v = rng.random(tc).astype(np.float32) * 3
+    got, sum_b, cap = run_select(d_k, d_v, lens, q, refresh, refresh_v=refresh_v)
+    starts = oracle.chunk_starts(lens)
+    bk = [oracle.probe_budget(n, *refresh) for n in lens]
+    bv = [oracle.probe_budget(n, *refresh_v) for n in lens]
+    sk = [oracle.select_top(d_k[s:s + n], b) + s for s, n, b in zip(starts, lens, bk)]
+    sv = [oracle.select_top(d_v[s:s + n], b) + s for s, n, b in zip(starts, lens, bv)]
+    assert list(got["probe_k"][:sum(bk)]) == [int(x) for x in np.concatenate(sk)]
+    assert list(got["probe_v"][:sum(bv)]) == [int(x) for x in np.concatenate(sv)]
+    in_k = np.zeros(tc, bool); in_v = np.zeros(tc, bool)
+    for p in sk: in_k[p] = True
+    for p in sv: in_v[p] = True
+    rows = np.concatenate([np.nonzero(in_k | in_v)[0], np.arange(tc, tc + q)])
+    assert int(got["n_rows"][0]) == len(rows) <= cap
+    np.testing.assert_array_equal(got["rows"][:len(rows)], rows)
+    wk = np.minimum(d_k, np.float32(1)) if refresh[0] else np.zeros(tc, np.float32)
+    wv = np.minimum(d_v, np.float32(1)) if refresh_v[0] else np.zeros(tc, np.float32)
+    np.testing.assert_array_equal(got["w_k"], wk)
+    np.testing.assert_array_equal(got["w_v"], wv)
+
+
 def test_select_given_probes_and_unit_weights():
     lens = [50, 80]
     rng = np.random.default_rng(10)
@@ -170,7 +198,7 @@ def test_select_given_probes_and_unit_weights():
     assert np.all(got["w_k"] == 1) and np.all(got["w_v"] == 1)
 
 
-def make_offset_case(dtype, lens, hkv, hd, seed, flags=0, refresh=(1, 5)):
+def make_offset_case(dtype, lens, hkv, hd, seed, flags=0, refresh=(1, 5), refresh_v=None):
     """Random cache, divergences and fresh rows; the probe sets, recomputed rows and weights
     come from the oracle's selection on the same divergences."""
     tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
@@ -181,8 +209,9 @@ def make_offset_case(dtype, lens, hkv, hd, seed, flags=0, refresh=(1, 5)):
     d_k = rng.random(tc).astype(np.float32) * 2
     d_v = rng.random(tc).astype(np.float32) * 2
     budgets = [oracle.probe_budget(n, *refresh) for n in lens]
+    budgets_v = [oracle.probe_budget(n, *(refresh_v or refresh)) for n in lens]
     sk = [oracle.select_top(d_k[s:s + n], b) + s for s, n, b in zip(starts, lens, budgets)]
-    sv = [oracle.select_top(d_v[s:s + n], b) + s for s, n, b in zip(starts, lens, budgets)]
+    sv = [oracle.select_top(d_v[s:s + n], b) + s for s, n, b in zip(starts, lens, budgets_v)]
     in_k = np.zeros(tc, bool)
     in_v = np.zeros(tc, bool)
     for p in sk:
@@ -205,13 +234,14 @@ def make_offset_case(dtype, lens, hkv, hd, seed, flags=0, refresh=(1, 5)):
     kf = storage_round(synthetic.random_array((cap, hkv, hd), seed + 3), tdt)
     vf = storage_round(synthetic.random_array((cap, hkv, hd), seed + 4), tdt)
     return dict(tdt=tdt, q=q, tc=tc, starts=starts, lens=lens, sel=sel, rows=rows, kc=kc, vc=vc,
-                kf=kf, vf=vf, refresh=refresh, flags=flags, budgets=budgets)
+                kf=kf, vf=vf, refresh=refresh, flags=flags, budgets=budgets, budgets_v=budgets_v,
+                refresh_v=refresh_v)
 
 
 def gpu_offset_and_correction(cs, hkv, hd, theta=1e6):
     lens, q = cs["lens"], cs["q"]
-    cfg = akvs.reuse_cfg(lens, q, cs["refresh"], 1, cs["flags"])
-    meta, (tc, sum_b, cap, t_all) = akvs.akvs_chunk_meta(cfg)
+    cfg = akvs.reuse_cfg(lens, q, cs["refresh"], 1, cs["flags"], cs["refresh_v"])
+    meta, (tc, sum_b, cap, t_all, sum_bv) = akvs.akvs_chunk_meta(cfg)
     m = akvs.ModelCfg(1, 64, hkv, hkv, hd, 64, 16, theta, 1e-6, akvs.dtype_code(cs["kc"]))
     tab = rope(t_all, hd, theta)
     sel = {k: to_dev(v) for k, v in cs["sel"].items()}
@@ -234,6 +264,7 @@ def oracle_offset_and_correction(cs, theta=1e6):
     lens, starts, q, tc = cs["lens"], cs["starts"], cs["q"], cs["tc"]
     sel = cs["sel"]
     off = np.concatenate([[0], np.cumsum(cs["budgets"])])
+    off_v = np.concatenate([[0], np.cumsum(cs["budgets_v"])])
     kc, vc, kf, vf = (f64(cs[k]) for k in ("kc", "vc", "kf", "vf"))
     reuse_k = np.concatenate([oracle.rerotate(kc[s:s + n], s, theta) for s, n in zip(starts, lens)])
     fresh_k = np.zeros((tc + q,) + kc.shape[1:])
@@ -244,28 +275,42 @@ def oracle_offset_and_correction(cs, theta=1e6):
     flags = cs["flags"]
     for i, (s, n) in enumerate(zip(starts, lens)):
         pk = sel["probe_k"][off[i]:off[i + 1]]
-        pv = sel["probe_v"][off[i]:off[i + 1]]
+        pv = sel["probe_v"][off_v[i]:off_v[i + 1]]
+        pre = bool(flags & oracle.F_PRE_ROPE_OFFSETS)
         if flags & oracle.F_NO_CORRECTION:
             mk = np.zeros(kc.shape[1:]); mv = np.zeros(kc.shape[1:])
+        elif pre:
+            mk = oracle.probe_offset_pre_rope(fresh_k[pk], reuse_k[pk], pk, theta)
+            mv = oracle.probe_offset(fresh_v[pv], vc[pv])
         else:
             mk = oracle.probe_offset(fresh_k[pk], reuse_k[pk])
             mv = oracle.probe_offset(fresh_v[pv], vc[pv])
         mus_k.append(mk); mus_v.append(mv)
         f = sel["flags"][s:s + n]
         any_ = (f != 0) if flags & oracle.F_FRESH_IF_RECOMPUTED else np.zeros(n, bool)
-        ck.append(oracle.correct_chunk(reuse_k[s:s + n], fresh_k[s:s + n], (f & 1).astype(bool) | any_,
-                                       sel["w_k"][s:s + n], mk))
+        fk = (f & 1).astype(bool) | any_
+        if pre:
+            ck.append(oracle.correct_chunk_pre_rope(reuse_k[s:s + n], fresh_k[s:s + n], fk,
+                                                    sel["w_k"][s:s + n], mk, np.arange(s, s + n),
+                                                    theta))
+        else:
+            ck.append(oracle.correct_chunk(reuse_k[s:s + n], fresh_k[s:s + n], fk,
+                                           sel["w_k"][s:s + n], mk))
         cv.append(oracle.correct_chunk(vc[s:s + n], fresh_v[s:s + n], (f & 2).astype(bool) | any_,
                                        sel["w_v"][s:s + n], mv))
     ck.append(fresh_k[tc:]); cv.append(fresh_v[tc:])
     return np.stack(mus_k), np.stack(mus_v), np.concatenate(ck), np.concatenate(cv)
 
 
-@pytest.mark.parametrize("dtype,hkv,hd,flags", [
-    ("bf16", 8, 128, 0), ("f32", 4, 64, 0), ("bf16", 4, 128, akvs.AKVS_F_FRESH_IF_RECOMPUTED),
-    ("bf16", 2, 64, akvs.AKVS_F_NO_CORRECTION), ("f32", 2, 128, akvs.AKVS_F_UNIT_WEIGHTS)])
-def test_chunk_offset_and_correction(dtype, hkv, hd, flags):
-    cs = make_offset_case(dtype, [23, 64, 1, 150], hkv, hd, seed=11, flags=flags)
+@pytest.mark.parametrize("dtype,hkv,hd,flags,refresh_v", [
+    ("bf16", 8, 128, 0, None), ("f32", 4, 64, 0, None),
+    ("bf16", 4, 128, akvs.AKVS_F_FRESH_IF_RECOMPUTED, None),
+    ("bf16", 2, 64, akvs.AKVS_F_NO_CORRECTION, None), ("f32", 2, 128, akvs.AKVS_F_UNIT_WEIGHTS, None),
+    ("bf16", 8, 128, akvs.AKVS_F_PRE_ROPE_OFFSETS, None), ("f32", 4, 64, akvs.AKVS_F_PRE_ROPE_OFFSETS, None),
+    ("bf16", 8, 128, 0, (1, 2)), ("f32", 4, 64, akvs.AKVS_F_PRE_ROPE_OFFSETS, (0, 1))])
+def test_chunk_offset_and_correction(dtype, hkv, hd, flags, refresh_v):
+    cs = make_offset_case(dtype, [23, 64, 1, 150], hkv, hd, seed=11, flags=flags,
+                          refresh_v=refresh_v)
     mu_k, mu_v, k_corr, v_corr = gpu_offset_and_correction(cs, hkv, hd)
     rmk, rmv, rck, rcv = oracle_offset_and_correction(cs)
     tol = 1e-5
