@@ -97,11 +97,11 @@ def traffic_summary(fetch_csv, write_csv):
         "# k_gemm_bf16 HBM traffic, 3B-class reuse prefill (r=1/5), bench.py counter runs",
         "# commands (from the repository root, on the GPU box):",
         "#   rocprofv3 --pmc FETCH_SIZE -f csv -d OUT/fetch -o run -- python3 bench.py --steps 2 "
-        "--warmup 1 --no-cpu-baseline --no-full --no-graph --refresh-sweep none --random-caches "
-        "--calibrate-copy",
+        "--warmup 1 --no-cpu-baseline --no-full --no-graph --no-decode --refresh-sweep none "
+        "--batch-sweep none --random-caches --calibrate-copy",
         "#   rocprofv3 --pmc WRITE_SIZE -f csv -d OUT/write -o run -- python3 bench.py --steps 2 "
-        "--warmup 1 --no-cpu-baseline --no-full --no-graph --refresh-sweep none --random-caches "
-        "--calibrate-copy",
+        "--warmup 1 --no-cpu-baseline --no-full --no-graph --no-decode --refresh-sweep none "
+        "--batch-sweep none --random-caches --calibrate-copy",
         "#   python3 bench.py --traffic-summary OUT/fetch/run_counter_collection.csv "
         "OUT/write/run_counter_collection.csv",
         f"source_sha256_16: {source_hash()}",
