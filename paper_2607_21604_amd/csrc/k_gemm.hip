@@ -7,6 +7,7 @@
 // next tile prefetched into registers during the MFMA loop. The accumulator tile is
 // staged through LDS so every epilogue can pair columns (rotary halves, gate/up) and
 // write coalesced rows. fp32 path (small models): 32x128x32 VALU tiles, same epilogues.
+#include <algorithm>
 #include <type_traits>
 
 #include "kernels.h"
@@ -327,6 +328,190 @@ __global__ __launch_bounds__(256, 2) void k_gemm_bf16(const bf16_t *__restrict__
   epilogue_tile<BM, GB_N, 256>(Cs, G_CLD, m0, n0, M_eff, N, epi);
 }
 
+// ------------------------------------------------------------------------------------------
+// bf16 MFMA GEMM with 8 waves: 512-thread blocks (two waves per SIMD) on BM x BN x 64 block
+// tiles, BM in {192, 256}, BN in {128, 256}. Waves form WGM x (8 / WGM), each owning
+// (BM / WGM) x (BN * WGM / 8) outputs as v_mfma_f32_32x32x16_bf16 tiles. Against 128x128
+// tiles of four waves this halves the operand bytes per flop while keeping two waves per
+// SIMD. Operands arrive through buffer loads into NST register stages; each k-tile's LDS
+// stores and global refills are spread over its four k-steps between the MFMAs
+// (scheduling groups), so every wait before an LDS store covers only loads issued a tile
+// earlier. The accumulators go through LDS half a tile of rows at a time for the shared
+// epilogues. Rows past the device-side M are skipped, operand rows past M / N are clamped
+// to valid rows (their results are discarded).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t gemm_rsrc(const void *p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, (int)bytes,
+                                           0x00020000);
+}
+
+template <int BM, int BN, int WGM, int NST>
+struct Gemm8 {
+  static constexpr int WGN = 8 / WGM, WM = BM / WGM, WN = BN / WGN;
+  static constexpr int MI = WM / 32, NJ = WN / 32;
+  static constexpr int ACH = BM / 64, BCH = BN / 64, CH = ACH + BCH;  // 16-B chunks per thread
+  static constexpr int ATILE = BM * G_LDS, BUF = (BM + BN) * G_LDS;  // bf16 elements
+  static constexpr int HB = BM / 2, CLD = BN + 4;                    // epilogue half tile
+  static constexpr int LOOP_BYTES = 2 * BUF * 2, C_BYTES = HB * CLD * 4;
+  static constexpr int SMEM = LOOP_BYTES > C_BYTES ? LOOP_BYTES : C_BYTES;
+  static_assert(WGM == 2 || WGM == 4, "wave rows must split in two halves");
+};
+
+template <int BM, int BN, int WGM, int NST>
+__global__ __launch_bounds__(512, 1) void k_gemm_bf16_w8(const bf16_t *__restrict__ A, int lda,
+                                                         const bf16_t *__restrict__ B, int ldb,
+                                                         int M, int N, int K,
+                                                         const int32_t *m_dev, Epi epi) {
+  using S = Gemm8<BM, BN, WGM, NST>;
+  __shared__ __attribute__((aligned(16))) unsigned char smem[S::SMEM];
+  bf16_t *sm = reinterpret_cast<bf16_t *>(smem);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / S::WGN, wn = wave % S::WGN;
+  int M_eff = M;
+  if (m_dev) M_eff = min(M, *m_dev);
+  const bool swiglu = epi.mode == EPI_SWIGLU;
+  const int bn_out = swiglu ? BN / 2 : BN;
+  const int n_tiles = (N + bn_out - 1) / bn_out;
+  const int tile = blockIdx.x;
+  if (tile >= ((M_eff + BM - 1) / BM) * n_tiles) return;
+  const int m0 = (tile / n_tiles) * BM;
+  const int n0 = (tile - (tile / n_tiles) * n_tiles) * bn_out;
+  const __amdgpu_buffer_rsrc_t ra = gemm_rsrc(A, (uint32_t)((size_t)M_eff * lda * 2));
+  const __amdgpu_buffer_rsrc_t rb =
+      gemm_rsrc(B, (uint32_t)((size_t)(swiglu ? 2 * N : N) * ldb * 2));
+
+  // chunk c of a thread: row (tid >> 3) + 64 c of the stacked [A tile; B tile], k columns
+  // (tid & 7) * 8 ..+7; SWIGLU B tiles stack BN/2 gate rows over the matching up rows
+  int goff[S::CH], loff[S::CH];
+#pragma unroll
+  for (int c = 0; c < S::CH; ++c) {
+    const int r = (tid >> 3) + 64 * c, kc = (tid & 7) * 8;
+    if (c < S::ACH) {
+      goff[c] = (min(m0 + r, M_eff - 1) * lda + kc) * 2;
+    } else {
+      const int rb_ = r - BM;
+      int gn;
+      if (swiglu) {
+        const int oc = min(n0 + (rb_ & (BN / 2 - 1)), N - 1);
+        gn = rb_ < BN / 2 ? oc : N + oc;
+      } else {
+        gn = min(n0 + rb_, N - 1);
+      }
+      goff[c] = (gn * ldb + kc) * 2;
+    }
+    loff[c] = r * G_LDS + kc;
+  }
+  const int nk = K / GB_K;
+
+  f32x16_t acc[S::MI][S::NJ];
+#pragma unroll
+  for (int i = 0; i < S::MI; ++i)
+#pragma unroll
+    for (int j = 0; j < S::NJ; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+  u32x4_t rg[NST][S::CH];
+  bf16x8_t fa[2][S::MI], fb[2][S::NJ];
+  const int fa_lane = (wm * S::WM + (lane & 31)) * G_LDS + (lane >> 5) * 8;
+  const int fb_lane = S::ATILE + (wn * S::WN + (lane & 31)) * G_LDS + (lane >> 5) * 8;
+
+#define AKVS_W8_GL(ST, KT, C0, C1)                                                          \
+  {                                                                                         \
+    const int so_ = (KT) * GB_K * 2;                                                        \
+    _Pragma("unroll") for (int c = (C0); c < (C1); ++c) rg[ST][c] = __builtin_bit_cast(     \
+        u32x4_t, c < S::ACH ? __builtin_amdgcn_raw_buffer_load_b128(ra, goff[c], so_, 0)    \
+                            : __builtin_amdgcn_raw_buffer_load_b128(rb, goff[c], so_, 0));  \
+  }
+#define AKVS_W8_SS(ST, BOFF, C0, C1)                                                        \
+  {                                                                                         \
+    bf16_t *b_ = sm + (BOFF);                                                               \
+    _Pragma("unroll") for (int c = (C0); c < (C1); ++c)                                     \
+        *reinterpret_cast<u32x4_t *>(b_ + loff[c]) = rg[ST][c];                             \
+  }
+#define AKVS_W8_FR(F, BOFF, KS)                                                             \
+  {                                                                                         \
+    const bf16_t *As_ = sm + (BOFF) + fa_lane + (KS) * 16;                                  \
+    const bf16_t *Bs_ = sm + (BOFF) + fb_lane + (KS) * 16;                                  \
+    _Pragma("unroll") for (int i = 0; i < S::MI; ++i) fa[F][i] =                            \
+        *reinterpret_cast<const bf16x8_t *>(As_ + i * 32 * G_LDS);                          \
+    _Pragma("unroll") for (int j = 0; j < S::NJ; ++j) fb[F][j] =                            \
+        *reinterpret_cast<const bf16x8_t *>(Bs_ + j * 32 * G_LDS);                          \
+  }
+  // k-tile T from LDS buffer `cur`; ring slot P holds tile T+1, which goes to buffer `nxt`
+  // a quarter per k-step while the slot refills with tile T+NST+1 (loads past the range
+  // re-read the last tile, so every load is unconditional and the waits stay exact)
+#define AKVS_W8_ITER(T, P)                                                                  \
+  {                                                                                         \
+    AKVS_W8_FR(0, cur, 0);                                                                  \
+    _Pragma("unroll") for (int ks = 0; ks < 4; ++ks) {                                      \
+      if (ks < 3) AKVS_W8_FR((ks + 1) & 1, cur, ks + 1);                                    \
+      const int q0_ = ks * S::CH / 4, q1_ = (ks + 1) * S::CH / 4;                           \
+      AKVS_W8_SS(P, nxt, q0_, q1_);                                                         \
+      AKVS_W8_GL(P, min((T) + NST + 1, nk - 1), q0_, q1_);                                  \
+      _Pragma("unroll") for (int i = 0; i < S::MI; ++i)                                     \
+          _Pragma("unroll") for (int j = 0; j < S::NJ; ++j) acc[i][j] =                     \
+              __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[ks & 1][i], fb[ks & 1][j],         \
+                                                      acc[i][j], 0, 0, 0);                  \
+      _Pragma("unroll") for (int g_ = 0; g_ < S::MI * S::NJ; ++g_) {                        \
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                                  \
+        if (ks < 3 && g_ < S::MI + S::NJ) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0); \
+        if (g_ < q1_ - q0_) __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);              \
+        if (g_ >= (S::MI * S::NJ) / 2 && g_ < (S::MI * S::NJ) / 2 + (q1_ - q0_))            \
+          __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);                                \
+      }                                                                                     \
+      __builtin_amdgcn_sched_barrier(0);                                                    \
+    }                                                                                       \
+    __syncthreads();                                                                        \
+    {                                                                                       \
+      const int t_ = cur;                                                                   \
+      cur = nxt;                                                                            \
+      nxt = t_;                                                                             \
+    }                                                                                       \
+  }
+  int cur = 0, nxt = S::BUF;
+  AKVS_W8_GL(0, 0, 0, S::CH);
+  AKVS_W8_SS(0, 0, 0, S::CH);
+#pragma unroll
+  for (int st = 0; st < NST; ++st) AKVS_W8_GL(st, min(1 + st, nk - 1), 0, S::CH);
+  __syncthreads();
+  int t = 0;
+  if (NST == 1) {
+    for (; t < nk; ++t) AKVS_W8_ITER(t, 0);
+  } else {
+    for (; t + 2 <= nk; t += 2) {
+      AKVS_W8_ITER(t, 0);
+      AKVS_W8_ITER(t + 1, NST - 1);
+    }
+    if (t < nk) AKVS_W8_ITER(t, 0);
+  }
+#undef AKVS_W8_ITER
+#undef AKVS_W8_FR
+#undef AKVS_W8_SS
+#undef AKVS_W8_GL
+
+  // epilogue: rows [h * HB, (h + 1) * HB) of the tile belong to waves wm / (WGM / 2) == h
+  float *Cs = reinterpret_cast<float *>(smem);
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    if (m0 + h * S::HB >= M_eff) break;  // block-uniform
+    if (wm / (WGM / 2) == h) {
+#pragma unroll
+      for (int i = 0; i < S::MI; ++i)
+#pragma unroll
+        for (int j = 0; j < S::NJ; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int row = wm * S::WM - h * S::HB + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 +
+                            (r & 3);
+            const int col = wn * S::WN + j * 32 + (lane & 31);
+            Cs[row * S::CLD + col] = acc[i][j][r];
+          }
+    }
+    __syncthreads();
+    epilogue_tile<S::HB, BN, 512>(Cs, S::CLD, m0 + h * S::HB, n0, M_eff, N, epi);
+    __syncthreads();
+  }
+}
+
 // Second pass of a K-split GEMM: a block takes G_FR rows of one tile, adds their partial
 // rows in split order into an LDS slice and runs the epilogue on it.
 constexpr int G_FR = 16;
@@ -497,12 +682,64 @@ static GemmPlan gemm_plan(int M, int N, int K, const int32_t *m_dev, const Epi &
   return p;
 }
 
+// Block tiles of the 8-wave kernel with their main-loop rate per CU relative to 256x256
+// (measured at the 3B projection shapes). A launch takes the tile with the least
+// (rounds of one tile per CU) x (tile area) / rate, at the expected row count.
+struct W8Tile {
+  int bm, bn;
+  double rate;
+};
+static const W8Tile kW8Tiles[] = {{256, 256, 1.0}, {192, 256, 0.99}, {256, 128, 0.92},
+                                  {192, 128, 0.88}};
+constexpr int kW8Count = sizeof(kW8Tiles) / sizeof(kW8Tiles[0]);
+
+static int gemm_w8_tile(int M_est, int N, int mode) {
+  const long long cus = gemm_cu_count();
+  int best = 0;
+  double best_cost = 0;
+  for (int i = 0; i < kW8Count; ++i) {
+    const W8Tile &c = kW8Tiles[i];
+    const int bn_out = mode == EPI_SWIGLU ? c.bn / 2 : c.bn;
+    const long long tiles =
+        (long long)((M_est + c.bm - 1) / c.bm) * ((N + bn_out - 1) / bn_out);
+    const double cost = (double)((tiles + cus - 1) / cus) * c.bm * c.bn / c.rate;
+    if (i == 0 || cost < best_cost) {
+      best = i;
+      best_cost = cost;
+    }
+  }
+  return best;
+}
+
+template <int BM, int BN, int WGM, int NST>
+static void launch_w8(const void *A, int lda, const void *B, int ldb, int M, int N, int K,
+                      const int32_t *m_dev, const Epi &epi, hipStream_t s) {
+  const int bn_out = epi.mode == EPI_SWIGLU ? BN / 2 : BN;
+  const int grid = ((M + BM - 1) / BM) * ((N + bn_out - 1) / bn_out);
+  hipLaunchKernelGGL((k_gemm_bf16_w8<BM, BN, WGM, NST>), dim3(grid), dim3(512), 0, s,
+                     reinterpret_cast<const bf16_t *>(A), lda,
+                     reinterpret_cast<const bf16_t *>(B), ldb, M, N, K, m_dev, epi);
+}
+
 hipError_t launch_gemm(const void *A, int lda, const void *B, int ldb, int M, int N, int K,
                        const int32_t *m_dev, int dtype, const Epi &epi, hipStream_t s,
                        float *part, int m_min) {
   if (M == 0 || N == 0) return hipSuccess;
   if (dtype == AKVS_BF16) {
     const GemmPlan p = gemm_plan(M, N, K, m_dev, epi, part, m_min);
+    const size_t b_rows = epi.mode == EPI_SWIGLU ? 2 * (size_t)N : (size_t)N;
+    // buffer offsets are 32-bit: larger operands stay on the 4-wave kernel
+    const bool fits = (size_t)M * lda * 2 < (1u << 31) && b_rows * ldb * 2 < (1u << 31);
+    if (!p.any_split && fits) {
+      const int M_est = m_dev ? (std::max(m_min, 1) + M) / 2 : M;
+      switch (gemm_w8_tile(M_est, N, epi.mode)) {
+        case 0: launch_w8<256, 256, 2, 1>(A, lda, B, ldb, M, N, K, m_dev, epi, s); break;
+        case 1: launch_w8<192, 256, 2, 1>(A, lda, B, ldb, M, N, K, m_dev, epi, s); break;
+        case 2: launch_w8<256, 128, 4, 2>(A, lda, B, ldb, M, N, K, m_dev, epi, s); break;
+        default: launch_w8<192, 128, 2, 2>(A, lda, B, ldb, M, N, K, m_dev, epi, s); break;
+      }
+      return hipGetLastError();
+    }
     hipLaunchKernelGGL((k_gemm_bf16<128, false>), dim3(p.items), dim3(256), 0, s,
                        reinterpret_cast<const bf16_t *>(A), lda,
                        reinterpret_cast<const bf16_t *>(B), ldb, M, N, K, m_dev, epi, p.n_slots,

@@ -84,10 +84,13 @@ def test_fullsize_attention_sampled_rows():
     assert max_rel(f64(out_split), f64(out_plain)) < 1e-2
 
 
-def test_fullsize_probe_layer_gemms_sampled_rows():
-    """QKV projection and O-proj + MLP of M ~ 1400 rows at the full 3B width (the probe
-    layers' GEMM shapes, split-K choice included); 32 sampled rows against the oracle."""
-    pos = probe_like_positions(3)
+@pytest.mark.parametrize("rows_kind", ["probe", "all"])
+def test_fullsize_probe_layer_gemms_sampled_rows(rows_kind):
+    """QKV projection and O-proj + MLP at the full 3B width, over M ~ 1400 probe-like rows
+    (the probe layers' GEMM shapes) and over all T = 4516 rows (the prefix layers'); the
+    two row counts take every block-tile shape of the projection GEMM between them. About
+    40 sampled rows, the rows at tile edges among them, against the oracle."""
+    pos = probe_like_positions(3) if rows_kind == "probe" else np.arange(T, dtype=np.int32)
     n = len(pos)
     w = synthetic.make_weights(SHAPE, seed=5, n_layers=1, embed=False)
     dims = oracle.dims_from(SHAPE.with_layers(1))
@@ -107,7 +110,8 @@ def test_fullsize_probe_layer_gemms_sampled_rows():
     att = storage_round(synthetic.random_array((n, hq * hd), 7), torch.bfloat16)
     akvs.akvs_probe_out_mlp(h_dev, n, to_dev(att), m, lws, ws)
     torch.cuda.synchronize()
-    rows = sample_rows(n, 29, 4)
+    edges = [e for e in (95, 96, 127, 128, 191, 192, 255, 256, 1279, 1280, 4479, 4480) if e < n]
+    rows = np.union1d(sample_rows(n, 29, 4), edges)
     sw = oracle.split_layer(lw, dims)
     h64 = h.astype(np.float64)[rows]
     rq, rk, rv = oracle.model.project_qkv(h64, pos[rows], sw, dims)
