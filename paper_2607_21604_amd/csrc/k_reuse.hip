@@ -249,102 +249,109 @@ hipError_t launch_select(const float *d_k, const float *d_v, const int32_t *meta
 }
 
 // ---------------------------------------------------------------------------------------
-// Per-unit offsets. grid = (m, 2 sides); block = up to 16 waves. Wave w sums the probes
-// k = w, w + W, ... of the unit in ascending order; lane u handles the 8 lo/hi element
-// pairs e0..e0+7 (and + hd/2) of head u / (hd/16), so a wave reads a whole K (or V) row per
-// probe with 16-byte loads. The W wave partials are then added in wave order through LDS:
-// a fixed fp32 summation order.
-constexpr int OFF_LDS = 16384;  // floats: waves x Hkv*hd partial rows
+// Per-unit offsets. grid = (m units, Hkv heads, 2 sides); block = 256 threads in groups of
+// hd/16 lanes. Lane l of a group owns the rotate-half pairs (8l + i, 8l + i + hd/2), i < 8,
+// of the block's head, so a group reads one probe's head slice as two contiguous runs.
+// Group g sums the probes k = g, g + G, ... of the unit in ascending k (two per step, both
+// loads in flight); the G group partials are then added in a fixed order through LDS
+// (each half of the block sums G/2 partials in group order, then the two halves), and
+// the sum is divided by b_i: a deterministic fp32 order. Splitting by head gives
+// m * Hkv * 2 blocks, enough to fill the chip with one short dependent chain each.
+constexpr int OFF_THREADS = 256;
 
-template <typename TF, int UP>
-__global__ __launch_bounds__(UP == 1 ? 1024 : 512) void k_chunk_offset(const TF *__restrict__ k_fresh,
-                                                       const TF *__restrict__ v_fresh,
-                                                       const int32_t *fresh_row, CacheLayer cache,
-                                                       const int4 *meta, const int32_t *probe_k,
-                                                       const int32_t *probe_v, uint32_t flags,
-                                                       int hkv, int hd, const float2 *rope,
-                                                       int rope_rows, float *mu_k, float *mu_v,
-                                                       const int32_t *fresh_base) {
-  __shared__ float s_part[OFF_LDS];
-  const int c = blockIdx.x;
-  const int side = blockIdx.y;  // 0 = K, 1 = V
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
-  const int half = hd >> 1, upr = half >> 3;  // 8-pair units per head
-  const int units = hkv * upr;                // <= 64 * UP
-  const int kvw = hkv * hd;
-  const int4 mc = meta[side * gridDim.x + c];  // this side's table
+template <typename TF>
+__global__ __launch_bounds__(OFF_THREADS) void k_chunk_offset(
+    const TF *__restrict__ k_fresh, const TF *__restrict__ v_fresh,
+    const int32_t *__restrict__ fresh_row, CacheLayer cache, const int4 *__restrict__ meta,
+    const int32_t *__restrict__ probe_k, const int32_t *__restrict__ probe_v, uint32_t flags,
+    int hkv, int hd, const float2 *__restrict__ rope, int rope_rows, float *mu_k, float *mu_v,
+    const int32_t *fresh_base) {
+  __shared__ float s_part[OFF_THREADS * 16];  // G partial head slices (G * hd floats)
+  __shared__ float s_half[2 * 128];
+  const int c = blockIdx.x, h = blockIdx.y, side = blockIdx.z;
+  const int n_chunks = gridDim.x;
+  const int lps = hd >> 4, G = OFF_THREADS / lps;
+  const int g = threadIdx.x / lps, l = threadIdx.x - g * lps;
+  const int half = hd >> 1, e0 = 8 * l;
+  const size_t rstride = (size_t)hkv * hd, hoff = (size_t)h * hd;
+  const int4 mc = meta[side * n_chunks + c];  // this side's table
   const int b = mc.z;
-  const bool pre_rope = side == 0 && (flags & AKVS_F_PRE_ROPE_OFFSETS);
-  float *mu = (side == 0 ? mu_k : mu_v) + (size_t)c * kvw;
+  float *mu = (side == 0 ? mu_k : mu_v) + (size_t)c * rstride + hoff;
   if (b == 0 || (flags & AKVS_F_NO_CORRECTION)) {
-    for (int e = threadIdx.x; e < kvw; e += blockDim.x) mu[e] = 0.f;
+    if (threadIdx.x < hd) mu[threadIdx.x] = 0.f;
     return;
   }
+  const bool pre_rope = side == 0 && (flags & AKVS_F_PRE_ROPE_OFFSETS);
+  const int fresh_off = fresh_base ? *fresh_base : 0;
   const TF *fresh = side == 0 ? k_fresh : v_fresh;
   const void *cb = side == 0 ? cache.k : cache.v;
   const _Float16 *cm = side == 0 ? cache.k_meta : cache.v_meta;
   const int32_t *probes = (side == 0 ? probe_k : probe_v) + mc.w;
   const int delta = (mc.x >= 0 && mc.x < rope_rows) ? mc.x : 0;
   const float2 *rrow = rope + (size_t)delta * half;
-  float acc[UP][16];
+  float alo[8], ahi[8];
 #pragma unroll
-  for (int q = 0; q < UP; ++q)
+  for (int i = 0; i < 8; ++i) alo[i] = ahi[i] = 0.f;
+  for (int k0 = g; k0 < b; k0 += 2 * G) {
+    float flo[2][8], fhi[2][8], clo[2][8], chi[2][8];
+    int jj[2];
+    bool ok[2];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) acc[q][i] = 0.f;
-#pragma unroll 2
-  for (int k = wave; k < b; k += nw) {
-    const int j = probes[k];
-    const bool inside = j >= mc.x && j < mc.x + mc.y;  // a token of this unit
-    int r = inside ? fresh_row[j] : -1;
-    if (r < 0) continue;  // uniform over the wave
-    if (fresh_base) r += *fresh_base;
-#pragma unroll
-    for (int q = 0; q < UP; ++q) {
-      const int u = lane + 64 * q;
-      if (u < units) {
-        const int h = u / upr, e0 = (u - h * upr) * 8;
-        float flo[8], fhi[8], clo[8], chi[8];
-        const TF *fr = fresh + ((size_t)r * hkv + h) * hd;
-        load8(fr + e0, flo);
-        load8(fr + e0 + half, fhi);
-        const size_t crow = (size_t)j * hkv + h;
-        cache_load8(cb, cm, cache.dtype, crow, hd, e0, clo);
-        cache_load8(cb, cm, cache.dtype, crow, hd, e0 + half, chi);
-        if (side == 0) rotate8(rrow, e0, clo, chi);
-        float dlo[8], dhi[8];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          dlo[i] = flo[i] - clo[i];
-          dhi[i] = fhi[i] - chi[i];
-        }
-        if (pre_rope) unrotate8(rope + (size_t)min(j, rope_rows - 1) * half, e0, dlo, dhi);
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          acc[q][i] += dlo[i];
-          acc[q][8 + i] += dhi[i];
-        }
+    for (int u = 0; u < 2; ++u) {
+      const int k = k0 + u * G;
+      int j = k < b ? probes[k] : -1;
+      ok[u] = j >= mc.x && j < mc.x + mc.y;  // a token of this unit
+      int r = ok[u] ? fresh_row[j] : -1;
+      ok[u] = r >= 0;
+      if (!ok[u]) {  // contributes nothing: read a valid row, drop it below
+        j = mc.x;
+        r = 0;
+      } else {
+        r += fresh_off;
       }
+      jj[u] = j;
+      const TF *fr = fresh + (size_t)r * rstride + hoff;
+      load8(fr + e0, flo[u]);
+      load8(fr + e0 + half, fhi[u]);
+      const size_t crow = (size_t)j * hkv + h;
+      cache_load8(cb, cm, cache.dtype, crow, hd, e0, clo[u]);
+      cache_load8(cb, cm, cache.dtype, crow, hd, e0 + half, chi[u]);
     }
-  }
 #pragma unroll
-  for (int q = 0; q < UP; ++q) {
-    const int u = lane + 64 * q;
-    if (u < units) {
-      const int h = u / upr, e0 = (u - h * upr) * 8;
-      float *dst = s_part + wave * kvw + h * hd + e0;
+    for (int u = 0; u < 2; ++u) {
+      if (!ok[u]) continue;
+      if (side == 0) rotate8(rrow, e0, clo[u], chi[u]);
+      float dlo[8], dhi[8];
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
-        dst[i] = acc[q][i];
-        dst[half + i] = acc[q][8 + i];
+        dlo[i] = flo[u][i] - clo[u][i];
+        dhi[i] = fhi[u][i] - chi[u][i];
+      }
+      if (pre_rope) unrotate8(rope + (size_t)min(jj[u], rope_rows - 1) * half, e0, dlo, dhi);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        alo[i] += dlo[i];
+        ahi[i] += dhi[i];
       }
     }
   }
-  __syncthreads();
-  for (int e = threadIdx.x; e < kvw; e += blockDim.x) {
-    float t = 0.f;
-    for (int w = 0; w < nw; ++w) t += s_part[w * kvw + e];
-    mu[e] = t / (float)b;
+  float *dst = s_part + g * hd;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    dst[e0 + i] = alo[i];
+    dst[e0 + half + i] = ahi[i];
   }
+  __syncthreads();
+  // thread = (element e, half p): partials p*G/2 .. (p+1)*G/2 - 1 in group order
+  const int e = threadIdx.x % hd, p = threadIdx.x / hd;
+  const int gh = G >> 1;
+  if (p < 2) {
+    float t = 0.f;
+    for (int w = p * gh; w < (p + 1) * gh; ++w) t += s_part[w * hd + e];
+    s_half[p * hd + e] = t;
+  }
+  __syncthreads();
+  if (threadIdx.x < hd) mu[threadIdx.x] = (s_half[threadIdx.x] + s_half[hd + threadIdx.x]) / (float)b;
 }
 
 hipError_t launch_chunk_offset(const void *k_fresh, const void *v_fresh, int fresh_dtype,
@@ -353,25 +360,19 @@ hipError_t launch_chunk_offset(const void *k_fresh, const void *v_fresh, int fre
                                uint32_t flags, int hkv, int hd, const float *rope, int rope_rows,
                                float *mu_k, float *mu_v, hipStream_t s,
                                const int32_t *fresh_base) {
-  const int kvw = hkv * hd;
-  if (kvw > 2048 || hd % 16) return hipErrorInvalidValue;
-  int nw = OFF_LDS / kvw;
-  if (nw > 16) nw = 16;
-  if (kvw > 1024 && nw > 8) nw = 8;  // two units per lane: 8 waves of up to 256 registers
-  dim3 g(n_chunks, 2), b(64 * nw);
+  if (hd != 64 && hd != 128) return hipErrorInvalidValue;
+  if (n_chunks < 1) return hipSuccess;
+  dim3 g(n_chunks, hkv, 2), b(OFF_THREADS);
   const int4 *m4 = reinterpret_cast<const int4 *>(meta);
   const float2 *r = reinterpret_cast<const float2 *>(rope);
-#define AKVS_OFFSET(TF, UP)                                                                    \
-  hipLaunchKernelGGL((k_chunk_offset<TF, UP>), g, b, 0, s, as<TF>(k_fresh), as<TF>(v_fresh),      \
-                     fresh_row, cache, m4, probe_k, probe_v, flags, hkv, hd, r, rope_rows, mu_k, \
-                     mu_v, fresh_base)
-  const bool wide = kvw > 1024;
-  if (fresh_dtype == AKVS_BF16) {
-    if (wide) AKVS_OFFSET(bf16_t, 2); else AKVS_OFFSET(bf16_t, 1);
-  } else {
-    if (wide) AKVS_OFFSET(float, 2); else AKVS_OFFSET(float, 1);
-  }
-#undef AKVS_OFFSET
+  if (fresh_dtype == AKVS_BF16)
+    hipLaunchKernelGGL(k_chunk_offset<bf16_t>, g, b, 0, s, as<bf16_t>(k_fresh),
+                       as<bf16_t>(v_fresh), fresh_row, cache, m4, probe_k, probe_v, flags, hkv,
+                       hd, r, rope_rows, mu_k, mu_v, fresh_base);
+  else
+    hipLaunchKernelGGL(k_chunk_offset<float>, g, b, 0, s, as<float>(k_fresh),
+                       as<float>(v_fresh), fresh_row, cache, m4, probe_k, probe_v, flags, hkv,
+                       hd, r, rope_rows, mu_k, mu_v, fresh_base);
   return hipGetLastError();
 }
 

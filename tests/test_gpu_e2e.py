@@ -22,10 +22,11 @@ def lib():
 class Case:
     """A model, a context of units + query, oracle-made unit caches and a GPU engine."""
 
-    def __init__(self, name, n_layers=None, n_units=None, seed=0):
+    def __init__(self, name, n_layers=None, n_units=None, seed=0, lens=None):
         wl = synthetic.workload(name, seed)
         self.shape = wl.shape if n_layers is None else wl.shape.with_layers(n_layers)
-        self.lens = list(wl.chunk_lens[:n_units] if n_units else wl.chunk_lens)
+        self.lens = list(lens) if lens else list(
+            wl.chunk_lens[:n_units] if n_units else wl.chunk_lens)
         self.q = wl.query_len
         self.refresh = wl.refresh[0]
         self.tdt = synthetic.torch_dtype(self.shape)
@@ -215,3 +216,17 @@ def test_3b_width_pre_rope_offsets(w3b):
     ref = w3b.oracle(flags=akvs.AKVS_F_PRE_ROPE_OFFSETS)
     out = w3b.gpu(flags=akvs.AKVS_F_PRE_ROPE_OFFSETS, probes=(ref["probe_k"], ref["probe_v"]))
     w3b.compare(out, ref)
+
+
+@pytest.fixture(scope="module")
+def long_units():
+    # a unit longer than one correction segment (512 tokens): its offsets take their own
+    # pass and the correction runs over several segments of the unit
+    return Case("tiny", lens=[600, 40, 130])
+
+
+@pytest.mark.parametrize("flags", [0, akvs.AKVS_F_PRE_ROPE_OFFSETS])
+def test_tiny_long_unit_reuse_prefill(long_units, flags):
+    ref = long_units.oracle(flags=flags)
+    out = long_units.gpu(flags=flags, probes=(ref["probe_k"], ref["probe_v"]))
+    long_units.compare(out, ref)
