@@ -119,20 +119,18 @@ __global__ void k_select_rank(const float *d_k, const float *d_v, const int4 *me
   const int bany = max(b, bv_);
   const bool given = (flags & AKVS_F_GIVEN_PROBES) != 0;
   const bool unit_w = (flags & AKVS_F_UNIT_WEIGHTS) != 0;
-  // each thread keeps the ranks of up to 8 of its tokens in registers (n <= 8*blockDim)
-  for (int jb = 0; jb < n; jb += 8 * blockDim.x) {
-    int rk[8], rv[8];
-    float dk[8], dv[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int j = jb + u * blockDim.x + threadIdx.x;
-      rk[u] = rv[u] = 0;
-      dk[u] = (j < n && bany > 0) ? d_k[s0 + j] : 0.f;
-      dv[u] = (j < n && bany > 0) ? d_v[s0 + j] : 0.f;
-      // a NaN divergence ranks below every number (keeps exactly b probes per side)
-      if (dk[u] != dk[u]) dk[u] = -INFINITY;
-      if (dv[u] != dv[u]) dv[u] = -INFINITY;
-    }
+  // one token per thread and pass; its rank counts, per side, the tokens with a larger
+  // divergence or an equal one at a smaller position (two counters per side, even and odd
+  // t, so consecutive comparisons do not wait on each other)
+  for (int jb = 0; jb < n; jb += blockDim.x) {
+    const int j = jb + threadIdx.x;
+    const bool valid = j < n;
+    float dk = (valid && bany > 0) ? d_k[s0 + j] : 0.f;
+    float dv = (valid && bany > 0) ? d_v[s0 + j] : 0.f;
+    // a NaN divergence ranks below every number (keeps exactly b probes per side)
+    if (dk != dk) dk = -INFINITY;
+    if (dv != dv) dv = -INFINITY;
+    int rk0 = 0, rk1 = 0, rv0 = 0, rv1 = 0;
     if (!given && bany > 0) {
       for (int tb = 0; tb < n; tb += SEL_TILE) {
         __syncthreads();
@@ -143,35 +141,36 @@ __global__ void k_select_rank(const float *d_k, const float *d_v, const int4 *me
         }
         __syncthreads();
         const int tn = min(SEL_TILE, n - tb);
-        for (int t = 0; t < tn; ++t) {
-          const float a = sk[t], bv = sv[t];
-          const int tt = tb + t;
-#pragma unroll
-          for (int u = 0; u < 8; ++u) {
-            const int j = jb + u * blockDim.x + threadIdx.x;
-            rk[u] += (a > dk[u]) || (a == dk[u] && tt < j);
-            rv[u] += (bv > dv[u]) || (bv == dv[u] && tt < j);
-          }
+        const int jr = j - tb;  // position of token j relative to this tile
+        int t = 0;
+        for (; t + 2 <= tn; t += 2) {
+          const float a0 = sk[t], a1 = sk[t + 1], b0 = sv[t], b1 = sv[t + 1];
+          rk0 += (a0 > dk) || (a0 == dk && t < jr);
+          rk1 += (a1 > dk) || (a1 == dk && t + 1 < jr);
+          rv0 += (b0 > dv) || (b0 == dv && t < jr);
+          rv1 += (b1 > dv) || (b1 == dv && t + 1 < jr);
+        }
+        if (t < tn) {
+          const float a0 = sk[t], b0 = sv[t];
+          rk0 += (a0 > dk) || (a0 == dk && t < jr);
+          rv0 += (b0 > dv) || (b0 == dv && t < jr);
         }
       }
     }
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int j = jb + u * blockDim.x + threadIdx.x;
-      if (j >= n) continue;
-      uint8_t f;
-      if (given) {
-        f = 0;
-        for (int k = 0; k < b; ++k) f |= (probe_k[off + k] == s0 + j) ? 1 : 0;
-        for (int k = 0; k < bv_; ++k) f |= (probe_v[offv + k] == s0 + j) ? 2 : 0;
-      } else {
-        f = (uint8_t)((rk[u] < b ? 1 : 0) | (rv[u] < bv_ ? 2 : 0));
-      }
-      tok_flags[s0 + j] = f;
-      // w only multiplies the unit's offset, which is 0 when that side's b == 0
-      w_k[s0 + j] = b == 0 ? 0.f : (unit_w ? 1.f : fmaxf(fminf(dk[u], 1.f), 0.f));
-      w_v[s0 + j] = bv_ == 0 ? 0.f : (unit_w ? 1.f : fmaxf(fminf(dv[u], 1.f), 0.f));
+    if (!valid) continue;
+    const int rk = rk0 + rk1, rv = rv0 + rv1;
+    uint8_t f;
+    if (given) {
+      f = 0;
+      for (int k = 0; k < b; ++k) f |= (probe_k[off + k] == s0 + j) ? 1 : 0;
+      for (int k = 0; k < bv_; ++k) f |= (probe_v[offv + k] == s0 + j) ? 2 : 0;
+    } else {
+      f = (uint8_t)((rk < b ? 1 : 0) | (rv < bv_ ? 2 : 0));
     }
+    tok_flags[s0 + j] = f;
+    // w only multiplies the unit's offset, which is 0 when that side's b == 0
+    w_k[s0 + j] = b == 0 ? 0.f : (unit_w ? 1.f : fmaxf(fminf(dk, 1.f), 0.f));
+    w_v[s0 + j] = bv_ == 0 ? 0.f : (unit_w ? 1.f : fmaxf(fminf(dv, 1.f), 0.f));
   }
   __syncthreads();
   if (threadIdx.x >= 64) return;
