@@ -512,6 +512,27 @@ __global__ __launch_bounds__(512, 1) void k_gemm_bf16_w8(const bf16_t *__restric
   }
 }
 
+// Sum of n partial float4s p[0], p[stride], ... added in index order; eight loads are in
+// flight before their adds, so the pass costs about n / 8 memory round trips.
+__device__ __forceinline__ float4 sum_pieces(const float *p, size_t stride, int n) {
+  float4 acc = *reinterpret_cast<const float4 *>(p);
+  int k = 1;
+  for (; k + 8 <= n; k += 8) {
+    float4 v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = *reinterpret_cast<const float4 *>(p + (size_t)(k + u) * stride);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      acc.x += v[u].x; acc.y += v[u].y; acc.z += v[u].z; acc.w += v[u].w;
+    }
+  }
+  for (; k < n; ++k) {
+    const float4 v = *reinterpret_cast<const float4 *>(p + (size_t)k * stride);
+    acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+  }
+  return acc;
+}
+
 // Second pass of a K-split GEMM: a block takes G_FR rows of one tile, adds their partial
 // rows in split order into an LDS slice and runs the epilogue on it.
 constexpr int G_FR = 16;
@@ -539,12 +560,7 @@ __global__ __launch_bounds__(256) void k_gemm_fixup(int M, int N, int K, const i
   for (int i = 0; i < PER; ++i) {
     const int e4 = threadIdx.x + 256 * i;
     const int row = e4 / (GB_N / 4), c4 = (e4 - row * (GB_N / 4)) * 4;
-    const float *p = src + row * GB_N + c4;
-    float4 acc = *reinterpret_cast<const float4 *>(p);
-    for (int sp = 1; sp < splits; ++sp) {
-      const float4 v = *reinterpret_cast<const float4 *>(p + (size_t)sp * BM * GB_N);
-      acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
-    }
+    const float4 acc = sum_pieces(src + row * GB_N + c4, (size_t)BM * GB_N, splits);
     *reinterpret_cast<float4 *>(Cs + row * G_CLD + c4) = acc;
   }
   __syncthreads();

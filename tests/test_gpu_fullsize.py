@@ -110,7 +110,7 @@ def test_fullsize_probe_layer_gemms_sampled_rows(rows_kind):
     att = storage_round(synthetic.random_array((n, hq * hd), 7), torch.bfloat16)
     akvs.akvs_probe_out_mlp(h_dev, n, to_dev(att), m, lws, ws)
     torch.cuda.synchronize()
-    edges = [e for e in (95, 96, 127, 128, 191, 192, 255, 256, 1279, 1280, 4479, 4480) if e < n]
+    edges = [e for e in (95, 96, 127, 128, 191, 192, 255, 256, 1279, 1280, 4479, 4480, n - 1) if e < n]
     rows = np.union1d(sample_rows(n, 29, 4), edges)
     sw = oracle.split_layer(lw, dims)
     h64 = h.astype(np.float64)[rows]
