@@ -313,7 +313,7 @@ void carve_layer_bufs(Carver &cv, const akvs_model_cfg *m, long long rows,
   }
   if (g) b.gpart = cv.take<float>(g);
   if (worst > 0) {
-    b.part_o = cv.take<float>((size_t)worst * m->n_q_heads * m->head_dim);
+    b.part_o = cv.take<float>((size_t)worst * m->n_q_heads * m->head_dim / 2);  // bf16
     b.part_ml = cv.take<float>((size_t)worst * m->n_q_heads * 2);
     b.part_rows = worst;
   }
@@ -555,7 +555,7 @@ size_t carve_batch(void *ws, const akvs_model_cfg *m, const akvs_reuse_cfg *cfgs
       }
     }
     if (worst > 0) {
-      b.lb.part_o = cv.take<float>((size_t)worst * hqw);
+      b.lb.part_o = cv.take<float>((size_t)worst * hqw / 2);  // bf16 elements
       b.lb.part_ml = cv.take<float>((size_t)worst * m->n_q_heads * 2);
       b.lb.part_rows = worst;
     }
@@ -853,7 +853,7 @@ static size_t attention_part_floats(const akvs_model_cfg *m, long long rows, lon
   const long long sp = attn_splits((int)rows, m->n_q_heads, m->n_kv_heads, (int)n_keys);
   if (sp < 2) return 0;
   *ml_floats = (size_t)(sp * rows) * m->n_q_heads * 2;
-  return (size_t)(sp * rows) * m->n_q_heads * m->head_dim;
+  return (size_t)(sp * rows) * m->n_q_heads * m->head_dim / 2;  // bf16 outputs, two per float
 }
 
 size_t akvs_attention_workspace_size(const akvs_model_cfg *m, int32_t n_rows, int32_t n_keys) {
@@ -884,7 +884,7 @@ akvs_status akvs_sparse_query_attention(const void *q, const int32_t *positions,
       Carver cv(ws);
       part_o = cv.take<float>(o);
       part_ml = cv.take<float>(ml);
-      part_rows = (long long)(o / ((size_t)m->n_q_heads * m->head_dim));
+      part_rows = (long long)(ml / ((size_t)m->n_q_heads * 2));
     }
   }
   LAUNCH(AKVS_K_ATTENTION, launch_attention(q, positions, 0, n_rows, nullptr, k, v, n_keys,
@@ -1277,7 +1277,7 @@ static size_t carve_decode(void *ws, const akvs_model_cfg *m, long long n_keys, 
   const size_t o = attention_part_floats(m, 1, n_keys, &ml);
   b.part_o = o ? cv.take<float>(o) : nullptr;
   b.part_ml = o ? cv.take<float>(ml) : nullptr;
-  b.part_rows = o ? (long long)(o / ((size_t)m->n_q_heads * m->head_dim)) : 0;
+  b.part_rows = o ? (long long)(ml / ((size_t)m->n_q_heads * 2)) : 0;
   return cv.off;
 }
 

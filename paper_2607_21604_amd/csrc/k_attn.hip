@@ -64,7 +64,7 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
                                                    int nrb, int n_tiles, int n_splits,
                                                    int split_keys, float scale_log2,
                                                    bf16_t *__restrict__ out,
-                                                   float *__restrict__ part_o,
+                                                   bf16_t *__restrict__ part_o,
                                                    float *__restrict__ part_ml,
                                                    const int32_t *row_base) {
   constexpr int KS = HD / 16;          // contraction steps of S
@@ -279,14 +279,15 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
   const float l_row = l_run + __shfl_xor(l_run, 32, 64);
   if (!rvalid) return;
   // o[db][i] is dim db*32 + (i/4)*8 + hi*4 + i%4 of row r
-  if (n_splits > 1) {  // unnormalised partial + (max, sum) for the combine pass
-    float *po = part_o + prow * HD + hi * 4;
+  if (n_splits > 1) {  // this split's output over its own keys (bf16) + (max, sum)
+    const float pinv = l_row > 0.f ? 1.0f / l_row : 0.f;  // no visible key: m = -inf, skipped
+    bf16_t *po = part_o + prow * HD + hi * 4;
 #pragma unroll
     for (int db = 0; db < DB; ++db)
 #pragma unroll
       for (int q4 = 0; q4 < 4; ++q4)
-        store4(po + db * 32 + q4 * 8, o[db][4 * q4], o[db][4 * q4 + 1], o[db][4 * q4 + 2],
-               o[db][4 * q4 + 3]);
+        store4(po + db * 32 + q4 * 8, o[db][4 * q4] * pinv, o[db][4 * q4 + 1] * pinv,
+               o[db][4 * q4 + 2] * pinv, o[db][4 * q4 + 3] * pinv);
     if (hi == 0) {
       part_ml[2 * prow] = m_run;
       part_ml[2 * prow + 1] = l_row;
@@ -303,12 +304,19 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
              o[db][4 * q4 + 2] * inv, o[db][4 * q4 + 3] * inv);
 }
 
-// Merge of the key splits of one (row, head): weights 2^(m_s - max m), fixed split order.
-// A split whose keys all lie past the row (causal mask) holds m = -inf and no output: it
-// is skipped, never multiplied in (its part_o slot holds whatever the workspace held).
+// Merge of the key splits of one (row, head): split s holds its output over its own keys,
+// o_s (bf16, normalised by its own sum l_s), and (m_s, l_s); the result is
+// sum_s w_s o_s / sum_s w_s with w_s = 2^(m_s - max m) l_s, added in split order. A split
+// whose keys all lie past the row (causal mask) holds m = -inf and is skipped, never
+// multiplied in (its part_o slot holds whatever the workspace held).
 // Thread = 4 consecutive head dims of one (row, head); the (m, l) pairs and the partial
 // outputs of four splits are requested at a time.
-__global__ __launch_bounds__(256) void k_attn_combine(const float *__restrict__ part_o,
+__device__ __forceinline__ float4 load_bf4(const bf16_t *p) {
+  const uint2 w = *reinterpret_cast<const uint2 *>(p);
+  return make_float4(__uint_as_float(w.x << 16), __uint_as_float(w.x & 0xffff0000u),
+                     __uint_as_float(w.y << 16), __uint_as_float(w.y & 0xffff0000u));
+}
+__global__ __launch_bounds__(256) void k_attn_combine(const bf16_t *__restrict__ part_o,
                                                       const float *__restrict__ part_ml,
                                                       int n_splits, int rows,
                                                       const int32_t *rows_dev, int hq, int hd,
@@ -336,13 +344,13 @@ __global__ __launch_bounds__(256) void k_attn_combine(const float *__restrict__ 
     for (int u = 0; u < 4; ++u) {
       const size_t pi = (sp + u) * stride + item;
       ml[u] = *reinterpret_cast<const float2 *>(part_ml + 2 * pi);
-      o[u] = *reinterpret_cast<const float4 *>(part_o + pi * hd + e0);
+      o[u] = load_bf4(part_o + pi * hd + e0);
     }
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       if (ml[u].x == -INFINITY) continue;  // no visible key: its part_o was never written
-      const float w = exp2f(ml[u].x - moff);
-      l += w * ml[u].y;
+      const float w = exp2f(ml[u].x - moff) * ml[u].y;
+      l += w;
       a.x += w * o[u].x; a.y += w * o[u].y; a.z += w * o[u].z; a.w += w * o[u].w;
     }
   }
@@ -350,9 +358,9 @@ __global__ __launch_bounds__(256) void k_attn_combine(const float *__restrict__ 
     const size_t pi = sp * stride + item;
     const float2 ml = *reinterpret_cast<const float2 *>(part_ml + 2 * pi);
     if (ml.x == -INFINITY) continue;
-    const float4 o = *reinterpret_cast<const float4 *>(part_o + pi * hd + e0);
-    const float w = exp2f(ml.x - moff);
-    l += w * ml.y;
+    const float4 o = load_bf4(part_o + pi * hd + e0);
+    const float w = exp2f(ml.x - moff) * ml.y;
+    l += w;
     a.x += w * o.x; a.y += w * o.y; a.z += w * o.z; a.w += w * o.w;
   }
   const float inv = 1.0f / l;
@@ -463,17 +471,18 @@ hipError_t launch_attention(const void *q, const int32_t *pos, int pos0, int row
     if (hd == 128)
       hipLaunchKernelGGL(k_attn_bf16<128>, g, b, 0, s, Q, pos, pos0, rows, rows_dev, K, V, n_keys,
                          hq, hkv, a.gh, a.n_groups, a.nrb, n_tiles, n_splits, split_keys,
-                         scale_log2, O, part_o, part_ml, row_base);
+                         scale_log2, O, reinterpret_cast<bf16_t *>(part_o), part_ml, row_base);
     else
       hipLaunchKernelGGL(k_attn_bf16<64>, g, b, 0, s, Q, pos, pos0, rows, rows_dev, K, V, n_keys,
                          hq, hkv, a.gh, a.n_groups, a.nrb, n_tiles, n_splits, split_keys,
-                         scale_log2, O, part_o, part_ml, row_base);
+                         scale_log2, O, reinterpret_cast<bf16_t *>(part_o), part_ml, row_base);
     if (n_splits > 1) {
       hipError_t e = hipGetLastError();
       if (e != hipSuccess) return e;
       const long long threads = (long long)rows * hq * (hd / 4);
       hipLaunchKernelGGL(k_attn_combine, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, s,
-                         part_o, part_ml, n_splits, rows, rows_dev, hq, hd, O, row_base);
+                         reinterpret_cast<const bf16_t *>(part_o), part_ml, n_splits, rows,
+                         rows_dev, hq, hd, O, row_base);
     }
   } else {
     const float scale = 1.0f / sqrtf((float)hd);

@@ -106,7 +106,9 @@ int gemm_cu_count();
 
 // ---- k_attn.hip ---------------------------------------------------------------------
 // With part_o / part_ml (bf16 path), the key range is split for parallelism:
-// part_o [splits][rows][hq][hd] fp32, part_ml [splits][rows][hq][2] fp32, splits as below,
+// part_o [splits][rows][hq][hd] bf16 (each split's output over its own keys, normalised by
+// its own sum; the buffer is typed float and needs half as many floats as elements),
+// part_ml [splits][rows][hq][2] fp32 (max, sum), splits as below,
 // lowered so that splits x rows stays within part_rows (what the buffers hold).
 // row_base (device, may be null): rows start at row *row_base of q, pos and out.
 hipError_t launch_attention(const void *q, const int32_t *pos, int pos0, int rows,
