@@ -1356,8 +1356,11 @@ akvs_status akvs_decode_step(const int32_t *token, int32_t n_past, const void *e
   for (int l = 0; l < m->n_layers; ++l) {
     char *kl = reinterpret_cast<char *>(k_cache) + l * layer_bytes;
     char *vl = reinterpret_cast<char *>(v_cache) + l * layer_bytes;
-    LAUNCH(AKVS_K_NORM, launch_rmsnorm(b.h, D, 1, nullptr, nullptr, lw[l].attn_norm, m->dtype, D,
-                                       m->rms_eps, b.x, m->dtype, D, stream));
+    // RMSNorm is folded into the matrix-vector kernels that consume it when the row fits LDS
+    const bool fold = D <= GEMV_NORM_MAX;
+    if (!fold)
+      LAUNCH(AKVS_K_NORM, launch_rmsnorm(b.h, D, 1, nullptr, nullptr, lw[l].attn_norm, m->dtype,
+                                         D, m->rms_eps, b.x, m->dtype, D, stream));
     GemvEpi e = gemv_epi(GV_QKV);
     e.out_dtype = m->dtype;
     e.q_out = b.q;
@@ -1367,19 +1370,30 @@ akvs_status akvs_decode_step(const int32_t *token, int32_t n_past, const void *e
     e.kv_w = kvw;
     e.hd = hd;
     e.rope = reinterpret_cast<const float2 *>(b.rope);
-    LAUNCH(AKVS_K_GEMV, launch_gemv(b.x, m->dtype, lw[l].w_qkv, m->dtype, qkvw, D, e, stream));
+    if (fold) {
+      e.norm = lw[l].attn_norm;
+      e.eps = m->rms_eps;
+    }
+    LAUNCH(AKVS_K_GEMV, launch_gemv(fold ? (const void *)b.h : b.x, fold ? AKVS_F32 : m->dtype,
+                                    lw[l].w_qkv, m->dtype, qkvw, D, e, stream));
     LAUNCH(AKVS_K_ATTENTION, launch_attention(b.q, nullptr, n_past, 1, nullptr, kl, vl, n_past + 1,
                                               m->n_q_heads, hkv, hd, m->dtype, b.att, b.part_o,
                                               b.part_ml, b.part_rows, stream));
     GemvEpi r = gemv_epi(GV_RESID);
     r.out_f32 = b.h;
     LAUNCH(AKVS_K_GEMV, launch_gemv(b.att, m->dtype, lw[l].w_o, m->dtype, D, hqw, r, stream));
-    LAUNCH(AKVS_K_NORM, launch_rmsnorm(b.h, D, 1, nullptr, nullptr, lw[l].mlp_norm, m->dtype, D,
-                                       m->rms_eps, b.x, m->dtype, D, stream));
+    if (!fold)
+      LAUNCH(AKVS_K_NORM, launch_rmsnorm(b.h, D, 1, nullptr, nullptr, lw[l].mlp_norm, m->dtype,
+                                         D, m->rms_eps, b.x, m->dtype, D, stream));
     GemvEpi g = gemv_epi(GV_SWIGLU);
     g.out = b.act;
     g.out_dtype = m->dtype;
-    LAUNCH(AKVS_K_GEMV, launch_gemv(b.x, m->dtype, lw[l].w_gate_up, m->dtype, 2 * F, D, g, stream));
+    if (fold) {
+      g.norm = lw[l].mlp_norm;
+      g.eps = m->rms_eps;
+    }
+    LAUNCH(AKVS_K_GEMV, launch_gemv(fold ? (const void *)b.h : b.x, fold ? AKVS_F32 : m->dtype,
+                                    lw[l].w_gate_up, m->dtype, 2 * F, D, g, stream));
     LAUNCH(AKVS_K_GEMV, launch_gemv(b.act, m->dtype, lw[l].w_down, m->dtype, D, F, r, stream));
   }
   LAUNCH(AKVS_K_NORM, launch_rmsnorm(b.h, D, 1, nullptr, nullptr, final_norm, m->dtype, D,

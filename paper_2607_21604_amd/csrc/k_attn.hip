@@ -332,7 +332,17 @@ __global__ __launch_bounds__(256) void k_attn_combine(const bf16_t *__restrict__
   if (item >= (long long)R * hq) return;
   const size_t stride = (size_t)rows * hq;  // items per split
   float mx = -INFINITY;
-  for (int sp = 0; sp < n_splits; ++sp) mx = fmaxf(mx, part_ml[2 * (sp * stride + item)]);
+  {
+    int sp = 0;
+    for (; sp + 8 <= n_splits; sp += 8) {  // eight maxima in flight per round trip
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = part_ml[2 * ((sp + u) * stride + item)];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) mx = fmaxf(mx, v[u]);
+    }
+    for (; sp < n_splits; ++sp) mx = fmaxf(mx, part_ml[2 * (sp * stride + item)]);
+  }
   const float moff = mx == -INFINITY ? 0.f : mx;
   float l = 0.f;
   float4 a = make_float4(0.f, 0.f, 0.f, 0.f);

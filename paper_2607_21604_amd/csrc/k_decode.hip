@@ -15,6 +15,14 @@ namespace {
 
 __device__ __forceinline__ float silu_dec(float g) { return g / (1.0f + __expf(-g)); }
 
+// v rounded to the storage type T and widened back to fp32.
+template <typename T>
+__device__ __forceinline__ float load1_round(float v);
+template <>
+__device__ __forceinline__ float load1_round<float>(float v) { return v; }
+template <>
+__device__ __forceinline__ float load1_round<bf16_t>(float v) { return bf2f(f2bf(v)); }
+
 // s0 = W[r0] . x, s1 = W[r1] . x over K (a multiple of 8), summed over the wave.
 template <typename TW, typename TX>
 __device__ __forceinline__ void dot2(const TW *__restrict__ w0, const TW *__restrict__ w1,
@@ -73,12 +81,47 @@ __device__ __forceinline__ bool better(float v, int i, float bv, int bi) {
   return bi < 0 || v > bv || (v == bv && i < bi);
 }
 
-template <typename TW, typename TX>
+// RMSNorm of the fp32 row h [K] into LDS: the arithmetic and summation order of k_rmsnorm
+// (per-thread strided sums, fixed wave butterfly, waves added pairwise), so the normalised
+// row equals what that kernel writes, rounded to TW.
+template <typename TW>
+__device__ __forceinline__ void norm_row_lds(const float *__restrict__ h, const TW *gain, int K,
+                                             float eps, float *s_x) {
+  __shared__ float red[4];
+  float ss = 0.f;
+  for (int e = threadIdx.x * 8; e < K; e += 256 * 8) {
+    float v[8];
+    load8(h + e, v);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) ss = fmaf(v[k], v[k], ss);
+  }
+  ss = wave_sum(ss);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  const float tot = (red[0] + red[1]) + (red[2] + red[3]);
+  const float inv = 1.0f / sqrtf(tot / (float)K + eps);
+  for (int e = threadIdx.x * 8; e < K; e += 256 * 8) {
+    float v[8], g[8];
+    load8(h + e, v);
+    load8(gain + e, g);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) v[k] = load1_round<TW>(v[k] * inv * g[k]);
+    store8(s_x + e, v);
+  }
+  __syncthreads();
+}
+
+template <typename TW, typename TX, bool NORM>
 __global__ __launch_bounds__(256) void k_gemv(const TX *__restrict__ x,
                                               const TW *__restrict__ W, int N, int K,
                                               GemvEpi e) {
   __shared__ float s_val[4];
   __shared__ int s_idx[4];
+  extern __shared__ float s_x[];  // NORM: the normalised row [K]
+  if (NORM) {
+    norm_row_lds(reinterpret_cast<const float *>(x), reinterpret_cast<const TW *>(e.norm), K,
+                 e.eps, s_x);
+  }
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const long long item = (long long)blockIdx.x * 4 + wave;
   const long long n_items = (N + 1) / 2;
@@ -109,7 +152,13 @@ __global__ __launch_bounds__(256) void k_gemv(const TX *__restrict__ x,
     }
   }
   float s0 = 0.f, s1 = 0.f;
-  if (live) dot2(W + (size_t)r0 * K, W + (size_t)r1 * K, x, K, lane, s0, s1);
+  if (live) {
+    if (NORM)
+      dot2(W + (size_t)r0 * K, W + (size_t)r1 * K, static_cast<const float *>(s_x), K, lane, s0,
+           s1);
+    else
+      dot2(W + (size_t)r0 * K, W + (size_t)r1 * K, x, K, lane, s0, s1);
+  }
   if (e.mode == GV_LOGITS) {
     // both logits out, then the block's best (value, index) as a partial of the pick
     float bv = -INFINITY;
@@ -196,22 +245,34 @@ hipError_t launch_gemv(const void *x, int x_dtype, const void *W, int w_dtype, i
                        const GemvEpi &e, hipStream_t s) {
   if (N == 0) return hipSuccess;
   dim3 g((unsigned)gemv_blocks(N)), b(256);
+  if (e.norm) {  // x: the fp32 residual row, normalised in each block
+    if (x_dtype != AKVS_F32 || K > GEMV_NORM_MAX || K % 8) return hipErrorInvalidValue;
+    const size_t lds = (size_t)K * sizeof(float);
+    const float *h = reinterpret_cast<const float *>(x);
+    if (w_dtype == AKVS_BF16)
+      hipLaunchKernelGGL((k_gemv<bf16_t, float, true>), g, b, lds, s, h,
+                         reinterpret_cast<const bf16_t *>(W), N, K, e);
+    else
+      hipLaunchKernelGGL((k_gemv<float, float, true>), g, b, lds, s, h,
+                         reinterpret_cast<const float *>(W), N, K, e);
+    return hipGetLastError();
+  }
   if (w_dtype == AKVS_BF16) {
     const bf16_t *w = reinterpret_cast<const bf16_t *>(W);
     if (x_dtype == AKVS_BF16)
-      hipLaunchKernelGGL((k_gemv<bf16_t, bf16_t>), g, b, 0, s,
+      hipLaunchKernelGGL((k_gemv<bf16_t, bf16_t, false>), g, b, 0, s,
                          reinterpret_cast<const bf16_t *>(x), w, N, K, e);
     else
-      hipLaunchKernelGGL((k_gemv<bf16_t, float>), g, b, 0, s, reinterpret_cast<const float *>(x),
-                         w, N, K, e);
+      hipLaunchKernelGGL((k_gemv<bf16_t, float, false>), g, b, 0, s,
+                         reinterpret_cast<const float *>(x), w, N, K, e);
   } else {
     const float *w = reinterpret_cast<const float *>(W);
     if (x_dtype == AKVS_BF16)
-      hipLaunchKernelGGL((k_gemv<float, bf16_t>), g, b, 0, s,
+      hipLaunchKernelGGL((k_gemv<float, bf16_t, false>), g, b, 0, s,
                          reinterpret_cast<const bf16_t *>(x), w, N, K, e);
     else
-      hipLaunchKernelGGL((k_gemv<float, float>), g, b, 0, s, reinterpret_cast<const float *>(x),
-                         w, N, K, e);
+      hipLaunchKernelGGL((k_gemv<float, float, false>), g, b, 0, s,
+                         reinterpret_cast<const float *>(x), w, N, K, e);
   }
   return hipGetLastError();
 }

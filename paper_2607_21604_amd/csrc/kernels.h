@@ -141,8 +141,14 @@ struct GemvEpi {
   const float2 *rope;
   float *part_val;
   int32_t *part_idx;
+  // RMSNorm folded in front of the product: x is the fp32 residual row, each block forms
+  // x * rstd * norm (rounded to the weight dtype) in LDS first; norm is in the weight dtype
+  const void *norm;
+  float eps;
 };
 int gemv_blocks(int N);
+// Largest row width (elements) launch_gemv can normalise in LDS.
+constexpr int GEMV_NORM_MAX = 16384;
 hipError_t launch_gemv(const void *x, int x_dtype, const void *W, int w_dtype, int N, int K,
                        const GemvEpi &e, hipStream_t s);
 // *out = index of the best of n (value, index) partials; -1 if none is a number.
