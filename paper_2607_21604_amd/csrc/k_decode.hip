@@ -218,8 +218,21 @@ __global__ __launch_bounds__(256) void k_pick(const float *__restrict__ pv,
   __shared__ int s_idx[256];
   float bv = -INFINITY;
   int bi = -1;
-  for (int i = threadIdx.x; i < n; i += 256)
-    if (better(pv[i], pi[i], bv, bi)) { bv = pv[i]; bi = pi[i]; }
+  int i0 = threadIdx.x;
+  for (; i0 + 7 * 256 < n; i0 += 8 * 256) {  // eight partials in flight per round trip
+    float v[8];
+    int ix[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      v[u] = pv[i0 + u * 256];
+      ix[u] = pi[i0 + u * 256];
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (better(v[u], ix[u], bv, bi)) { bv = v[u]; bi = ix[u]; }
+  }
+  for (; i0 < n; i0 += 256)
+    if (better(pv[i0], pi[i0], bv, bi)) { bv = pv[i0]; bi = pi[i0]; }
   s_val[threadIdx.x] = bv;
   s_idx[threadIdx.x] = bi;
   __syncthreads();
