@@ -338,7 +338,9 @@ __global__ __launch_bounds__(256, 2) void k_gemm_bf16(const bf16_t *__restrict__
 // (scheduling groups), so every wait before an LDS store covers only loads issued a tile
 // earlier. The accumulators go through LDS half a tile of rows at a time for the shared
 // epilogues. Rows past the device-side M are skipped, operand rows past M / N are clamped
-// to valid rows (their results are discarded).
+// to valid rows (their results are discarded). The B row count (2N for SWIGLU) arrives as a
+// kernel argument: derived on the device from the epilogue mode, the compiler keeps it in a
+// vector register and wraps every B load in a loop over distinct descriptors.
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t gemm_rsrc(const void *p, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, (int)bytes,
                                            0x00020000);
@@ -359,7 +361,7 @@ struct Gemm8 {
 template <int BM, int BN, int WGM, int NST>
 __global__ __launch_bounds__(512, 1) void k_gemm_bf16_w8(const bf16_t *__restrict__ A, int lda,
                                                          const bf16_t *__restrict__ B, int ldb,
-                                                         int M, int N, int K,
+                                                         int M, int N, int K, int b_rows,
                                                          const int32_t *m_dev, Epi epi) {
   using S = Gemm8<BM, BN, WGM, NST>;
   __shared__ __attribute__((aligned(16))) unsigned char smem[S::SMEM];
@@ -376,8 +378,7 @@ __global__ __launch_bounds__(512, 1) void k_gemm_bf16_w8(const bf16_t *__restric
   const int m0 = (tile / n_tiles) * BM;
   const int n0 = (tile - (tile / n_tiles) * n_tiles) * bn_out;
   const __amdgpu_buffer_rsrc_t ra = gemm_rsrc(A, (uint32_t)((size_t)M_eff * lda * 2));
-  const __amdgpu_buffer_rsrc_t rb =
-      gemm_rsrc(B, (uint32_t)((size_t)(swiglu ? 2 * N : N) * ldb * 2));
+  const __amdgpu_buffer_rsrc_t rb = gemm_rsrc(B, (uint32_t)b_rows * (uint32_t)ldb * 2u);
 
   // chunk c of a thread: row (tid >> 3) + 64 c of the stacked [A tile; B tile], k columns
   // (tid & 7) * 8 ..+7; SWIGLU B tiles stack BN/2 gate rows over the matching up rows
@@ -508,6 +509,160 @@ __global__ __launch_bounds__(512, 1) void k_gemm_bf16_w8(const bf16_t *__restric
     }
     __syncthreads();
     epilogue_tile<S::HB, BN, 512>(Cs, S::CLD, m0 + h * S::HB, n0, M_eff, N, epi);
+    __syncthreads();
+  }
+}
+
+// ------------------------------------------------------------------------------------------
+// bf16 MFMA GEMM, 8 waves in two groups that take turns ("ping-pong"). Waves w and w + 4 of
+// a block run on the same SIMD, so group 0 (waves 0-3) and group 1 (waves 4-7) hold one wave
+// of every SIMD. Group g owns rows [g BM/2, (g+1) BM/2) of the BM x BN block tile, as four
+// waves side by side over BN, each (BM/2) x (BN/4) in 32x32 MFMA tiles. The two groups run
+// half a k-tile apart and alternate two phases, each closed by a block barrier:
+//   memory phase of k-tile t: read all of this wave's operand fragments of tile t from LDS
+//     into registers, store this thread's share of tile t+1 (loaded two phases earlier)
+//     into the other LDS buffer, and issue the global loads of its share of tile t+2;
+//   compute phase of k-tile t: only the MFMAs over the fragments already in registers.
+// So while one wave of a SIMD multiplies, the other feeds LDS and memory, and the MFMA pipe
+// is never left waiting on a wave's own loads. Group 1 starts one phase late and finishes
+// one phase late; both groups pass the same number of barriers. Buffer hazards: tile t+1 is
+// written into the buffer of tile t-1 only after both groups read tile t-1 (the barrier
+// before the writing phase follows the second group's reads, which complete before it).
+template <int BM, int BN>
+struct GemmPP {
+  static constexpr int HM = BM / 2, WM = HM, WN = BN / 4;
+  static constexpr int MI = WM / 32, NJ = WN / 32;
+  static constexpr int CH = (BM + BN) / 64;  // 16-byte chunks per thread per k-tile
+  static constexpr int ACH = BM / 64;
+  static constexpr int ATILE = BM * G_LDS, BUF = (BM + BN) * G_LDS;
+  static constexpr int CLD = BN + 4;
+  static constexpr int LOOP_BYTES = 2 * BUF * 2, C_BYTES = HM * CLD * 4;
+  static constexpr int SMEM = LOOP_BYTES > C_BYTES ? LOOP_BYTES : C_BYTES;
+  static_assert(BM % 64 == 0 && WM % 32 == 0 && WN % 32 == 0, "tile shape");
+};
+
+template <int BM, int BN>
+__global__ __launch_bounds__(512, 1) void k_gemm_bf16_pp(const bf16_t *__restrict__ A, int lda,
+                                                         const bf16_t *__restrict__ B, int ldb,
+                                                         int M, int N, int K, int b_rows,
+                                                         const int32_t *m_dev, Epi epi) {
+  using S = GemmPP<BM, BN>;
+  __shared__ __attribute__((aligned(16))) unsigned char smem[S::SMEM];
+  bf16_t *sm = reinterpret_cast<bf16_t *>(smem);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int grp = wave >> 2, wn = wave & 3;
+  int M_eff = M;
+  if (m_dev) M_eff = min(M, *m_dev);
+  const bool swiglu = epi.mode == EPI_SWIGLU;
+  const int bn_out = swiglu ? BN / 2 : BN;
+  const int n_tiles = (N + bn_out - 1) / bn_out;
+  const int tile = blockIdx.x;
+  if (tile >= ((M_eff + BM - 1) / BM) * n_tiles) return;
+  const int m0 = (tile / n_tiles) * BM;
+  const int n0 = (tile - (tile / n_tiles) * n_tiles) * bn_out;
+  const __amdgpu_buffer_rsrc_t ra = gemm_rsrc(A, (uint32_t)((size_t)M_eff * lda * 2));
+  const __amdgpu_buffer_rsrc_t rb = gemm_rsrc(B, (uint32_t)b_rows * (uint32_t)ldb * 2u);
+
+  // chunk c of a thread: row (tid >> 3) + 64 c of the stacked [A tile; B tile], k columns
+  // (tid & 7) * 8 ..+7 (the same map as the 8-wave kernel, SWIGLU stacking included)
+  int goff[S::CH], loff[S::CH];
+#pragma unroll
+  for (int c = 0; c < S::CH; ++c) {
+    const int r = (tid >> 3) + 64 * c, kc = (tid & 7) * 8;
+    if (c < S::ACH) {
+      goff[c] = (min(m0 + r, M_eff - 1) * lda + kc) * 2;
+    } else {
+      const int rb_ = r - BM;
+      int gn;
+      if (swiglu) {
+        const int oc = min(n0 + (rb_ & (BN / 2 - 1)), N - 1);
+        gn = rb_ < BN / 2 ? oc : N + oc;
+      } else {
+        gn = min(n0 + rb_, N - 1);
+      }
+      goff[c] = (gn * ldb + kc) * 2;
+    }
+    loff[c] = r * G_LDS + kc;
+  }
+  const int nk = K / GB_K;
+
+  f32x16_t acc[S::MI][S::NJ];
+#pragma unroll
+  for (int i = 0; i < S::MI; ++i)
+#pragma unroll
+    for (int j = 0; j < S::NJ; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+  u32x4_t rg[S::CH];
+  bf16x8_t fa[4][S::MI], fb[4][S::NJ];
+  const int fa_lane = (grp * S::HM + (lane & 31)) * G_LDS + (lane >> 5) * 8;
+  const int fb_lane = S::ATILE + (wn * S::WN + (lane & 31)) * G_LDS + (lane >> 5) * 8;
+
+  auto gload = [&](int kt) {
+    const int so = kt * GB_K * 2;
+#pragma unroll
+    for (int c = 0; c < S::CH; ++c)
+      rg[c] = __builtin_bit_cast(u32x4_t,
+                                 c < S::ACH ? __builtin_amdgcn_raw_buffer_load_b128(ra, goff[c], so, 0)
+                                            : __builtin_amdgcn_raw_buffer_load_b128(rb, goff[c], so, 0));
+  };
+  auto lstore = [&](int boff) {
+#pragma unroll
+    for (int c = 0; c < S::CH; ++c) *reinterpret_cast<u32x4_t *>(sm + boff + loff[c]) = rg[c];
+  };
+  auto fread = [&](int boff) {
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+#pragma unroll
+      for (int i = 0; i < S::MI; ++i)
+        fa[ks][i] = *reinterpret_cast<const bf16x8_t *>(sm + boff + fa_lane + i * 32 * G_LDS + ks * 16);
+#pragma unroll
+      for (int j = 0; j < S::NJ; ++j)
+        fb[ks][j] = *reinterpret_cast<const bf16x8_t *>(sm + boff + fb_lane + j * 32 * G_LDS + ks * 16);
+    }
+  };
+
+  gload(0);
+  lstore(0);
+  if (nk > 1) gload(1);
+  __syncthreads();
+  if (grp == 1) __syncthreads();  // group 1 starts one phase late
+  for (int t = 0; t < nk; ++t) {
+    const int cur = (t & 1) * S::BUF, nxt = S::BUF - cur;
+    fread(cur);
+    if (t + 1 < nk) lstore(nxt);
+    if (t + 2 < nk) gload(t + 2);
+    __syncthreads();
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+      for (int i = 0; i < S::MI; ++i)
+#pragma unroll
+        for (int j = 0; j < S::NJ; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[ks][i], fb[ks][j], acc[i][j], 0, 0, 0);
+    if (grp == 0 || t + 1 < nk) __syncthreads();  // group 1 skips its last one
+  }
+  __syncthreads();
+
+  // epilogue: half h of the tile's rows is group h's
+  float *Cs = reinterpret_cast<float *>(smem);
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    if (m0 + h * S::HM >= M_eff) break;  // block-uniform
+    if (grp == h) {
+#pragma unroll
+      for (int i = 0; i < S::MI; ++i)
+#pragma unroll
+        for (int j = 0; j < S::NJ; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int row = i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+            const int col = wn * S::WN + j * 32 + (lane & 31);
+            Cs[row * S::CLD + col] = acc[i][j][r];
+          }
+    }
+    __syncthreads();
+    epilogue_tile<S::HM, BN, 512>(Cs, S::CLD, m0 + h * S::HM, n0, M_eff, N, epi);
     __syncthreads();
   }
 }
@@ -698,15 +853,21 @@ static GemmPlan gemm_plan(int M, int N, int K, const int32_t *m_dev, const Epi &
   return p;
 }
 
-// Block tiles of the 8-wave kernel with their main-loop rate per CU relative to 256x256
-// (measured at the 3B projection shapes). A launch takes the tile with the least
-// (rounds of one tile per CU) x (tile area) / rate, at the expected row count.
+// Block tiles of the 8-wave kernels with their rate per CU relative to the 256x256 tile,
+// measured on the 3B projection shapes with every CU busy (M = 1405 and 4516 rows). A launch
+// takes the tile with the least (rounds of one tile per CU) x (tile area) / rate at the
+// expected row count. The ping-pong kernel needs long compute phases: only its 192x256 tile
+// was kept (with 128 columns per tile a phase holds 12 MFMAs and the shared schedule is
+// faster; at 192x256 the shared schedule measured 0.75 against the ping-pong's 0.88).
 struct W8Tile {
   int bm, bn;
+  bool pp;
   double rate;
 };
-static const W8Tile kW8Tiles[] = {{256, 256, 1.0}, {192, 256, 0.99}, {256, 128, 0.92},
-                                  {192, 128, 0.88}};
+static const W8Tile kW8Tiles[] = {{256, 256, false, 1.0},
+                                  {192, 256, true, 0.88},
+                                  {256, 128, false, 0.78},
+                                  {192, 128, false, 0.74}};
 constexpr int kW8Count = sizeof(kW8Tiles) / sizeof(kW8Tiles[0]);
 
 static int gemm_w8_tile(int M_est, int N, int mode) {
@@ -734,7 +895,19 @@ static void launch_w8(const void *A, int lda, const void *B, int ldb, int M, int
   const int grid = ((M + BM - 1) / BM) * ((N + bn_out - 1) / bn_out);
   hipLaunchKernelGGL((k_gemm_bf16_w8<BM, BN, WGM, NST>), dim3(grid), dim3(512), 0, s,
                      reinterpret_cast<const bf16_t *>(A), lda,
-                     reinterpret_cast<const bf16_t *>(B), ldb, M, N, K, m_dev, epi);
+                     reinterpret_cast<const bf16_t *>(B), ldb, M, N, K,
+                     epi.mode == EPI_SWIGLU ? 2 * N : N, m_dev, epi);
+}
+
+template <int BM, int BN>
+static void launch_pp(const void *A, int lda, const void *B, int ldb, int M, int N, int K,
+                      const int32_t *m_dev, const Epi &epi, hipStream_t s) {
+  const int bn_out = epi.mode == EPI_SWIGLU ? BN / 2 : BN;
+  const int grid = ((M + BM - 1) / BM) * ((N + bn_out - 1) / bn_out);
+  hipLaunchKernelGGL((k_gemm_bf16_pp<BM, BN>), dim3(grid), dim3(512), 0, s,
+                     reinterpret_cast<const bf16_t *>(A), lda,
+                     reinterpret_cast<const bf16_t *>(B), ldb, M, N, K,
+                     epi.mode == EPI_SWIGLU ? 2 * N : N, m_dev, epi);
 }
 
 hipError_t launch_gemm(const void *A, int lda, const void *B, int ldb, int M, int N, int K,
@@ -750,7 +923,7 @@ hipError_t launch_gemm(const void *A, int lda, const void *B, int ldb, int M, in
       const int M_est = m_dev ? (std::max(m_min, 1) + M) / 2 : M;
       switch (gemm_w8_tile(M_est, N, epi.mode)) {
         case 0: launch_w8<256, 256, 2, 1>(A, lda, B, ldb, M, N, K, m_dev, epi, s); break;
-        case 1: launch_w8<192, 256, 2, 1>(A, lda, B, ldb, M, N, K, m_dev, epi, s); break;
+        case 1: launch_pp<192, 256>(A, lda, B, ldb, M, N, K, m_dev, epi, s); break;
         case 2: launch_w8<256, 128, 4, 2>(A, lda, B, ldb, M, N, K, m_dev, epi, s); break;
         default: launch_w8<192, 128, 2, 2>(A, lda, B, ldb, M, N, K, m_dev, epi, s); break;
       }
