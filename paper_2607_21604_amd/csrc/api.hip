@@ -1257,7 +1257,15 @@ struct DecodeBufs {
   int32_t *part_idx;
   void *x, *q, *att, *act;
   long long part_rows;
+  bool one_row_attn;  // partials of the one-row attention kernel, else of the general one
 };
+
+// The one-row attention kernel covers bf16 models with hd 64 / 128 and <= 8 query heads per
+// KV head; others use the general attention with one row.
+static bool decode_one_row_attn(const akvs_model_cfg *m) {
+  const int G = m->n_q_heads / m->n_kv_heads;
+  return m->dtype == AKVS_BF16 && G >= 1 && G <= 8 && (m->head_dim == 64 || m->head_dim == 128);
+}
 
 static size_t carve_decode(void *ws, const akvs_model_cfg *m, long long n_keys, DecodeBufs &b) {
   Carver cv(ws);
@@ -1273,6 +1281,15 @@ static size_t carve_decode(void *ws, const akvs_model_cfg *m, long long n_keys, 
   b.q = cv.take<char>((size_t)hqw * es);
   b.att = cv.take<char>((size_t)hqw * es);
   b.act = cv.take<char>((size_t)F * es);
+  b.one_row_attn = decode_one_row_attn(m);
+  if (b.one_row_attn) {
+    int chunk;
+    const size_t nc = (size_t)decode_attn_chunks((int)n_keys, m->n_kv_heads, &chunk);
+    b.part_o = cv.take<float>(nc * m->n_q_heads * m->head_dim);
+    b.part_ml = cv.take<float>(nc * m->n_q_heads * 2);
+    b.part_rows = 0;
+    return cv.off;
+  }
   size_t ml;
   const size_t o = attention_part_floats(m, 1, n_keys, &ml);
   b.part_o = o ? cv.take<float>(o) : nullptr;
@@ -1376,9 +1393,13 @@ akvs_status akvs_decode_step(const int32_t *token, int32_t n_past, const void *e
     }
     LAUNCH(AKVS_K_GEMV, launch_gemv(fold ? (const void *)b.h : b.x, fold ? AKVS_F32 : m->dtype,
                                     lw[l].w_qkv, m->dtype, qkvw, D, e, stream));
-    LAUNCH(AKVS_K_ATTENTION, launch_attention(b.q, nullptr, n_past, 1, nullptr, kl, vl, n_past + 1,
-                                              m->n_q_heads, hkv, hd, m->dtype, b.att, b.part_o,
-                                              b.part_ml, b.part_rows, stream));
+    if (b.one_row_attn)
+      LAUNCH(AKVS_K_ATTENTION, launch_attention_decode(b.q, kl, vl, n_past + 1, m->n_q_heads, hkv,
+                                                       hd, b.att, b.part_o, b.part_ml, stream));
+    else
+      LAUNCH(AKVS_K_ATTENTION, launch_attention(b.q, nullptr, n_past, 1, nullptr, kl, vl,
+                                                n_past + 1, m->n_q_heads, hkv, hd, m->dtype,
+                                                b.att, b.part_o, b.part_ml, b.part_rows, stream));
     GemvEpi r = gemv_epi(GV_RESID);
     r.out_f32 = b.h;
     LAUNCH(AKVS_K_GEMV, launch_gemv(b.att, m->dtype, lw[l].w_o, m->dtype, D, hqw, r, stream));

@@ -152,6 +152,13 @@ constexpr int GEMV_NORM_MAX = 16384;
 hipError_t launch_gemv(const void *x, int x_dtype, const void *W, int w_dtype, int N, int K,
                        const GemvEpi &e, hipStream_t s);
 // *out = index of the best of n (value, index) partials; -1 if none is a number.
+// Attention of one new row (bf16, hd 64 or 128, hq / hkv <= 8) over n_keys cached keys:
+// per (KV head, key chunk) partials part_o [n_chunks][hq][hd] and part_ml [n_chunks][hq][2]
+// (fp32), merged into out [hq][hd] by a second kernel.
+int decode_attn_chunks(int n_keys, int hkv, int *chunk_keys);
+hipError_t launch_attention_decode(const void *q, const void *k, const void *v, int n_keys,
+                                   int hq, int hkv, int hd, void *out, float *part_o,
+                                   float *part_ml, hipStream_t s);
 hipError_t launch_pick(const float *part_val, const int32_t *part_idx, int n, int32_t *out,
                        hipStream_t s);
 

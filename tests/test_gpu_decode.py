@@ -102,3 +102,34 @@ def test_decode_workspace_and_bounds():
     kc = torch.zeros((shape.n_layers, 8, shape.n_kv_heads, shape.head_dim), device=DEV)
     with pytest.raises(akvs.AkvsError):
         eng.decode_step(to_dev(np.array([1], np.int32)), 8, kc, kc.clone())  # no room for row 8
+
+
+@pytest.mark.parametrize("n_q,n_kv,hd,n", [
+    (24, 8, 128, 0), (24, 8, 128, 16), (24, 8, 128, 4516), (28, 4, 128, 1000),
+    (40, 8, 128, 16128), (8, 1, 64, 300), (4, 4, 64, 129)])
+def test_decode_step_one_row_attention_shapes(n_q, n_kv, hd, n):
+    """One decode step of a one-layer bf16 model over random caches of n positions, at the
+    query / KV head ratios of the 3B, 7B and 32B shapes and at head dim 64: the one-row
+    attention kernel from a single key chunk up to 127 chunks of 128 keys. Keys are scaled
+    so that the softmax is far from uniform. Logits and the new K/V row against the oracle
+    run on the same cache values."""
+    shape = synthetic.ModelShape("dec", 1, 512, n_q, n_kv, hd, 1024, 2048, 1.0e6)
+    w = synthetic.make_weights(shape, seed=7)
+    eng = Engine(shape, dev_weights(w))
+    dims = oracle.dims_from(shape)
+    layers = [oracle.split_layer(lw, dims) for lw in w["layers"]]
+    rng = np.random.default_rng(n + n_q)
+    k = torch.from_numpy(rng.standard_normal((1, n, n_kv, hd)).astype(np.float32) * 30).bfloat16()
+    v = torch.from_numpy(rng.standard_normal((1, n, n_kv, hd)).astype(np.float32)).bfloat16()
+    kc = torch.zeros((1, n + 1, n_kv, hd), dtype=torch.bfloat16, device=DEV)
+    vc = torch.zeros_like(kc)
+    kc[:, :n].copy_(k.to(DEV))
+    vc[:, :n].copy_(v.to(DEV))
+    t = 77
+    lg, nt = eng.decode_step(to_dev(np.array([t], np.int32)), n, kc, vc)
+    torch.cuda.synchronize()
+    _, r_lg, kn, vn = oracle.decode_step(t, f64(k), f64(v), w, dims, layers)
+    assert max_rel(f64(kc[:, n]), kn) < 2e-2
+    assert max_rel(f64(vc[:, n]), vn) < 2e-2
+    assert max_rel(f64(lg), r_lg) < 2e-2
+    check_pick(nt[0], lg)
