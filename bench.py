@@ -51,6 +51,8 @@ def parse():
     p.add_argument("--no-graph", action="store_true", help="skip the graph-replay leg")
     p.add_argument("--random-caches", action="store_true",
                    help="unit caches drawn at random instead of prefilled (counter runs)")
+    p.add_argument("--calibrate-mfma", action="store_true",
+                   help="run the library's MFMA-only loop first (reference for MFMA-busy counters)")
     p.add_argument("--calibrate-copy", action="store_true",
                    help="run one 1 GiB read + 1 GiB write kernel first (FETCH/WRITE counter calibration)")
     p.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -258,6 +260,21 @@ def main():
     print(f"# workload {wl.name}: T={wl.n_tokens} ({len(wl.chunk_lens)} units, q={wl.query_len}), "
           f"L={shape.n_layers}, r={num}/{den}", file=sys.stderr, flush=True)
 
+    if args.calibrate_mfma:
+        # two blocks of four waves per CU (two waves per SIMD), MFMAs only
+        n_blocks = 2 * torch.cuda.get_device_properties(dev).multi_processor_count
+        iters = 4000
+        buf = torch.empty(n_blocks * 256, dtype=torch.float32, device=dev)
+        akvs.akvs_mfma_busy_loop(n_blocks, 16, buf)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        akvs.akvs_mfma_busy_loop(n_blocks, iters, buf)
+        torch.cuda.synchronize()
+        dt = time.perf_counter() - t0
+        tf = n_blocks * 4 * iters * 8 * 32768.0 / dt * 1e-12
+        print(f"# MFMA-only loop: {dt * 1e3:.3f} ms, {tf:.0f} TFLOP/s (wall clock, one launch)",
+              file=sys.stderr, flush=True)
+        del buf
     if args.calibrate_copy:
         # an elementwise kernel that reads and writes COPY_BYTES once each (a same-dtype
         # copy_ may go to the DMA engines and show no kernel dispatch)

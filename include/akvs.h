@@ -351,6 +351,15 @@ enum {
 akvs_status akvs_profile_enable(int32_t class_mask);
 akvs_status akvs_profile_read(int32_t kernel_class, int64_t *launches, double *total_ms);
 
+/* ---- counter calibration ----------------------------------------------------------------
+ * akvs_mfma_busy_loop: not part of the method; the reference point for hardware counters
+ * of matrix-core use. Launches n_blocks blocks of 256 threads in which every wave issues
+ * iters x 8 independent 32x32x16 bf16 MFMAs and nothing else (the matrix cores of every
+ * SIMD it occupies stay busy), then writes one fp32 per thread to out (device
+ * [n_blocks * 256], caller-owned, 16-byte aligned). Asynchronous on stream. Errors:
+ * EINVAL for negative sizes, a null or misaligned out (with n_blocks > 0); EHIP. */
+akvs_status akvs_mfma_busy_loop(int32_t n_blocks, int32_t iters, float *out, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -116,6 +116,7 @@ _SIGS = {
                               _P, _P, _I, _P, _P, _P, ctypes.c_size_t, _P]),
     "akvs_profile_enable": (_I, [_I]),
     "akvs_profile_read": (_I, [_I, ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_double)]),
+    "akvs_mfma_busy_loop": (_I, [_I, _I, _P, _P]),
 }
 EXPORTED = tuple(_SIGS)
 
@@ -369,6 +370,12 @@ def akvs_decode_step(token, n_past, embed, layers: ctypes.Array, final_norm, w_o
 def akvs_profile_enable(class_mask: int):
     """Bit (1 << class) enables event timing of that kernel class; 0 disables."""
     _check(load().akvs_profile_enable(int(class_mask)), "akvs_profile_enable")
+
+
+def akvs_mfma_busy_loop(n_blocks: int, iters: int, out, stream=None):
+    """Counter reference: n_blocks x 256 threads of independent bf16 MFMAs; out fp32 [n_blocks*256]."""
+    _check(load().akvs_mfma_busy_loop(int(n_blocks), int(iters), ptr(out), stream_handle(stream)),
+           "akvs_mfma_busy_loop")
 
 
 def akvs_profile_read(kernel_class: int):

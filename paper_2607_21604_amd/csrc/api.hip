@@ -683,6 +683,14 @@ akvs_status akvs_profile_read(int32_t cls, int64_t *launches, double *total_ms) 
   return AKVS_OK;
 }
 
+akvs_status akvs_mfma_busy_loop(int32_t n_blocks, int32_t iters, float *out, hipStream_t stream) {
+  REQUIRE(n_blocks >= 0 && iters >= 0, AKVS_EINVAL, "n_blocks and iters must be >= 0");
+  REQUIRE(n_blocks == 0 || out, AKVS_EINVAL, "NULL argument");
+  REQUIRE(aligned16(out), AKVS_EINVAL, "misaligned argument");
+  LAUNCH(AKVS_K_OTHER, launch_mfma_busy_loop(n_blocks, iters, out, stream));
+  return AKVS_OK;
+}
+
 // ---- step entries ---------------------------------------------------------------------------
 
 akvs_status akvs_rope_table(int32_t n_pos, int32_t head_dim, float rope_theta, float *table,

@@ -225,4 +225,36 @@ hipError_t launch_token_setup(const int32_t *meta, int n_chunks, int32_t *tok_de
   return hipGetLastError();
 }
 
+// ---- measurement helper --------------------------------------------------------------
+// A loop of independent v_mfma_f32_32x32x16_bf16 (8 accumulators per wave, no other work)
+// that keeps the matrix cores busy: the reference for the MFMA-busy counters.
+__global__ __launch_bounds__(256) void k_mfma_busy_loop(float *out, int iters) {
+  bf16x8_t a, b;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    a[j] = (__bf16)(0.001f * (float)(threadIdx.x + j));
+    b[j] = (__bf16)(0.002f * (float)j);
+  }
+  f32x16_t acc[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[i][r] = 0.f;
+  for (int it = 0; it < iters; ++it)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[i], 0, 0, 0);
+  float sum = 0.f;
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) sum += acc[i][r];
+  out[(size_t)blockIdx.x * 256 + threadIdx.x] = sum;
+}
+
+hipError_t launch_mfma_busy_loop(int n_blocks, int iters, float *out, hipStream_t s) {
+  if (n_blocks <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_mfma_busy_loop, dim3(n_blocks), dim3(256), 0, s, out, iters);
+  return hipGetLastError();
+}
+
 }  // namespace akvs

@@ -67,6 +67,10 @@ hipError_t launch_correction(CacheLayer cache, const float *mu_k, const float *m
 hipError_t launch_quantize(const void *x, int x_dtype, int n_rows, int hd, int bits,
                            uint8_t *codes, _Float16 *meta, hipStream_t s);
 
+// Measurement helper: n_blocks x 256 threads of independent bf16 MFMAs (iters x 8 per
+// wave); out [n_blocks * 256] fp32 receives each thread's accumulator sum.
+hipError_t launch_mfma_busy_loop(int n_blocks, int iters, float *out, hipStream_t s);
+
 // ---- k_gemm.hip ---------------------------------------------------------------------
 enum EpiMode { EPI_STORE = 0, EPI_QKV = 1, EPI_RESID = 2, EPI_SWIGLU = 3 };
 

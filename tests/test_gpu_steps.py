@@ -453,3 +453,16 @@ def test_quantize_cache_bit_exact(bits):
     akvs.akvs_quantize_cache(to_dev(x), 300, 128, bits, c, mt)
     np.testing.assert_array_equal(c.cpu().numpy(), oracle.pack_codes(codes, bits))
     np.testing.assert_array_equal(mt.cpu().numpy().view(np.uint16), meta.view(np.uint16))
+
+
+def test_mfma_busy_loop_runs_and_rejects_bad_arguments():
+    """The counter-calibration loop: every thread's sum is finite and the same for every
+    block (the inputs depend on the thread index only); negative sizes are rejected."""
+    out = torch.full((3 * 256,), float("nan"), dtype=torch.float32, device=DEV)
+    akvs.akvs_mfma_busy_loop(3, 5, out)
+    torch.cuda.synchronize()
+    o = out.view(3, 256).cpu()
+    assert torch.isfinite(o).all()
+    assert torch.equal(o[0], o[1]) and torch.equal(o[0], o[2])
+    with pytest.raises(akvs.AkvsError):
+        akvs.akvs_mfma_busy_loop(-1, 5, out)
