@@ -309,8 +309,8 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
 // sum_s w_s o_s / sum_s w_s with w_s = 2^(m_s - max m) l_s, added in split order. A split
 // whose keys all lie past the row (causal mask) holds m = -inf and is skipped, never
 // multiplied in (its part_o slot holds whatever the workspace held).
-// Thread = 4 consecutive head dims of one (row, head); the (m, l) pairs and the partial
-// outputs of four splits are requested at a time.
+// Thread = 4 consecutive head dims of one (row, head). Up to 8 splits, all (m, l) pairs and
+// partial outputs are requested at once; with more, four splits at a time.
 __device__ __forceinline__ float4 load_bf4(const bf16_t *p) {
   const uint2 w = *reinterpret_cast<const uint2 *>(p);
   return make_float4(__uint_as_float(w.x << 16), __uint_as_float(w.x & 0xffff0000u),
@@ -323,14 +323,50 @@ __global__ __launch_bounds__(256) void k_attn_combine(const bf16_t *__restrict__
                                                       bf16_t *__restrict__ out,
                                                       const int32_t *row_base) {
   const int per = hd >> 2;  // threads per (row, head)
-  if (row_base) out += (size_t)*row_base * hq * hd;
   const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
   const long long item = gid / per;
   const int e0 = (int)(gid - item * per) * 4;
+  if (item >= (long long)rows * hq) return;
+  const size_t stride = (size_t)rows * hq;  // items per split
+  if (n_splits <= 8) {
+    // every partial of this item requested at once, before the live row count arrives
+    // (slots of rows past it are in the buffer and never used)
+    float2 ml[8];
+    float4 o[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      if (u < n_splits) {
+        const size_t pi = u * stride + item;
+        ml[u] = *reinterpret_cast<const float2 *>(part_ml + 2 * pi);
+        o[u] = load_bf4(part_o + pi * hd + e0);
+      }
+    }
+    int R = rows;
+    if (rows_dev) R = min(R, *rows_dev);
+    if (item >= (long long)R * hq) return;
+    if (row_base) out += (size_t)*row_base * hq * hd;
+    float mx = -INFINITY;
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (u < n_splits) mx = fmaxf(mx, ml[u].x);
+    const float moff = mx == -INFINITY ? 0.f : mx;
+    float l = 0.f;
+    float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      if (u >= n_splits || ml[u].x == -INFINITY) continue;
+      const float w = exp2f(ml[u].x - moff) * ml[u].y;
+      l += w;
+      a.x += w * o[u].x; a.y += w * o[u].y; a.z += w * o[u].z; a.w += w * o[u].w;
+    }
+    const float inv = 1.0f / l;
+    store4(out + item * hd + e0, a.x * inv, a.y * inv, a.z * inv, a.w * inv);
+    return;
+  }
   int R = rows;
   if (rows_dev) R = min(R, *rows_dev);
   if (item >= (long long)R * hq) return;
-  const size_t stride = (size_t)rows * hq;  // items per split
+  if (row_base) out += (size_t)*row_base * hq * hd;
   float mx = -INFINITY;
   {
     int sp = 0;

@@ -58,6 +58,9 @@ hipError_t launch_embed(const int32_t *tok, int n, const void *embed, int dtype,
 }
 
 // One block (256 threads) per row; D % 8 == 0. Sum of squares with a fixed reduction tree.
+// Rows of up to RMS_REG * 2048 elements are read once into registers (row and gain loads
+// all in flight before the sum); longer rows take a second pass over the row.
+constexpr int RMS_REG = 4;
 template <typename TG, typename TO>
 __global__ void k_rmsnorm(const float *h, int ldh, int rows, const int32_t *rows_dev,
                           const int32_t *base_dev, const TG *gain, int D, float eps, TO *out,
@@ -72,6 +75,42 @@ __global__ void k_rmsnorm(const float *h, int ldh, int rows, const int32_t *rows
     if (src < 0) return;
   }
   const float *x = h + (size_t)src * ldh;
+  __shared__ float red[4];
+  TO *y = out + (size_t)i * ldo;
+  if (D <= RMS_REG * 256 * 8) {  // one read of the row, kept in registers
+    float v[RMS_REG][8], g[RMS_REG][8];
+    float ss = 0.f;
+#pragma unroll
+    for (int c = 0; c < RMS_REG; ++c) {
+      const int e = threadIdx.x * 8 + c * 256 * 8;
+      if (e < D) {
+        load8(x + e, v[c]);
+        load8(gain + e, g[c]);
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < RMS_REG; ++c) {
+      if (threadIdx.x * 8 + c * 256 * 8 < D) {
+#pragma unroll
+        for (int k = 0; k < 8; ++k) ss = fmaf(v[c][k], v[c][k], ss);
+      }
+    }
+    ss = wave_sum(ss);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+    __syncthreads();
+    const float tot = (red[0] + red[1]) + (red[2] + red[3]);
+    const float inv = 1.0f / sqrtf(tot / (float)D + eps);
+#pragma unroll
+    for (int c = 0; c < RMS_REG; ++c) {
+      const int e = threadIdx.x * 8 + c * 256 * 8;
+      if (e < D) {
+#pragma unroll
+        for (int k = 0; k < 8; ++k) v[c][k] = v[c][k] * inv * g[c][k];
+        store8(y + e, v[c]);
+      }
+    }
+    return;
+  }
   float ss = 0.f;
   for (int e = threadIdx.x * 8; e < D; e += 256 * 8) {
     float v[8];
@@ -79,13 +118,11 @@ __global__ void k_rmsnorm(const float *h, int ldh, int rows, const int32_t *rows
 #pragma unroll
     for (int k = 0; k < 8; ++k) ss = fmaf(v[k], v[k], ss);
   }
-  __shared__ float red[4];
   ss = wave_sum(ss);
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
   __syncthreads();
   const float tot = (red[0] + red[1]) + (red[2] + red[3]);
   const float inv = 1.0f / sqrtf(tot / (float)D + eps);
-  TO *y = out + (size_t)i * ldo;
   for (int e = threadIdx.x * 8; e < D; e += 256 * 8) {
     float v[8], g[8];
     load8(x + e, v);

@@ -422,14 +422,13 @@ __device__ __forceinline__ CorrTok corr_token(int t, int t_ctx, const uint8_t *t
   return c;
 }
 
-// One side (K: rotated) of one position: the 8 lo/hi pairs e0.. of head h.
+// The rest of one side once its cache values (of a unit token) are in lo / hi: fresh rows
+// replace them, reused rows get the re-rotation and the weighted offset.
 template <typename TS>
-__device__ __forceinline__ void corr_side(bool fresh, int fr, const TS *__restrict__ fresh_buf,
-                                          const void *cb, const _Float16 *cm, int dtype,
-                                          size_t orow, int hkv, int h, int hd, int e0,
-                                          const float2 *rrow, const float *mu, float w,
-                                          float (&lo)[8], float (&hi)[8],
-                                          const float2 *mu_rot = nullptr) {
+__device__ __forceinline__ void corr_finish(bool fresh, int fr, const TS *__restrict__ fresh_buf,
+                                            int hkv, int h, int hd, int e0, const float2 *rrow,
+                                            const float *mu, float w, float (&lo)[8],
+                                            float (&hi)[8], const float2 *mu_rot = nullptr) {
   const int half = hd >> 1;
   if (fresh) {
     if (fr >= 0) {
@@ -442,8 +441,6 @@ __device__ __forceinline__ void corr_side(bool fresh, int fr, const TS *__restri
     }
     return;
   }
-  cache_load8(cb, cm, dtype, orow, hd, e0, lo);
-  cache_load8(cb, cm, dtype, orow, hd, e0 + half, hi);
   if (rrow) rotate8(rrow, e0, lo, hi);
   if (mu) {
     float ml[8], mh[8];
@@ -490,18 +487,25 @@ __global__ __launch_bounds__(256) void k_correction(CacheLayer cache, const floa
 #pragma unroll
   for (int i = 0; i < CORR_T; ++i) {
     const int t = min(t0 + i, t_all - 1);  // a repeated last position is computed twice
+    const size_t orow = (size_t)t * hkv + h;
+    // the cache rows of a unit token are requested before its flags are known, so they
+    // arrive with the bookkeeping (wasted for the recomputed tokens, whose rows are fresh)
+    if (t < t_ctx) {
+      cache_load8(cache.k, cache.k_meta, cache.dtype, orow, hd, e0, klo[i]);
+      cache_load8(cache.k, cache.k_meta, cache.dtype, orow, hd, e0 + half, khi[i]);
+      cache_load8(cache.v, cache.v_meta, cache.dtype, orow, hd, e0, vlo[i]);
+      cache_load8(cache.v, cache.v_meta, cache.dtype, orow, hd, e0 + half, vhi[i]);
+    }
     const CorrTok c = corr_token(t, t_ctx, tok_flags, fresh_row, tok_chunk, tok_delta, meta,
                                  n_chunks, rope_rows, flags, fresh_off);
-    const size_t orow = (size_t)t * hkv + h;
     const size_t mo = (size_t)c.chunk * hkv * hd + (size_t)h * hd;
     const float2 *mu_rot = (flags & AKVS_F_PRE_ROPE_OFFSETS)
                                ? rope + (size_t)min(t, rope_rows - 1) * half
                                : nullptr;
-    corr_side(c.fresh_k, c.fr, k_fresh, cache.k, cache.k_meta, cache.dtype, orow, hkv, h, hd, e0,
-              rope + (size_t)c.delta * half, mu_k ? mu_k + mo : nullptr, mu_k ? w_k[t] : 0.f,
-              klo[i], khi[i], mu_rot);
-    corr_side(c.fresh_v, c.fr, v_fresh, cache.v, cache.v_meta, cache.dtype, orow, hkv, h, hd, e0,
-              nullptr, mu_v ? mu_v + mo : nullptr, mu_v ? w_v[t] : 0.f, vlo[i], vhi[i]);
+    corr_finish(c.fresh_k, c.fr, k_fresh, hkv, h, hd, e0, rope + (size_t)c.delta * half,
+                mu_k ? mu_k + mo : nullptr, mu_k ? w_k[t] : 0.f, klo[i], khi[i], mu_rot);
+    corr_finish(c.fresh_v, c.fr, v_fresh, hkv, h, hd, e0, nullptr, mu_v ? mu_v + mo : nullptr,
+                mu_v ? w_v[t] : 0.f, vlo[i], vhi[i]);
   }
 #pragma unroll
   for (int i = 0; i < CORR_T; ++i) {
