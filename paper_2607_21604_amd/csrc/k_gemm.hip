@@ -2,11 +2,18 @@
 // epilogues: RoPE + q/k/v split (QKV), residual add into the fp32 stream (RESID),
 // SiLU(gate) * up (SWIGLU) and plain stores.
 //
-// bf16 path: 128x128x64 block tiles, 4 waves in 2x2, each wave 64x64 from 2x2 MFMA
-// 32x32x16 bf16 tiles with fp32 accumulation; operand tiles double-buffered in LDS,
-// next tile prefetched into registers during the MFMA loop. The accumulator tile is
-// staged through LDS so every epilogue can pair columns (rotary halves, gate/up) and
-// write coalesced rows. fp32 path (small models): 32x128x32 VALU tiles, same epilogues.
+// bf16 path, three kernels on v_mfma_f32_32x32x16_bf16 with fp32 accumulation, operand
+// tiles double-buffered in LDS and fed by register stages of global loads:
+//   k_gemm_bf16_w8 - 8 waves, BM x BN x 64 tiles (256/192 x 256/128), all waves on one
+//                    schedule interleaving loads, LDS stores and MFMAs;
+//   k_gemm_bf16_pp - 8 waves, 192 x 256 tiles, two wave groups alternating memory and
+//                    MFMA phases ("ping-pong");
+//   k_gemm_bf16    - 4 waves, 128 x 128 tiles, with the K split (and its fixup pass) for
+//                    grids too small to fill the GPU and for operands past 2 GiB.
+// launch_gemm picks the tile per launch from the expected row count. In every kernel the
+// accumulator tile is staged through LDS so the epilogues can pair columns (rotary halves,
+// gate/up) and write coalesced rows. fp32 path (small models): 32x128x32 VALU tiles, same
+// epilogues.
 #include <algorithm>
 #include <type_traits>
 
