@@ -326,11 +326,12 @@ __global__ __launch_bounds__(256) void k_attn_combine(const bf16_t *__restrict__
   const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
   const long long item = gid / per;
   const int e0 = (int)(gid - item * per) * 4;
-  if (item >= (long long)rows * hq) return;
+  int R = rows;
+  if (rows_dev) R = min(R, *rows_dev);
+  if (item >= (long long)R * hq) return;
+  if (row_base) out += (size_t)*row_base * hq * hd;
   const size_t stride = (size_t)rows * hq;  // items per split
-  if (n_splits <= 8) {
-    // every partial of this item requested at once, before the live row count arrives
-    // (slots of rows past it are in the buffer and never used)
+  if (n_splits <= 8) {  // every partial of this item requested at once
     float2 ml[8];
     float4 o[8];
 #pragma unroll
@@ -341,10 +342,6 @@ __global__ __launch_bounds__(256) void k_attn_combine(const bf16_t *__restrict__
         o[u] = load_bf4(part_o + pi * hd + e0);
       }
     }
-    int R = rows;
-    if (rows_dev) R = min(R, *rows_dev);
-    if (item >= (long long)R * hq) return;
-    if (row_base) out += (size_t)*row_base * hq * hd;
     float mx = -INFINITY;
 #pragma unroll
     for (int u = 0; u < 8; ++u)
@@ -363,10 +360,6 @@ __global__ __launch_bounds__(256) void k_attn_combine(const bf16_t *__restrict__
     store4(out + item * hd + e0, a.x * inv, a.y * inv, a.z * inv, a.w * inv);
     return;
   }
-  int R = rows;
-  if (rows_dev) R = min(R, *rows_dev);
-  if (item >= (long long)R * hq) return;
-  if (row_base) out += (size_t)*row_base * hq * hd;
   float mx = -INFINITY;
   {
     int sp = 0;
