@@ -242,3 +242,46 @@ def test_fullsize_check_layer_divergence_and_probe_sets(bench_case):
                       budgets, slack_k)
     check_valid_top_b(ref_v, d_v, [pv[off[i]:off[i + 1]] for i in range(len(LENS))], starts, LENS,
                       budgets, slack_v)
+
+
+@pytest.mark.parametrize("name,n_ctx,rows_kind", [
+    ("32b", 2600, "all"), ("32b", 2600, "probe"), ("7b", 4200, "all"), ("7b", 4200, "probe")])
+def test_attention_head_layouts_sampled_rows(name, n_ctx, rows_kind):
+    """Attention at the 32B (40 query heads over 8 KV heads) and 7B (28 over 4) head
+    layouts. All positions of a context: several query heads of one KV head per block,
+    sharing each K/V tile (5 and 7 heads per block at these row counts). About 900
+    probe-like rows: one head per block with key splits. Sampled rows, the tile edges and
+    the last rows among them, against per-row oracle attention, with and without the
+    split workspace."""
+    shape = synthetic.SHAPES[name]
+    hq, hkv, hd = shape.n_q_heads, shape.n_kv_heads, shape.head_dim
+    if rows_kind == "all":
+        pos = np.arange(n_ctx, dtype=np.int32)
+    else:
+        rng = np.random.default_rng(n_ctx)
+        pick = rng.choice(n_ctx - 64, size=900 - 64, replace=False)
+        pos = np.sort(np.concatenate([pick, np.arange(n_ctx - 64, n_ctx)])).astype(np.int32)
+    n = len(pos)
+    q = storage_round(synthetic.random_array((n, hq, hd), 71), torch.bfloat16)
+    k = storage_round(synthetic.random_array((n_ctx, hkv, hd), 72) * 3, torch.bfloat16)
+    v = storage_round(synthetic.random_array((n_ctx, hkv, hd), 73), torch.bfloat16)
+    m = akvs.model_cfg(shape, n_layers=1)
+    qd, pd, kd, vd = to_dev(q), to_dev(pos), to_dev(k), to_dev(v)
+    out_plain = torch.empty((n, hq * hd), dtype=torch.bfloat16, device=DEV)
+    akvs.akvs_sparse_query_attention(qd, pd, n, kd, vd, n_ctx, m, out_plain)
+    outs = [out_plain]
+    ws_bytes = akvs.akvs_attention_workspace_size(m, n, n_ctx)
+    if ws_bytes:
+        ws = torch.empty(ws_bytes, dtype=torch.uint8, device=DEV)
+        out_split = torch.empty_like(out_plain)
+        akvs.akvs_sparse_query_attention(qd, pd, n, kd, vd, n_ctx, m, out_split, ws)
+        outs.append(out_split)
+    torch.cuda.synchronize()
+    edges = [e for e in (31, 32, 63, 64, 127, 128, 159, 160, n - 65, n - 64) if 0 <= e < n]
+    rows = np.union1d(sample_rows(n, 29, 3), edges)
+    ref = oracle.attention(f64(q)[rows], pos[rows], f64(k), f64(v),
+                           np.arange(n_ctx)).reshape(len(rows), -1)
+    for o in outs:
+        assert max_rel(f64(o)[rows], ref) < 1e-2
+    if len(outs) == 2:
+        assert max_rel(f64(outs[1]), f64(outs[0])) < 1e-2

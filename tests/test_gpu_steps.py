@@ -378,7 +378,7 @@ def gemm_case(shape, n_rows, seed):
     return w, dims, lw, h
 
 
-@pytest.mark.parametrize("name,n_rows", [("3b", 200), ("7b", 129), ("tiny", 70)])
+@pytest.mark.parametrize("name,n_rows", [("3b", 200), ("7b", 129), ("32b", 300), ("tiny", 70)])
 def test_probe_qkv_and_out_mlp(name, n_rows):
     shape = synthetic.SHAPES[name]
     w, dims, lw, h = gemm_case(shape, n_rows, seed=3)
