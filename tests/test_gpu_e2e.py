@@ -230,3 +230,16 @@ def test_tiny_long_unit_reuse_prefill(long_units, flags):
     ref = long_units.oracle(flags=flags)
     out = long_units.gpu(flags=flags, probes=(ref["probe_k"], ref["probe_v"]))
     long_units.compare(out, ref)
+
+
+@pytest.mark.parametrize("lens", [[1, 2, 70, 1], [50], [1]])
+@pytest.mark.parametrize("refresh", [(1, 5), (0, 1)])
+def test_tiny_degenerate_unit_lengths(lens, refresh):
+    """Units of one and two tokens (whose budget ceil(r n) covers the whole unit on both
+    sides at r = 1/5, and nothing at r = 0), a single unit, and a single one-token unit:
+    the whole procedure against the oracle on the oracle's probe sets."""
+    c = Case("tiny", lens=lens)
+    ref = c.oracle(refresh=refresh)
+    given = (ref["probe_k"], ref["probe_v"]) if refresh[0] else None  # r = 0: empty sets
+    out = c.gpu(refresh=refresh, probes=given)
+    c.compare(out, ref)
