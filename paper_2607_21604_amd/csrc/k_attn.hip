@@ -309,101 +309,69 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
 // sum_s w_s o_s / sum_s w_s with w_s = 2^(m_s - max m) l_s, added in split order. A split
 // whose keys all lie past the row (causal mask) holds m = -inf and is skipped, never
 // multiplied in (its part_o slot holds whatever the workspace held).
-// Thread = 4 consecutive head dims of one (row, head). Up to 8 splits, all (m, l) pairs and
-// partial outputs are requested at once; with more, four splits at a time.
-__device__ __forceinline__ float4 load_bf4(const bf16_t *p) {
-  const uint2 w = *reinterpret_cast<const uint2 *>(p);
-  return make_float4(__uint_as_float(w.x << 16), __uint_as_float(w.x & 0xffff0000u),
-                     __uint_as_float(w.y << 16), __uint_as_float(w.y & 0xffff0000u));
-}
+// Thread = 8 consecutive head dims of one (row, head) (16-byte loads and stores). Up to 8
+// splits, all (m, l) pairs and partial outputs are requested at once; with more, the
+// maxima first, then the splits in order.
 __global__ __launch_bounds__(256) void k_attn_combine(const bf16_t *__restrict__ part_o,
                                                       const float *__restrict__ part_ml,
                                                       int n_splits, int rows,
                                                       const int32_t *rows_dev, int hq, int hd,
                                                       bf16_t *__restrict__ out,
                                                       const int32_t *row_base) {
-  const int per = hd >> 2;  // threads per (row, head)
+  const int per = hd >> 3;  // threads per (row, head)
   const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
   const long long item = gid / per;
-  const int e0 = (int)(gid - item * per) * 4;
+  const int e0 = (int)(gid - item * per) * 8;
   int R = rows;
   if (rows_dev) R = min(R, *rows_dev);
   if (item >= (long long)R * hq) return;
   if (row_base) out += (size_t)*row_base * hq * hd;
   const size_t stride = (size_t)rows * hq;  // items per split
+  float mx = -INFINITY, l = 0.f, a[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) a[i] = 0.f;
   if (n_splits <= 8) {  // every partial of this item requested at once
     float2 ml[8];
-    float4 o[8];
+    float o[8][8];
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       if (u < n_splits) {
         const size_t pi = u * stride + item;
         ml[u] = *reinterpret_cast<const float2 *>(part_ml + 2 * pi);
-        o[u] = load_bf4(part_o + pi * hd + e0);
+        load8(part_o + pi * hd + e0, o[u]);
       }
     }
-    float mx = -INFINITY;
 #pragma unroll
     for (int u = 0; u < 8; ++u)
       if (u < n_splits) mx = fmaxf(mx, ml[u].x);
     const float moff = mx == -INFINITY ? 0.f : mx;
-    float l = 0.f;
-    float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       if (u >= n_splits || ml[u].x == -INFINITY) continue;
       const float w = exp2f(ml[u].x - moff) * ml[u].y;
       l += w;
-      a.x += w * o[u].x; a.y += w * o[u].y; a.z += w * o[u].z; a.w += w * o[u].w;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) a[i] += w * o[u][i];
     }
-    const float inv = 1.0f / l;
-    store4(out + item * hd + e0, a.x * inv, a.y * inv, a.z * inv, a.w * inv);
-    return;
-  }
-  float mx = -INFINITY;
-  {
-    int sp = 0;
-    for (; sp + 8 <= n_splits; sp += 8) {  // eight maxima in flight per round trip
-      float v[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) v[u] = part_ml[2 * ((sp + u) * stride + item)];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) mx = fmaxf(mx, v[u]);
-    }
-    for (; sp < n_splits; ++sp) mx = fmaxf(mx, part_ml[2 * (sp * stride + item)]);
-  }
-  const float moff = mx == -INFINITY ? 0.f : mx;
-  float l = 0.f;
-  float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
-  int sp = 0;
-  for (; sp + 4 <= n_splits; sp += 4) {
-    float2 ml[4];
-    float4 o[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const size_t pi = (sp + u) * stride + item;
-      ml[u] = *reinterpret_cast<const float2 *>(part_ml + 2 * pi);
-      o[u] = load_bf4(part_o + pi * hd + e0);
-    }
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      if (ml[u].x == -INFINITY) continue;  // no visible key: its part_o was never written
-      const float w = exp2f(ml[u].x - moff) * ml[u].y;
+  } else {
+    for (int sp = 0; sp < n_splits; ++sp) mx = fmaxf(mx, part_ml[2 * (sp * stride + item)]);
+    const float moff = mx == -INFINITY ? 0.f : mx;
+    for (int sp = 0; sp < n_splits; ++sp) {
+      const size_t pi = sp * stride + item;
+      const float2 ml = *reinterpret_cast<const float2 *>(part_ml + 2 * pi);
+      if (ml.x == -INFINITY) continue;  // no visible key: its part_o was never written
+      float o[8];
+      load8(part_o + pi * hd + e0, o);
+      const float w = exp2f(ml.x - moff) * ml.y;
       l += w;
-      a.x += w * o[u].x; a.y += w * o[u].y; a.z += w * o[u].z; a.w += w * o[u].w;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) a[i] += w * o[i];
     }
-  }
-  for (; sp < n_splits; ++sp) {
-    const size_t pi = sp * stride + item;
-    const float2 ml = *reinterpret_cast<const float2 *>(part_ml + 2 * pi);
-    if (ml.x == -INFINITY) continue;
-    const float4 o = load_bf4(part_o + pi * hd + e0);
-    const float w = exp2f(ml.x - moff) * ml.y;
-    l += w;
-    a.x += w * o.x; a.y += w * o.y; a.z += w * o.z; a.w += w * o.w;
   }
   const float inv = 1.0f / l;
-  store4(out + item * hd + e0, a.x * inv, a.y * inv, a.z * inv, a.w * inv);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) a[i] *= inv;
+  store8(out + item * hd + e0, a);
 }
 
 // fp32 path (small models): one wave per (row, head), keys in tiles of 64, online softmax.
@@ -518,7 +486,7 @@ hipError_t launch_attention(const void *q, const int32_t *pos, int pos0, int row
     if (n_splits > 1) {
       hipError_t e = hipGetLastError();
       if (e != hipSuccess) return e;
-      const long long threads = (long long)rows * hq * (hd / 4);
+      const long long threads = (long long)rows * hq * (hd / 8);
       hipLaunchKernelGGL(k_attn_combine, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, s,
                          reinterpret_cast<const bf16_t *>(part_o), part_ml, n_splits, rows,
                          rows_dev, hq, hd, O, row_base);

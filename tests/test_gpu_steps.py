@@ -344,9 +344,11 @@ def test_constant_residual_is_recovered_on_gpu():
 
 @pytest.mark.parametrize("dtype,hq,hkv,hd,n_rows,n_keys", [
     ("bf16", 6, 2, 128, 77, 300), ("bf16", 28, 4, 128, 130, 1000), ("bf16", 4, 4, 64, 64, 64),
-    ("bf16", 24, 8, 128, 600, 2400),
+    ("bf16", 24, 8, 128, 600, 2400), ("bf16", 6, 2, 128, 5, 2000), ("bf16", 24, 8, 128, 3, 4096),
     ("f32", 4, 4, 64, 50, 288), ("f32", 6, 3, 128, 9, 70)])
 def test_sparse_query_attention(dtype, hq, hkv, hd, n_rows, n_keys):
+    """Against the oracle with and without the key-split workspace; the few-row cases split
+    the keys 8 and 16 ways (both merge paths)."""
     tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
     rng = np.random.default_rng(n_rows)
     pos = np.sort(rng.choice(n_keys, size=n_rows, replace=False)).astype(np.int32)
