@@ -502,10 +502,13 @@ __global__ __launch_bounds__(256) void k_correction(CacheLayer cache, const floa
     const float2 *mu_rot = (flags & AKVS_F_PRE_ROPE_OFFSETS)
                                ? rope + (size_t)min(t, rope_rows - 1) * half
                                : nullptr;
+    // the weights cover the unit tokens only ([t_ctx]); query rows are always fresh
+    const bool unit_tok = t < t_ctx;
     corr_finish(c.fresh_k, c.fr, k_fresh, hkv, h, hd, e0, rope + (size_t)c.delta * half,
-                mu_k ? mu_k + mo : nullptr, mu_k ? w_k[t] : 0.f, klo[i], khi[i], mu_rot);
+                mu_k ? mu_k + mo : nullptr, (mu_k && unit_tok) ? w_k[t] : 0.f, klo[i], khi[i],
+                mu_rot);
     corr_finish(c.fresh_v, c.fr, v_fresh, hkv, h, hd, e0, nullptr, mu_v ? mu_v + mo : nullptr,
-                mu_v ? w_v[t] : 0.f, vlo[i], vhi[i]);
+                (mu_v && unit_tok) ? w_v[t] : 0.f, vlo[i], vhi[i]);
   }
 #pragma unroll
   for (int i = 0; i < CORR_T; ++i) {

@@ -26,6 +26,9 @@ class Engine:
         self._ws = None
 
     def workspace(self, nbytes: int) -> torch.Tensor:
+        """The engine's workspace, grown when a call needs more. A grown workspace replaces
+        the old tensor; a captured graph keeps its own reference to the tensor it was
+        captured with (see ReuseGraph), so replays never run on freed memory."""
         if self._ws is None or self._ws.numel() < nbytes:
             self._ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=self.device)
         return self._ws
@@ -202,10 +205,12 @@ class BatchGraph:
         kw.pop("outputs", None)
         self.out = reuse_prefill_batch(engine, requests, *args, **kw)
         torch.cuda.synchronize(engine.device)
+        self.ws = engine._ws  # the captured kernels address this workspace: keep it alive
         self.graph = torch.cuda.CUDAGraph()
         with torch.cuda.graph(self.graph):
             reuse_prefill_batch(engine, requests, *args, outputs=self.out, **kw)
         torch.cuda.synchronize(engine.device)
+        assert engine._ws is self.ws
 
     def replay(self):
         self.graph.replay()
@@ -226,10 +231,12 @@ class ReuseGraph:
         kw.pop("outputs", None)
         self.out = engine.reuse_prefill(*args, **kw)
         torch.cuda.synchronize(engine.device)
+        self.ws = engine._ws  # the captured kernels address this workspace: keep it alive
         self.graph = torch.cuda.CUDAGraph()
         with torch.cuda.graph(self.graph):
             engine.reuse_prefill(*args, outputs=self.out, **kw)
         torch.cuda.synchronize(engine.device)
+        assert engine._ws is self.ws
 
     def replay(self):
         self.graph.replay()
@@ -243,10 +250,12 @@ class FullGraph:
     def __init__(self, engine: Engine, tokens: torch.Tensor, pos0: int = 0, want_h: bool = True):
         engine.full_prefill(tokens, pos0, want_h)  # sizes the workspace
         torch.cuda.synchronize(engine.device)
+        self.ws = engine._ws  # the captured kernels address this workspace: keep it alive
         self.graph = torch.cuda.CUDAGraph()
         with torch.cuda.graph(self.graph):
             self.out = engine.full_prefill(tokens, pos0, want_h)
         torch.cuda.synchronize(engine.device)
+        assert engine._ws is self.ws
 
     def replay(self):
         self.graph.replay()

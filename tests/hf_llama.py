@@ -63,3 +63,23 @@ def continue_from(model, past_k, past_v, tokens, pos0):
     pos = (pos0 + torch.arange(ids.shape[1]))[None]
     out = model(input_ids=ids, position_ids=pos, past_key_values=cache, use_cache=True)
     return out.last_hidden_state[0].numpy()
+
+
+def build_causal_lm(weights: dict, dims, vocab: int):
+    """LlamaForCausalLM with the output embedding tied to the input embedding, carrying
+    the same weights as a library-layout weight dict (fp64, eager attention)."""
+    from transformers import LlamaForCausalLM
+    base = build(weights, dims, vocab)
+    cfg = base.config
+    cfg.tie_word_embeddings = True
+    lm = LlamaForCausalLM(cfg).double().eval()
+    lm.model.load_state_dict(base.state_dict(), strict=True)
+    lm.tie_weights()
+    return lm
+
+
+@torch.no_grad()
+def next_token_logits(lm, tokens):
+    """Logits [n][vocab] of every position of an ordinary prefill of `tokens`."""
+    ids = torch.as_tensor(tokens, dtype=torch.long)[None]
+    return lm(input_ids=ids).logits[0].numpy()

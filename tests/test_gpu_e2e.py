@@ -66,14 +66,19 @@ class Case:
         off = np.concatenate([[0], np.cumsum(budgets)])
         return [flat[off[i]:off[i + 1]] for i in range(len(budgets))]
 
-    def compare(self, out, ref, tol=None):
+    def compare(self, out, ref, tol=None, rows=True):
+        """h_query and K_corr / V_corr of every layer, each layer against its own largest
+        reference value, within tol; the recomputed rows bit-exact."""
         tol = tol or self.tol
-        errs = {"h_query": max_rel(f64(out["h_query"]), ref["h_query"]),
-                "k_corr": max_rel(f64(out["k_corr"]), ref["k_corr"]),
-                "v_corr": max_rel(f64(out["v_corr"]), ref["v_corr"])}
+        errs = {"h_query": max_rel(f64(out["h_query"]), ref["h_query"])}
+        k, v = f64(out["k_corr"]), f64(out["v_corr"])
+        for l in range(ref["k_corr"].shape[0]):
+            errs[f"k_corr[{l}]"] = max_rel(k[l, :ref["k_corr"].shape[1]], ref["k_corr"][l])
+            errs[f"v_corr[{l}]"] = max_rel(v[l, :ref["v_corr"].shape[1]], ref["v_corr"][l])
         assert all(e <= tol for e in errs.values()), errs
-        n = int(out["n_rows"][0])
-        np.testing.assert_array_equal(out["rows"][:n].cpu().numpy(), ref["rows"])
+        if rows:
+            n = int(out["n_rows"][0])
+            np.testing.assert_array_equal(out["rows"][:n].cpu().numpy(), ref["rows"])
         return errs
 
 
@@ -175,31 +180,6 @@ def test_3b_width_full_refresh_equals_full_prefill(w3b):
     h, k, v = w3b.eng.full_prefill(w3b.tok_dev)
     assert max_rel(f64(out["h_query"]), f64(h)[-w3b.q:]) < 2e-2
     assert max_rel(f64(out["k_corr"]), f64(k)) < 2e-2
-
-
-@pytest.fixture(scope="module")
-def w7b():
-    return Case("7b", n_layers=3, n_units=8)
-
-
-def test_7b_width_reuse_prefill(w7b):
-    ref = w7b.oracle()
-    errs = w7b.compare(w7b.gpu(probes=(ref["probe_k"], ref["probe_v"])), ref)
-    print("7b-width errors", errs)
-
-
-@pytest.mark.parametrize("bits", [4, 2, 8])
-def test_7b_width_quantised_cache(w7b, bits):
-    codes_k, meta_k, deq_k, dt = oracle_quantized(f64(w7b.k_all), bits)
-    codes_v, meta_v, deq_v, _ = oracle_quantized(f64(w7b.v_all), bits)
-    kc = [deq_k[:, s:s + n] for s, n in zip(w7b.starts, w7b.lens)]
-    vc = [deq_v[:, s:s + n] for s, n in zip(w7b.starts, w7b.lens)]
-    ref = w7b.oracle(kc=kc, vc=vc)
-    out = w7b.gpu(probes=(ref["probe_k"], ref["probe_v"]),
-                  k_cache=to_dev(codes_k), v_cache=to_dev(codes_v),
-                  k_meta=to_dev(meta_k), v_meta=to_dev(meta_v), cache_dtype=dt)
-    errs = w7b.compare(out, ref)
-    print(f"7b-width {bits}-bit errors", errs)
 
 
 @pytest.mark.parametrize("flags,refresh_v", [

@@ -45,10 +45,20 @@ def test_graph_replays_match_eager(name, n_layers, n_units):
         got = snapshot(g.replay())
         torch.cuda.synchronize()
         assert_same(got, eager)
-        # eager work of the program between replays, on other buffers
+        # eager work of the program between replays, on other buffers; the full refresh
+        # needs a larger workspace, so the engine replaces its workspace tensor while the
+        # graph keeps the one it was captured with
         other = c.eng.reuse_prefill(c.tok_dev, c.lens, c.q, c.k_all, c.v_all, (1, 1), 1, 0)
         torch.cuda.synchronize()
         assert int(other["n_rows"][0]) == len(c.toks)
+        assert c.eng._ws is not g.ws
+        assert c.eng._ws.data_ptr() != g.ws.data_ptr()
+        # a replay writes nothing into the eager call's outputs or its workspace's results
+        before = snapshot(other)
+        again = snapshot(g.replay())
+        torch.cuda.synchronize()
+        assert_same(snapshot(other), before)
+        assert_same(again, eager)
 
 
 def test_graph_replay_with_new_tokens_in_place():
@@ -85,3 +95,9 @@ def test_batch_graph_replays_match_eager():
                                     r["v_cache"], (1, 1), 1, 0)
         torch.cuda.synchronize()
         assert int(other["n_rows"][0]) == sum(r["chunk_lens"]) + r["query_len"]
+        before = snapshot(other)
+        again = [snapshot(o) for o in g.replay()]
+        torch.cuda.synchronize()
+        assert_same(snapshot(other), before)
+        for a, b in zip(again, eager):
+            assert_same(a, b)

@@ -148,3 +148,27 @@ def test_decode_step_on_arbitrary_caches_matches_transformers_llama():
 
 def test_greedy_token_takes_the_lowest_index_of_equal_maxima():
     assert oracle.greedy_token(np.array([0.5, 2.0, -1.0, 2.0])) == 1
+
+
+def test_lm_logits_match_transformers_tied_causal_lm():
+    """Next-token logits of the final-normed rows with the output embedding tied to the
+    input embedding: the transformers LlamaForCausalLM (tie_word_embeddings) gives the same
+    logits at every position, and the same greedy token."""
+    dims, w, V = small_model(seed=13, hq=4, hkv=2, hd=8, D=32)
+    toks = context(13, [9, 6], 4, V)
+    h, _, _ = oracle.full_prefill(toks, 0, w, dims)
+    ours = oracle.lm_logits(h, w)
+    lm = hf_llama.build_causal_lm(w, dims, V)
+    assert lm.lm_head.weight.data_ptr() == lm.model.embed_tokens.weight.data_ptr()
+    ref = hf_llama.next_token_logits(lm, toks)
+    assert ours.shape == ref.shape == (len(toks), V)
+    close_to(ours, ref, 1e-5)  # the decoders differ by transformers' fp32 norms / angles
+    # the head alone, on transformers' own final hidden states: exact up to fp64 rounding
+    import torch
+    with torch.no_grad():
+        h_hf = lm.model(input_ids=torch.as_tensor(toks, dtype=torch.long)[None]).last_hidden_state[0]
+    close_to(oracle.lm_logits(h_hf.numpy(), w), ref, 1e-13)
+    assert [oracle.greedy_token(r) for r in ours] == [int(np.argmax(r)) for r in ref]
+    # an untied table is used when given
+    other = np.random.default_rng(13).standard_normal((V, dims.d_model))
+    np.testing.assert_allclose(oracle.lm_logits(h[:2], w, other), h[:2] @ other.T, rtol=1e-13)
