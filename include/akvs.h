@@ -14,7 +14,8 @@
  *    row-major, 16-byte aligned, unless the argument says "host". Descriptor structs
  *    and chunk-length arrays are host memory read during the call only. The library
  *    never allocates, frees or keeps a pointer; scratch memory comes from a caller
- *    workspace sized by akvs_workspace_size / akvs_step_workspace_size.
+ *    workspace sized by akvs_workspace_size / akvs_step_workspace_size (the one
+ *    exception, akvs_decode_step_noalloc, uses a fixed device array of the library).
  *  - Streams: every call only enqueues work on `stream` and returns; buffers must stay
  *    alive until the stream has finished. akvs_chunk_meta and the query functions are
  *    host-only. Calls on different streams must not share output or workspace buffers.
@@ -335,6 +336,28 @@ akvs_status akvs_decode_step(const int32_t *token, int32_t n_past, const void *e
                              const akvs_model_cfg *m, void *k_cache, void *v_cache,
                              int32_t cache_rows, float *logits, int32_t *next_token, void *ws,
                              size_t ws_bytes, hipStream_t stream);
+
+/* ---- decode step without allocation ---------------------------------------------------
+ * For callers that cannot allocate device memory or pass a workspace: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc. akvs_decode_step_noalloc
+ * is akvs_decode_step (same arguments, same kernels, identical results) with the workspace
+ * taken from a device array inside the library of AKVS_NOALLOC_SCRATCH_BYTES bytes, which
+ * every device that runs it holds until the process ends. The call itself allocates nothing
+ * and frees nothing; its first call on a device looks up that device's array address.
+ * Errors: AKVS_ENOSPACE when akvs_decode_workspace_size(m, n_past) exceeds
+ * AKVS_NOALLOC_SCRATCH_BYTES (the attention partials grow with n_past: about 200K past
+ * tokens for the 32B-class shape); AKVS_EINVAL when `stream` belongs to a device other
+ * than the calling thread's current one; otherwise as akvs_decode_step. All calls on one
+ * device share that device's array: calls that overlap in time on one device (on different
+ * streams, or from several threads without ordering) race on it and give unspecified
+ * results. Calls ordered on one stream are safe; the array keeps the last call's contents,
+ * none of which a later call reads before writing it. */
+#define AKVS_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+akvs_status akvs_decode_step_noalloc(const int32_t *token, int32_t n_past, const void *embed,
+                                     const akvs_layer_w *lw, const void *final_norm,
+                                     const void *w_out, const akvs_model_cfg *m, void *k_cache,
+                                     void *v_cache, int32_t cache_rows, float *logits,
+                                     int32_t *next_token, hipStream_t stream);
 
 /* ---- kernel timing -------------------------------------------------------------------
  * akvs_profile_enable(mask): for every kernel class whose bit (1 << class) is set in

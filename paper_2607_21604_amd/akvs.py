@@ -26,6 +26,7 @@ AKVS_F_FRESH_IF_RECOMPUTED = 4
 AKVS_F_NO_PREFIX_RECOMPUTE = 8
 AKVS_F_GIVEN_PROBES = 16
 AKVS_F_PRE_ROPE_OFFSETS = 32
+AKVS_NOALLOC_SCRATCH_BYTES = 32 << 20  # scratch array of akvs_decode_step_noalloc (akvs.h)
 (AKVS_K_GEMM, AKVS_K_ATTENTION, AKVS_K_CORRECTION, AKVS_K_OFFSET, AKVS_K_DIVERGENCE,
  AKVS_K_SELECT, AKVS_K_NORM, AKVS_K_OTHER, AKVS_K_GEMV) = range(9)
 KERNEL_CLASSES = ("gemm", "attention", "correction", "offset", "divergence", "select", "norm",
@@ -114,6 +115,8 @@ _SIGS = {
     "akvs_lm_head": (_I, [_P, _I, _P, ctypes.POINTER(ModelCfg), _P, _P, _P, ctypes.c_size_t, _P]),
     "akvs_decode_step": (_I, [_P, _I, _P, ctypes.POINTER(LayerW), _P, _P, ctypes.POINTER(ModelCfg),
                               _P, _P, _I, _P, _P, _P, ctypes.c_size_t, _P]),
+    "akvs_decode_step_noalloc": (_I, [_P, _I, _P, ctypes.POINTER(LayerW), _P, _P,
+                                      ctypes.POINTER(ModelCfg), _P, _P, _I, _P, _P, _P]),
     "akvs_profile_enable": (_I, [_I]),
     "akvs_profile_read": (_I, [_I, ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_double)]),
     "akvs_mfma_busy_loop": (_I, [_I, _I, _P, _P]),
@@ -365,6 +368,17 @@ def akvs_decode_step(token, n_past, embed, layers: ctypes.Array, final_norm, w_o
                                    int(cache_rows), ptr(logits), ptr(next_token), ptr(ws),
                                    ws.numel() * ws.element_size(), stream_handle(stream)),
            "akvs_decode_step")
+
+
+def akvs_decode_step_noalloc(token, n_past, embed, layers: ctypes.Array, final_norm, w_out,
+                             m: ModelCfg, k_cache, v_cache, cache_rows, logits, next_token,
+                             stream=None):
+    """akvs_decode_step on the library's own scratch array (no workspace argument)."""
+    _check(load().akvs_decode_step_noalloc(ptr(token), int(n_past), ptr(embed), layers,
+                                           ptr(final_norm), ptr(w_out), ctypes.byref(m),
+                                           ptr(k_cache), ptr(v_cache), int(cache_rows),
+                                           ptr(logits), ptr(next_token), stream_handle(stream)),
+           "akvs_decode_step_noalloc")
 
 
 def akvs_profile_enable(class_mask: int):

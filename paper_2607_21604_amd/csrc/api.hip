@@ -1353,11 +1353,15 @@ akvs_status akvs_lm_head(const float *h, int32_t n_rows, const void *w_out,
   return AKVS_OK;
 }
 
-akvs_status akvs_decode_step(const int32_t *token, int32_t n_past, const void *embed,
-                             const akvs_layer_w *lw, const void *final_norm, const void *w_out,
-                             const akvs_model_cfg *m, void *k_cache, void *v_cache,
-                             int32_t cache_rows, float *logits, int32_t *next_token, void *ws,
-                             size_t ws_bytes, hipStream_t stream) {
+}  // extern "C"
+
+// The decode step over a workspace of ws_bytes bytes at ws (a caller's buffer, or the
+// library's no-allocation scratch array).
+static akvs_status decode_step(const int32_t *token, int32_t n_past, const void *embed,
+                               const akvs_layer_w *lw, const void *final_norm, const void *w_out,
+                               const akvs_model_cfg *m, void *k_cache, void *v_cache,
+                               int32_t cache_rows, float *logits, int32_t *next_token, void *ws,
+                               size_t ws_bytes, hipStream_t stream) {
   akvs_status st = check_model(m);
   if (st) return st;
   if ((st = check_layers(m, lw))) return st;
@@ -1429,6 +1433,75 @@ akvs_status akvs_decode_step(const int32_t *token, int32_t n_past, const void *e
                                      m->rms_eps, b.hf, AKVS_F32, D, stream));
   return lm_head_row(m, b.hf, w_out ? w_out : embed, logits ? logits : b.logits, b.part_val,
                      b.part_idx, next_token, stream);
+}
+
+// ---- the no-allocation decode step --------------------------------------------------------
+// A device array of fixed size serves as the decode step's workspace for callers that
+// cannot allocate. Every device that runs it holds its own copy of the array (at its own
+// address) until the process ends. Host code never uses the array's name as an address:
+// the device address comes from hipGetSymbolAddress, looked up once per device with that
+// device current, and is what the kernels receive. The decode step's kernels write every
+// scratch value before they read it, so nothing needs clearing between calls.
+static __device__ __align__(256) unsigned char scratch[AKVS_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+static std::mutex g_scratch_mu;
+static void *g_scratch_dev[kMaxDevices];  // device address of `scratch` per device
+
+static akvs_status scratch_address(hipStream_t stream, void **out) {
+  int cur = -1;
+  hipError_t e = hipGetDevice(&cur);
+  if (e != hipSuccess) return fail(AKVS_EHIP, "hipGetDevice: %s", hipGetErrorString(e));
+  if (stream) {
+    hipDevice_t sd = -1;
+    e = hipStreamGetDevice(stream, &sd);
+    if (e != hipSuccess) return fail(AKVS_EHIP, "hipStreamGetDevice: %s", hipGetErrorString(e));
+    REQUIRE((int)sd == cur, AKVS_EINVAL,
+            "the stream belongs to device %d but device %d is current", (int)sd, cur);
+  }
+  REQUIRE(cur >= 0 && cur < kMaxDevices, AKVS_EUNSUPPORTED, "device index %d above %d", cur,
+          kMaxDevices - 1);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_dev[cur]) {
+    void *p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(AKVS_EHIP, "hipGetSymbolAddress(scratch) on device %d: %s", cur,
+                  hipGetErrorString(e));
+    g_scratch_dev[cur] = p;
+  }
+  *out = g_scratch_dev[cur];
+  return AKVS_OK;
+}
+
+extern "C" {
+
+akvs_status akvs_decode_step(const int32_t *token, int32_t n_past, const void *embed,
+                             const akvs_layer_w *lw, const void *final_norm, const void *w_out,
+                             const akvs_model_cfg *m, void *k_cache, void *v_cache,
+                             int32_t cache_rows, float *logits, int32_t *next_token, void *ws,
+                             size_t ws_bytes, hipStream_t stream) {
+  return decode_step(token, n_past, embed, lw, final_norm, w_out, m, k_cache, v_cache,
+                     cache_rows, logits, next_token, ws, ws_bytes, stream);
+}
+
+akvs_status akvs_decode_step_noalloc(const int32_t *token, int32_t n_past, const void *embed,
+                                     const akvs_layer_w *lw, const void *final_norm,
+                                     const void *w_out, const akvs_model_cfg *m, void *k_cache,
+                                     void *v_cache, int32_t cache_rows, float *logits,
+                                     int32_t *next_token, hipStream_t stream) {
+  akvs_status st = check_model(m);
+  if (st) return st;
+  REQUIRE(n_past >= 0, AKVS_EINVAL, "n_past must be >= 0");
+  const size_t need = akvs_decode_workspace_size(m, n_past);
+  REQUIRE(need > 0 && need <= AKVS_NOALLOC_SCRATCH_BYTES, AKVS_ENOSPACE,
+          "the decode step needs %zu bytes of scratch with n_past %d; the no-allocation entry "
+          "point holds %zu (use akvs_decode_step with a workspace)",
+          need, n_past, (size_t)AKVS_NOALLOC_SCRATCH_BYTES);
+  void *ws = nullptr;
+  if ((st = scratch_address(stream, &ws))) return st;
+  return decode_step(token, n_past, embed, lw, final_norm, w_out, m, k_cache, v_cache,
+                     cache_rows, logits, next_token, ws, AKVS_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 }  // extern "C"

@@ -204,3 +204,23 @@ def test_batch_workspace_and_validation(lib):
     st = lib.akvs_reuse_prefill_batch(tp, 0, 4096, lw, 4096, ctypes.byref(m), ca, None, None,
                                       4096, 1 << 30, None)
     assert st == akvs.AKVS_EINVAL and b"batch 0" in lib.akvs_last_error()
+
+
+def test_noalloc_decode_scratch_limit(lib):
+    """The no-allocation decode step states its scratch size in the header (the binding
+    carries the same number) and rejects, before touching the GPU, a step whose workspace
+    would exceed it."""
+    import re
+    from tests.libutil import HEADER
+    text = open(HEADER).read()
+    mt = re.search(r"#define AKVS_NOALLOC_SCRATCH_BYTES \(\(size_t\)(\d+) << (\d+)\)", text)
+    assert mt and int(mt.group(1)) << int(mt.group(2)) == akvs.AKVS_NOALLOC_SCRATCH_BYTES
+    m = akvs.ModelCfg(2, 3072, 24, 8, 128, 8192, 128256, 1e6, 1e-6, akvs.AKVS_BF16)
+    assert akvs.akvs_decode_workspace_size(m, 16128) <= akvs.AKVS_NOALLOC_SCRATCH_BYTES
+    big = 1 << 22
+    assert akvs.akvs_decode_workspace_size(m, big) > akvs.AKVS_NOALLOC_SCRATCH_BYTES
+    layers = (akvs.LayerW * 2)()
+    st = lib.akvs_decode_step_noalloc(None, big, None, layers, None, None, ctypes.byref(m), None,
+                                      None, big + 1, None, None, None)
+    assert st == akvs.AKVS_ENOSPACE
+    assert "no-allocation entry point holds" in lib.akvs_last_error().decode()
