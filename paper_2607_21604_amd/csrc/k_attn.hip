@@ -26,15 +26,27 @@ __device__ __forceinline__ int vt_col(int r, int g) { return (g ^ ((r >> 3) & 1)
 
 // Block shape for G query heads per KV head: heads per block gh (G split into G / gh
 // groups) and 32-row blocks per block nrb, 4 <= gh * nrb <= 8 waves, of which the first
-// four stage the K / V tiles. Heads of one KV head share a block (and its K / V tiles)
-// when that still gives two blocks per compute unit; with fewer rows (the recomputed
-// probe rows) each block takes one head and 128 rows, so that the blocks fill the GPU.
+// four stage the K / V tiles. With about 200 VGPRs a compute unit holds eight waves, so
+// blocks of 8 waves (one per unit) or 4 (two per unit) use every SIMD evenly. In order:
+//  - one head, 256 rows (8 waves sharing each K / V tile) when that still makes 512 blocks
+//    (32B probe layer, 5527 rows over 16128 keys: 1094 us against 1383 us for five-head
+//    blocks of 32 rows, whose 5 waves leave SIMDs unevenly loaded);
+//  - the G heads of a KV head sharing a block (and its K / V tiles) when that gives 512
+//    blocks;
+//  - else one head and 128 rows per block, so that the blocks fill the GPU (the key range
+//    is then split, see attn_splits).
 struct AttnShape {
   int gh, n_groups, nrb;
 };
 static inline AttnShape attn_shape(int G, int rows, int hkv) {
   AttnShape a{0, 0, 0};
   if (G < 1) return a;
+  if ((long long)((rows + 255) / 256) * hkv * G >= 512) {
+    a.gh = 1;
+    a.n_groups = G;
+    a.nrb = 8;
+    return a;
+  }
   int n = (G + 7) / 8;
   while (G % n) ++n;
   a.n_groups = n;

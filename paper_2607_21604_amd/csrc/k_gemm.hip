@@ -353,6 +353,26 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t gemm_rsrc(const void *p, uint3
                                            0x00020000);
 }
 
+
+// Output tile of block b: blocks past the live tile count exit; the live blocks are spread
+// so that each XCD (blocks b, b+8, ... of the dispatch order) takes one contiguous run of
+// the logical tile order, and the logical order walks groups of GM row tiles, rows fastest,
+// so that the blocks resident on one XCD share a few A and B panels in its L2.
+template <int GM>
+__device__ __forceinline__ bool grouped_tile(int b, int m_tiles, int n_tiles, int &mt, int &nt) {
+  const int live = m_tiles * n_tiles;
+  if (b >= live) return false;
+  const int x = b & 7, idx = b >> 3;
+  const int base = live >> 3, extra = live & 7;
+  const int t = x * base + min(x, extra) + idx;
+  const int per_group = GM * n_tiles;
+  const int g = t / per_group, local = t - g * per_group;
+  const int rows = min(GM, m_tiles - g * GM);
+  mt = g * GM + local % rows;
+  nt = local / rows;
+  return true;
+}
+
 template <int BM, int BN, int WGM, int NST>
 struct Gemm8 {
   static constexpr int WGN = 8 / WGM, WM = BM / WGM, WN = BN / WGN;
@@ -380,10 +400,10 @@ __global__ __launch_bounds__(512, 1) void k_gemm_bf16_w8(const bf16_t *__restric
   const bool swiglu = epi.mode == EPI_SWIGLU;
   const int bn_out = swiglu ? BN / 2 : BN;
   const int n_tiles = (N + bn_out - 1) / bn_out;
-  const int tile = blockIdx.x;
-  if (tile >= ((M_eff + BM - 1) / BM) * n_tiles) return;
-  const int m0 = (tile / n_tiles) * BM;
-  const int n0 = (tile - (tile / n_tiles) * n_tiles) * bn_out;
+  int mt_, nt_;
+  if (!grouped_tile<8>(blockIdx.x, (M_eff + BM - 1) / BM, n_tiles, mt_, nt_)) return;
+  const int m0 = mt_ * BM;
+  const int n0 = nt_ * bn_out;
   const __amdgpu_buffer_rsrc_t ra = gemm_rsrc(A, (uint32_t)((size_t)M_eff * lda * 2));
   const __amdgpu_buffer_rsrc_t rb = gemm_rsrc(B, (uint32_t)b_rows * (uint32_t)ldb * 2u);
 
@@ -563,10 +583,10 @@ __global__ __launch_bounds__(512, 1) void k_gemm_bf16_pp(const bf16_t *__restric
   const bool swiglu = epi.mode == EPI_SWIGLU;
   const int bn_out = swiglu ? BN / 2 : BN;
   const int n_tiles = (N + bn_out - 1) / bn_out;
-  const int tile = blockIdx.x;
-  if (tile >= ((M_eff + BM - 1) / BM) * n_tiles) return;
-  const int m0 = (tile / n_tiles) * BM;
-  const int n0 = (tile - (tile / n_tiles) * n_tiles) * bn_out;
+  int mt_, nt_;
+  if (!grouped_tile<8>(blockIdx.x, (M_eff + BM - 1) / BM, n_tiles, mt_, nt_)) return;
+  const int m0 = mt_ * BM;
+  const int n0 = nt_ * bn_out;
   const __amdgpu_buffer_rsrc_t ra = gemm_rsrc(A, (uint32_t)((size_t)M_eff * lda * 2));
   const __amdgpu_buffer_rsrc_t rb = gemm_rsrc(B, (uint32_t)b_rows * (uint32_t)ldb * 2u);
 
