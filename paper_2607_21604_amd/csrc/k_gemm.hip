@@ -10,7 +10,8 @@
 //                    MFMA phases ("ping-pong");
 //   k_gemm_bf16    - 4 waves, 128 x 128 tiles, with the K split (and its fixup pass) for
 //                    grids too small to fill the GPU and for operands past 2 GiB.
-// launch_gemm picks the tile per launch from the expected row count. In every kernel the
+// launch_gemm picks the tile per launch from the row count (on the device when only the device
+// knows it: k_gemm_bf16_pick runs the chosen kernel's blocks). In every kernel the
 // accumulator tile is staged through LDS so the epilogues can pair columns (rotary halves,
 // gate/up) and write coalesced rows. fp32 path (small models): 32x128x32 VALU tiles, same
 // epilogues.
@@ -385,23 +386,21 @@ struct Gemm8 {
   static_assert(WGM == 2 || WGM == 4, "wave rows must split in two halves");
 };
 
+// Body of block `bid` of the 8-wave kernel on LDS `smem` (S::SMEM bytes), M_eff live rows.
 template <int BM, int BN, int WGM, int NST>
-__global__ __launch_bounds__(512, 1) void k_gemm_bf16_w8(const bf16_t *__restrict__ A, int lda,
-                                                         const bf16_t *__restrict__ B, int ldb,
-                                                         int M, int N, int K, int b_rows,
-                                                         const int32_t *m_dev, Epi epi) {
+__device__ __forceinline__ void gemm_w8_body(unsigned char *smem, int bid,
+                                             const bf16_t *__restrict__ A, int lda,
+                                             const bf16_t *__restrict__ B, int ldb, int M_eff,
+                                             int N, int K, int b_rows, const Epi &epi) {
   using S = Gemm8<BM, BN, WGM, NST>;
-  __shared__ __attribute__((aligned(16))) unsigned char smem[S::SMEM];
   bf16_t *sm = reinterpret_cast<bf16_t *>(smem);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / S::WGN, wn = wave % S::WGN;
-  int M_eff = M;
-  if (m_dev) M_eff = min(M, *m_dev);
   const bool swiglu = epi.mode == EPI_SWIGLU;
   const int bn_out = swiglu ? BN / 2 : BN;
   const int n_tiles = (N + bn_out - 1) / bn_out;
   int mt_, nt_;
-  if (!grouped_tile<8>(blockIdx.x, (M_eff + BM - 1) / BM, n_tiles, mt_, nt_)) return;
+  if (!grouped_tile<8>(bid, (M_eff + BM - 1) / BM, n_tiles, mt_, nt_)) return;
   const int m0 = mt_ * BM;
   const int n0 = nt_ * bn_out;
   const __amdgpu_buffer_rsrc_t ra = gemm_rsrc(A, (uint32_t)((size_t)M_eff * lda * 2));
@@ -540,6 +539,16 @@ __global__ __launch_bounds__(512, 1) void k_gemm_bf16_w8(const bf16_t *__restric
   }
 }
 
+template <int BM, int BN, int WGM, int NST>
+__global__ __launch_bounds__(512, 1) void k_gemm_bf16_w8(const bf16_t *__restrict__ A, int lda,
+                                                         const bf16_t *__restrict__ B, int ldb,
+                                                         int M, int N, int K, int b_rows,
+                                                         const int32_t *m_dev, Epi epi) {
+  __shared__ __attribute__((aligned(16))) unsigned char smem[Gemm8<BM, BN, WGM, NST>::SMEM];
+  const int M_eff = m_dev ? min(M, *m_dev) : M;
+  gemm_w8_body<BM, BN, WGM, NST>(smem, blockIdx.x, A, lda, B, ldb, M_eff, N, K, b_rows, epi);
+}
+
 // ------------------------------------------------------------------------------------------
 // bf16 MFMA GEMM, 8 waves in two groups that take turns ("ping-pong"). Waves w and w + 4 of
 // a block run on the same SIMD, so group 0 (waves 0-3) and group 1 (waves 4-7) hold one wave
@@ -569,22 +578,19 @@ struct GemmPP {
 };
 
 template <int BM, int BN>
-__global__ __launch_bounds__(512, 1) void k_gemm_bf16_pp(const bf16_t *__restrict__ A, int lda,
-                                                         const bf16_t *__restrict__ B, int ldb,
-                                                         int M, int N, int K, int b_rows,
-                                                         const int32_t *m_dev, Epi epi) {
+__device__ __forceinline__ void gemm_pp_body(unsigned char *smem, int bid,
+                                             const bf16_t *__restrict__ A, int lda,
+                                             const bf16_t *__restrict__ B, int ldb, int M_eff,
+                                             int N, int K, int b_rows, const Epi &epi) {
   using S = GemmPP<BM, BN>;
-  __shared__ __attribute__((aligned(16))) unsigned char smem[S::SMEM];
   bf16_t *sm = reinterpret_cast<bf16_t *>(smem);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int grp = wave >> 2, wn = wave & 3;
-  int M_eff = M;
-  if (m_dev) M_eff = min(M, *m_dev);
   const bool swiglu = epi.mode == EPI_SWIGLU;
   const int bn_out = swiglu ? BN / 2 : BN;
   const int n_tiles = (N + bn_out - 1) / bn_out;
   int mt_, nt_;
-  if (!grouped_tile<8>(blockIdx.x, (M_eff + BM - 1) / BM, n_tiles, mt_, nt_)) return;
+  if (!grouped_tile<8>(bid, (M_eff + BM - 1) / BM, n_tiles, mt_, nt_)) return;
   const int m0 = mt_ * BM;
   const int n0 = nt_ * bn_out;
   const __amdgpu_buffer_rsrc_t ra = gemm_rsrc(A, (uint32_t)((size_t)M_eff * lda * 2));
@@ -691,6 +697,83 @@ __global__ __launch_bounds__(512, 1) void k_gemm_bf16_pp(const bf16_t *__restric
     __syncthreads();
     epilogue_tile<S::HM, BN, 512>(Cs, S::CLD, m0 + h * S::HM, n0, M_eff, N, epi);
     __syncthreads();
+  }
+}
+
+template <int BM, int BN>
+__global__ __launch_bounds__(512, 1) void k_gemm_bf16_pp(const bf16_t *__restrict__ A, int lda,
+                                                         const bf16_t *__restrict__ B, int ldb,
+                                                         int M, int N, int K, int b_rows,
+                                                         const int32_t *m_dev, Epi epi) {
+  __shared__ __attribute__((aligned(16))) unsigned char smem[GemmPP<BM, BN>::SMEM];
+  const int M_eff = m_dev ? min(M, *m_dev) : M;
+  gemm_pp_body<BM, BN>(smem, blockIdx.x, A, lda, B, ldb, M_eff, N, K, b_rows, epi);
+}
+
+// Block tiles of the 8-wave kernels with their rate per CU relative to the 256x256 tile,
+// measured on the 3B projection shapes with every CU busy (M = 1405 and 4516 rows). A launch
+// takes the tile with the least (rounds of one tile per CU) x (tile area) / rate at its row
+// count. The ping-pong kernel needs long compute phases: only its 192x256 tile was kept
+// (with 128 columns per tile a phase holds 12 MFMAs and the shared schedule is faster; at
+// 192x256 the shared schedule measured 0.75 against the ping-pong's 0.88). Checked on the
+// 7B and 32B projection shapes with the clocks warmed up: the model's pick was the fastest
+// tile or within a few percent of it.
+struct W8Tile {
+  int bm, bn;
+  bool pp;
+  float rate;
+};
+constexpr int kW8Count = 4;
+__host__ __device__ inline W8Tile w8_tile(int i) {
+  switch (i) {
+    case 0: return {256, 256, false, 1.0f};
+    case 1: return {192, 256, true, 0.88f};
+    case 2: return {256, 128, false, 0.78f};
+    default: return {192, 128, false, 0.74f};
+  }
+}
+__host__ __device__ inline int gemm_w8_tile(int M, int N, int mode, int cus) {
+  int best = 0;
+  float best_cost = 0;
+  for (int i = 0; i < kW8Count; ++i) {
+    const W8Tile c = w8_tile(i);
+    const int bn_out = mode == EPI_SWIGLU ? c.bn / 2 : c.bn;
+    const int tiles = ((M + c.bm - 1) / c.bm) * ((N + bn_out - 1) / bn_out);
+    const float cost = (float)((tiles + cus - 1) / cus) * (float)(c.bm * c.bn) / c.rate;
+    if (i == 0 || cost < best_cost) {
+      best = i;
+      best_cost = cost;
+    }
+  }
+  return best;
+}
+
+// One launch for a row count known only on the device: each block applies the tile model
+// to the live row count and runs as a block of the chosen kernel (blocks past that kernel's
+// tile count exit). The grid covers the largest of the four grids at the row cap M.
+constexpr int kPickSmem =
+    std::max(std::max(Gemm8<256, 256, 2, 1>::SMEM, GemmPP<192, 256>::SMEM),
+             std::max(Gemm8<256, 128, 4, 2>::SMEM, Gemm8<192, 128, 2, 2>::SMEM));
+__global__ __launch_bounds__(512, 1) void k_gemm_bf16_pick(const bf16_t *__restrict__ A, int lda,
+                                                           const bf16_t *__restrict__ B, int ldb,
+                                                           int M, int N, int K, int b_rows,
+                                                           const int32_t *m_dev, Epi epi,
+                                                           int cus) {
+  __shared__ __attribute__((aligned(16))) unsigned char smem[kPickSmem];
+  const int M_eff = min(M, *m_dev);
+  switch (gemm_w8_tile(M_eff, N, epi.mode, cus)) {
+    case 0:
+      gemm_w8_body<256, 256, 2, 1>(smem, blockIdx.x, A, lda, B, ldb, M_eff, N, K, b_rows, epi);
+      break;
+    case 1:
+      gemm_pp_body<192, 256>(smem, blockIdx.x, A, lda, B, ldb, M_eff, N, K, b_rows, epi);
+      break;
+    case 2:
+      gemm_w8_body<256, 128, 4, 2>(smem, blockIdx.x, A, lda, B, ldb, M_eff, N, K, b_rows, epi);
+      break;
+    default:
+      gemm_w8_body<192, 128, 2, 2>(smem, blockIdx.x, A, lda, B, ldb, M_eff, N, K, b_rows, epi);
+      break;
   }
 }
 
@@ -880,41 +963,6 @@ static GemmPlan gemm_plan(int M, int N, int K, const int32_t *m_dev, const Epi &
   return p;
 }
 
-// Block tiles of the 8-wave kernels with their rate per CU relative to the 256x256 tile,
-// measured on the 3B projection shapes with every CU busy (M = 1405 and 4516 rows). A launch
-// takes the tile with the least (rounds of one tile per CU) x (tile area) / rate at the
-// expected row count. The ping-pong kernel needs long compute phases: only its 192x256 tile
-// was kept (with 128 columns per tile a phase holds 12 MFMAs and the shared schedule is
-// faster; at 192x256 the shared schedule measured 0.75 against the ping-pong's 0.88).
-struct W8Tile {
-  int bm, bn;
-  bool pp;
-  double rate;
-};
-static const W8Tile kW8Tiles[] = {{256, 256, false, 1.0},
-                                  {192, 256, true, 0.88},
-                                  {256, 128, false, 0.78},
-                                  {192, 128, false, 0.74}};
-constexpr int kW8Count = sizeof(kW8Tiles) / sizeof(kW8Tiles[0]);
-
-static int gemm_w8_tile(int M_est, int N, int mode) {
-  const long long cus = gemm_cu_count();
-  int best = 0;
-  double best_cost = 0;
-  for (int i = 0; i < kW8Count; ++i) {
-    const W8Tile &c = kW8Tiles[i];
-    const int bn_out = mode == EPI_SWIGLU ? c.bn / 2 : c.bn;
-    const long long tiles =
-        (long long)((M_est + c.bm - 1) / c.bm) * ((N + bn_out - 1) / bn_out);
-    const double cost = (double)((tiles + cus - 1) / cus) * c.bm * c.bn / c.rate;
-    if (i == 0 || cost < best_cost) {
-      best = i;
-      best_cost = cost;
-    }
-  }
-  return best;
-}
-
 template <int BM, int BN, int WGM, int NST>
 static void launch_w8(const void *A, int lda, const void *B, int ldb, int M, int N, int K,
                       const int32_t *m_dev, const Epi &epi, hipStream_t s) {
@@ -947,8 +995,29 @@ hipError_t launch_gemm(const void *A, int lda, const void *B, int ldb, int M, in
     // buffer offsets are 32-bit: larger operands stay on the 4-wave kernel
     const bool fits = (size_t)M * lda * 2 < (1u << 31) && b_rows * ldb * 2 < (1u << 31);
     if (!p.any_split && fits) {
-      const int M_est = m_dev ? (std::max(m_min, 1) + M) / 2 : M;
-      switch (gemm_w8_tile(M_est, N, epi.mode)) {
+      const int cus = gemm_cu_count();
+      int choice = gemm_w8_tile(M, N, epi.mode, cus);
+      if (m_dev) {
+        // a row count known only on the device: one static tile if every count the host
+        // cannot rule out picks it, else the launch that picks on the device
+        bool one = true;
+        for (int m = std::max(m_min, 1); m < M && one; m = std::min(M, m + 16))
+          one = gemm_w8_tile(m, N, epi.mode, cus) == choice;
+        if (!one) {
+          int grid = 0;
+          for (int i = 0; i < kW8Count; ++i) {
+            const W8Tile c = w8_tile(i);
+            const int bn_out = epi.mode == EPI_SWIGLU ? c.bn / 2 : c.bn;
+            grid = std::max(grid, ((M + c.bm - 1) / c.bm) * ((N + bn_out - 1) / bn_out));
+          }
+          hipLaunchKernelGGL(k_gemm_bf16_pick, dim3(grid), dim3(512), 0, s,
+                             reinterpret_cast<const bf16_t *>(A), lda,
+                             reinterpret_cast<const bf16_t *>(B), ldb, M, N, K,
+                             epi.mode == EPI_SWIGLU ? 2 * N : N, m_dev, epi, cus);
+          return hipGetLastError();
+        }
+      }
+      switch (choice) {
         case 0: launch_w8<256, 256, 2, 1>(A, lda, B, ldb, M, N, K, m_dev, epi, s); break;
         case 1: launch_pp<192, 256>(A, lda, B, ldb, M, N, K, m_dev, epi, s); break;
         case 2: launch_w8<256, 128, 4, 2>(A, lda, B, ldb, M, N, K, m_dev, epi, s); break;
