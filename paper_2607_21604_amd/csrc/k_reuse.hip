@@ -524,7 +524,7 @@ __global__ __launch_bounds__(256) void k_correction(CacheLayer cache, const floa
   }
 }
 
-// The correction for bf16 unit caches (the common case). A thread serves one side (K or V)
+// The correction for bf16 and quantised unit caches. A thread serves one side (K or V)
 // of a position's 16-element pair group, in few enough registers that eight waves fit on
 // each SIMD, and reads only the rows it uses: the token's bookkeeping first, then either
 // its cache row (reused) or its fresh row (recomputed), so the cache rows of recomputed
@@ -601,9 +601,17 @@ __global__ __launch_bounds__(256) void k_correction_bf(CacheLayer cache, const f
       for (int i = 0; i < 8; ++i) lo[i] = hi[i] = 0.f;
     }
   } else {
-    const bf16_t *cb = reinterpret_cast<const bf16_t *>(vside ? cache.v : cache.k) + orow * hd;
-    unpack_bf8(__builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(cb + e0)), lo);
-    unpack_bf8(__builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(cb + e0 + half)), hi);
+    if (cache.dtype == AKVS_BF16) {
+      const bf16_t *cb = reinterpret_cast<const bf16_t *>(vside ? cache.v : cache.k) + orow * hd;
+      unpack_bf8(__builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(cb + e0)), lo);
+      unpack_bf8(__builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(cb + e0 + half)),
+                 hi);
+    } else {  // quantised unit caches: codes and their group's scale / zero
+      const void *cb = vside ? cache.v : cache.k;
+      const _Float16 *cm = vside ? cache.v_meta : cache.k_meta;
+      cache_load8(cb, cm, cache.dtype, orow, hd, e0, lo);
+      cache_load8(cb, cm, cache.dtype, orow, hd, e0 + half, hi);
+    }
     const float *mu = vside ? mu_v : mu_k;
     const size_t mo = (size_t)chunk * hkv * hd + (size_t)h * hd;
     const float w = mu ? (vside ? w_v[t] : w_k[t]) : 0.f;
@@ -650,7 +658,7 @@ hipError_t launch_correction(CacheLayer cache, const float *mu_k, const float *m
   if (threads == 0) return hipSuccess;
   dim3 g((unsigned)((threads + 255) / 256)), b(256);
   const float2 *r = reinterpret_cast<const float2 *>(rope);
-  if (cache.dtype == AKVS_BF16 && CORR_T == 1) {
+  if (cache.dtype != AKVS_F32 && CORR_T == 1) {
     const long long thr2 = (long long)t_all * 2 * hkv * (hd / 16);
     g = dim3((unsigned)((thr2 + 255) / 256));
     if (out_dtype == AKVS_BF16)
