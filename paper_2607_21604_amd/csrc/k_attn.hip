@@ -24,40 +24,26 @@ namespace akvs {
 constexpr int VT_ST = 72;
 __device__ __forceinline__ int vt_col(int r, int g) { return (g ^ ((r >> 3) & 1)) * 4; }
 
-// Block shape for G query heads per KV head: heads per block gh (G split into G / gh
-// groups) and 32-row blocks per block nrb, 4 <= gh * nrb <= 8 waves, of which the first
-// four stage the K / V tiles. With about 200 VGPRs a compute unit holds eight waves, so
-// blocks of 8 waves (one per unit) or 4 (two per unit) use every SIMD evenly. In order:
-//  - one head, 256 rows (8 waves sharing each K / V tile) when that still makes 512 blocks
-//    (32B probe layer, 5527 rows over 16128 keys: 1094 us against 1383 us for five-head
-//    blocks of 32 rows, whose 5 waves leave SIMDs unevenly loaded);
-//  - the G heads of a KV head sharing a block (and its K / V tiles) when that gives 512
-//    blocks;
-//  - else one head and 128 rows per block, so that the blocks fill the GPU (the key range
-//    is then split, see attn_splits).
+// Block shape: one query head per block, 32-row waves. With about 200 VGPRs (250 for the
+// read-ahead variant) a compute unit holds eight waves, so blocks of 8 waves (one per unit)
+// or 4 (two per unit) use every SIMD evenly; the first four waves stage the K / V tiles.
+//  - 256 rows (8 waves sharing each K / V tile) when that still makes 512 blocks (32B probe
+//    layer, 5527 rows over 16128 keys: 1094 us against 1383 us for blocks that grouped the
+//    five query heads of a KV head over 32 rows, whose 5 waves leave SIMDs unevenly loaded);
+//  - else 128 rows (4 waves) per block; when those make fewer than 512 blocks the key range
+//    is split as well (see attn_splits). (32B probe layer at r = 1/10, 3050 rows: 664 us
+//    against 751 us for the five-head 32-row blocks; the 3B full prefill measured the same
+//    with three-head 64-row blocks. Grouped-head blocks never make more blocks than these,
+//    so they are not used; the kernel still takes the general head grouping gh.)
 struct AttnShape {
   int gh, n_groups, nrb;
 };
 static inline AttnShape attn_shape(int G, int rows, int hkv) {
   AttnShape a{0, 0, 0};
   if (G < 1) return a;
-  if ((long long)((rows + 255) / 256) * hkv * G >= 512) {
-    a.gh = 1;
-    a.n_groups = G;
-    a.nrb = 8;
-    return a;
-  }
-  int n = (G + 7) / 8;
-  while (G % n) ++n;
-  a.n_groups = n;
-  a.gh = G / n;
-  a.nrb = 8 / a.gh < 4 ? 8 / a.gh : 4;
-  const long long blocks = (long long)((rows + 32 * a.nrb - 1) / (32 * a.nrb)) * hkv * n;
-  if (blocks < 512) {
-    a.gh = 1;
-    a.n_groups = G;
-    a.nrb = 4;
-  }
+  a.gh = 1;
+  a.n_groups = G;
+  a.nrb = (long long)((rows + 255) / 256) * hkv * G >= 512 ? 8 : 4;
   return a;
 }
 
