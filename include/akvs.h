@@ -376,9 +376,11 @@ akvs_status akvs_profile_read(int32_t kernel_class, int64_t *launches, double *t
 
 /* ---- counter calibration ----------------------------------------------------------------
  * akvs_mfma_busy_loop: not part of the method; the reference point for hardware counters
- * of matrix-core use. Launches n_blocks blocks of 256 threads in which every wave issues
- * iters x 8 independent 32x32x16 bf16 MFMAs and nothing else (the matrix cores of every
- * SIMD it occupies stay busy), then writes one fp32 per thread to out (device
+ * of matrix-core use and for the MFMA rate the chip sustains. Launches n_blocks blocks of
+ * 256 threads in which every wave issues iters (rounded up to even) x 8 independent
+ * 32x32x16 bf16 MFMAs on random operands that change from one MFMA to the next, and
+ * nothing else (the matrix cores of every SIMD it occupies stay busy), then writes one
+ * fp32 per thread to out (device
  * [n_blocks * 256], caller-owned, 16-byte aligned). Asynchronous on stream. Errors:
  * EINVAL for negative sizes, a null or misaligned out (with n_blocks > 0); EHIP. */
 akvs_status akvs_mfma_busy_loop(int32_t n_blocks, int32_t iters, float *out, hipStream_t stream);

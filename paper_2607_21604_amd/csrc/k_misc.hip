@@ -264,22 +264,34 @@ hipError_t launch_token_setup(const int32_t *meta, int n_chunks, int32_t *tok_de
 
 // ---- measurement helper --------------------------------------------------------------
 // A loop of independent v_mfma_f32_32x32x16_bf16 (8 accumulators per wave, no other work)
-// that keeps the matrix cores busy: the reference for the MFMA-busy counters.
+// that keeps the matrix cores busy: the reference for the MFMA-busy counters and for the
+// rate the chip sustains. The operands are random bf16 values in [-1, 1), four sets per
+// lane used in turn, so that every MFMA sees other operand bits than the one before (the
+// matrix cores draw more power, and the clock settles lower, on changing data than on a
+// constant operand).
 __global__ __launch_bounds__(256) void k_mfma_busy_loop(float *out, int iters) {
-  bf16x8_t a, b;
+  bf16x8_t a[4], b[4];
+  uint32_t x = 0x9e3779b9u * (blockIdx.x * 256 + threadIdx.x + 1);
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    a[j] = (__bf16)(0.001f * (float)(threadIdx.x + j));
-    b[j] = (__bf16)(0.002f * (float)j);
-  }
+  for (int s = 0; s < 4; ++s)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      x ^= x << 13; x ^= x >> 17; x ^= x << 5;
+      a[s][j] = (__bf16)((float)(x >> 8) * (2.0f / 16777216.0f) - 1.0f);
+      x ^= x << 13; x ^= x >> 17; x ^= x << 5;
+      b[s][j] = (__bf16)((float)(x >> 8) * (2.0f / 16777216.0f) - 1.0f);
+    }
   f32x16_t acc[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i)
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[i][r] = 0.f;
-  for (int it = 0; it < iters; ++it)
+  for (int it = 0; it < iters; it += 2) {
 #pragma unroll
-    for (int i = 0; i < 8; ++i) acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[i], 0, 0, 0);
+    for (int i = 0; i < 8; ++i) acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i & 3], b[(i + 1) & 3], acc[i], 0, 0, 0);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[(i + 2) & 3], b[(i + 3) & 3], acc[i], 0, 0, 0);
+  }
   float sum = 0.f;
 #pragma unroll
   for (int i = 0; i < 8; ++i)
