@@ -155,8 +155,14 @@ size_t akvs_attention_workspace_size(const akvs_model_cfg *m, int32_t n_rows, in
 
 /* ---- step entries ---------------------------------------------------------------- */
 
-/* Rotary table for positions 0..n_pos-1: table[p][k] = (cos, sin)(p * theta^(-2k/hd)),
- * angles and their cos/sin in fp64, stored rounded to fp32. table: [n_pos][hd/2][2]. */
+/* Rotary table for positions 0..n_pos-1 (Sec. 2: reused states are moved to their new
+ * positions by adjusting their positional embedding; rotary embeddings, rotate-half form, are
+ * this library's reading of the decoders of Sec. 4.1, and every re-rotation, probe QKV
+ * projection and pre-RoPE offset reads this table):
+ * table[p][k] = (cos, sin)(p * theta^(-2k/hd)), angles and their cos/sin in fp64, stored
+ * rounded to fp32. table: [n_pos][hd/2][2], caller-owned device memory, 16-byte aligned;
+ * n_pos = 0 writes nothing. Errors: EINVAL (n_pos < 0, hd odd or outside [2, 1024],
+ * theta <= 0, null or misaligned table), EHIP. */
 akvs_status akvs_rope_table(int32_t n_pos, int32_t head_dim, float rope_theta, float *table,
                             hipStream_t stream);
 
@@ -245,9 +251,11 @@ akvs_status akvs_sparse_query_attention(const void *q, const int32_t *positions,
                                         const akvs_model_cfg *m, void *out, void *ws,
                                         size_t ws_bytes, hipStream_t stream);
 
-/* Rest of the probe rows' layer: h += attn_out W_o^T; x = RMSNorm(h) * mlp_norm;
- * h += (silu(x W_gate^T) * (x W_up^T)) W_down^T. h: [n_rows][D] fp32 (updated in
- * place); attn_out: [n_rows][Hq*hd] model dtype. */
+/* Rest of the probe rows' layer (Algorithm 1, "recompute fresh KV for S_K u S_V at layer
+ * l": the fresh K/V of the next layer need these rows' hidden states carried through this
+ * layer's attention output and MLP; Sec. 3.3): h += attn_out W_o^T;
+ * x = RMSNorm(h) * mlp_norm; h += (silu(x W_gate^T) * (x W_up^T)) W_down^T.
+ * h: [n_rows][D] fp32 (updated in place); attn_out: [n_rows][Hq*hd] model dtype. */
 akvs_status akvs_probe_out_mlp(float *h, int32_t n_rows, const void *attn_out,
                                const akvs_model_cfg *m, const akvs_layer_w *lw, void *ws,
                                size_t ws_bytes, hipStream_t stream);
