@@ -387,11 +387,15 @@ struct Gemm8 {
 };
 
 // Body of block `bid` of the 8-wave kernel on LDS `smem` (S::SMEM bytes), M_eff live rows.
+// With splits > 1 block bid computes k-slice bid % splits of tile bid / splits and writes
+// its fp32 partial tile to part ([tile][split][BM][BN], tiles in row-major order) for
+// k_gemm_fixup, which adds the slices in order and runs the epilogue.
 template <int BM, int BN, int WGM, int NST>
 __device__ __forceinline__ void gemm_w8_body(unsigned char *smem, int bid,
                                              const bf16_t *__restrict__ A, int lda,
                                              const bf16_t *__restrict__ B, int ldb, int M_eff,
-                                             int N, int K, int b_rows, const Epi &epi) {
+                                             int N, int K, int b_rows, const Epi &epi,
+                                             int splits = 1, float *part = nullptr) {
   using S = Gemm8<BM, BN, WGM, NST>;
   bf16_t *sm = reinterpret_cast<bf16_t *>(smem);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -399,8 +403,9 @@ __device__ __forceinline__ void gemm_w8_body(unsigned char *smem, int bid,
   const bool swiglu = epi.mode == EPI_SWIGLU;
   const int bn_out = swiglu ? BN / 2 : BN;
   const int n_tiles = (N + bn_out - 1) / bn_out;
+  const int tile_bid = bid / splits, split = bid - tile_bid * splits;
   int mt_, nt_;
-  if (!grouped_tile<8>(bid, (M_eff + BM - 1) / BM, n_tiles, mt_, nt_)) return;
+  if (!grouped_tile<8>(tile_bid, (M_eff + BM - 1) / BM, n_tiles, mt_, nt_)) return;
   const int m0 = mt_ * BM;
   const int n0 = nt_ * bn_out;
   const __amdgpu_buffer_rsrc_t ra = gemm_rsrc(A, (uint32_t)((size_t)M_eff * lda * 2));
@@ -427,7 +432,10 @@ __device__ __forceinline__ void gemm_w8_body(unsigned char *smem, int bid,
     }
     loff[c] = r * G_LDS + kc;
   }
-  const int nk = K / GB_K;
+  const int nk_all = K / GB_K;
+  const int per = (nk_all + splits - 1) / splits;
+  const int kt0 = min(nk_all, split * per);
+  const int nk = max(1, min(nk_all, kt0 + per) - kt0);  // >= 1: splits <= nk_all
 
   f32x16_t acc[S::MI][S::NJ];
 #pragma unroll
@@ -443,7 +451,7 @@ __device__ __forceinline__ void gemm_w8_body(unsigned char *smem, int bid,
 
 #define AKVS_W8_GL(ST, KT, C0, C1)                                                          \
   {                                                                                         \
-    const int so_ = (KT) * GB_K * 2;                                                        \
+    const int so_ = (kt0 + (KT)) * GB_K * 2;                                                \
     _Pragma("unroll") for (int c = (C0); c < (C1); ++c) rg[ST][c] = __builtin_bit_cast(     \
         u32x4_t, c < S::ACH ? __builtin_amdgcn_raw_buffer_load_b128(ra, goff[c], so_, 0)    \
                             : __builtin_amdgcn_raw_buffer_load_b128(rb, goff[c], so_, 0));  \
@@ -514,6 +522,22 @@ __device__ __forceinline__ void gemm_w8_body(unsigned char *smem, int bid,
 #undef AKVS_W8_FR
 #undef AKVS_W8_SS
 #undef AKVS_W8_GL
+
+  if (splits > 1) {  // this k-slice's fp32 partial tile, rows of BN floats
+    const int t_rm = mt_ * n_tiles + nt_;
+    float *dst = part + ((size_t)t_rm * splits + split) * BM * BN;
+#pragma unroll
+    for (int i = 0; i < S::MI; ++i)
+#pragma unroll
+      for (int j = 0; j < S::NJ; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = wm * S::WM + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+          const int col = wn * S::WN + j * 32 + (lane & 31);
+          dst[row * BN + col] = acc[i][j][r];
+        }
+    return;
+  }
 
   // epilogue: rows [h * HB, (h + 1) * HB) of the tile belong to waves wm / (WGM / 2) == h
   float *Cs = reinterpret_cast<float *>(smem);
@@ -748,9 +772,27 @@ __host__ __device__ inline int gemm_w8_tile(int M, int N, int mode, int cus) {
   return best;
 }
 
+// K split of the 192x128 8-wave tile for row counts whose tiles would leave at least half of
+// the CUs idle (probe layers at small refresh ratios, the query rows of the last layer):
+// about one round of (tile, k-slice) items, slices of at least 16 k-tiles, at most 8 per
+// tile; k_gemm_fixup adds the slices in order. (At 810 rows of the 3B shape the output and
+// down projections make 120 such tiles for 256 CUs.)
+constexpr int kW8SplitBM = 192, kW8SplitBN = 128;
+__host__ __device__ inline int w8_k_splits(int M, int N, int K, int mode, int cus) {
+  const int bn_out = mode == EPI_SWIGLU ? kW8SplitBN / 2 : kW8SplitBN;
+  const int tiles = ((M + kW8SplitBM - 1) / kW8SplitBM) * ((N + bn_out - 1) / bn_out);
+  const int nk = K / GB_K;
+  if (tiles <= 0 || 2 * tiles > cus || nk < 32) return 1;
+  int sp = cus / tiles;
+  if (sp > nk / 16) sp = nk / 16;
+  if (sp > 8) sp = 8;
+  return sp < 2 ? 1 : sp;
+}
+
 // One launch for a row count known only on the device: each block applies the tile model
-// to the live row count and runs as a block of the chosen kernel (blocks past that kernel's
-// tile count exit). The grid covers the largest of the four grids at the row cap M.
+// (and, with a partial-tile workspace, the K split) to the live row count and runs as a
+// block of the chosen kernel (blocks past that kernel's item count exit). The grid covers
+// the largest of the grids over the row counts the host cannot rule out.
 constexpr int kPickSmem =
     std::max(std::max(Gemm8<256, 256, 2, 1>::SMEM, GemmPP<192, 256>::SMEM),
              std::max(Gemm8<256, 128, 4, 2>::SMEM, Gemm8<192, 128, 2, 2>::SMEM));
@@ -758,9 +800,15 @@ __global__ __launch_bounds__(512, 1) void k_gemm_bf16_pick(const bf16_t *__restr
                                                            const bf16_t *__restrict__ B, int ldb,
                                                            int M, int N, int K, int b_rows,
                                                            const int32_t *m_dev, Epi epi,
-                                                           int cus) {
+                                                           int cus, float *part) {
   __shared__ __attribute__((aligned(16))) unsigned char smem[kPickSmem];
-  const int M_eff = min(M, *m_dev);
+  const int M_eff = m_dev ? min(M, *m_dev) : M;
+  const int sp = part ? w8_k_splits(M_eff, N, K, epi.mode, cus) : 1;
+  if (sp > 1) {
+    gemm_w8_body<kW8SplitBM, kW8SplitBN, 2, 2>(smem, blockIdx.x, A, lda, B, ldb, M_eff, N, K,
+                                               b_rows, epi, sp, part);
+    return;
+  }
   switch (gemm_w8_tile(M_eff, N, epi.mode, cus)) {
     case 0:
       gemm_w8_body<256, 256, 2, 1>(smem, blockIdx.x, A, lda, B, ldb, M_eff, N, K, b_rows, epi);
@@ -801,7 +849,9 @@ __device__ __forceinline__ float4 sum_pieces(const float *p, size_t stride, int 
 // Second pass of a K-split GEMM: a block takes G_FR rows of one tile, adds their partial
 // rows in split order into an LDS slice and runs the epilogue on it.
 constexpr int G_FR = 16;
-template <int BM>
+// W8: partials of the 192x128 8-wave tile (split by w8_k_splits, n_slots = CU count), else
+// of the 4-wave 128x128 kernel (gemm_k_splits).
+template <int BM, bool W8>
 __global__ __launch_bounds__(256) void k_gemm_fixup(int M, int N, int K, const int32_t *m_dev,
                                                     Epi epi, int n_slots,
                                                     const float *__restrict__ part) {
@@ -812,7 +862,8 @@ __global__ __launch_bounds__(256) void k_gemm_fixup(int M, int N, int K, const i
   const int bn_out = swiglu ? GB_N / 2 : GB_N;
   const int n_tiles = (N + bn_out - 1) / bn_out;
   const int tiles = ((M_eff + BM - 1) / BM) * n_tiles;
-  const int splits = gemm_k_splits(tiles, K / GB_K, n_slots);
+  const int splits = W8 ? w8_k_splits(M_eff, N, K, epi.mode, n_slots)
+                        : gemm_k_splits(tiles, K / GB_K, n_slots);
   constexpr int SLICES = BM / G_FR;
   const int tile = blockIdx.x / SLICES, slice = blockIdx.x - tile * SLICES;
   if (splits < 2 || tile >= tiles) return;
@@ -932,7 +983,16 @@ size_t gemm_part_floats(int M, int N, int K, int mode) {
     const int sp = gemm_k_splits(t, K / GB_K, n_slots);
     if (sp > 1 && (size_t)t * sp > items) items = (size_t)t * sp;
   }
-  return items * 128 * GB_N;
+  size_t floats = items * 128 * GB_N;
+  // the 8-wave split: at most one (tile, slice) item per CU, for any row count up to M
+  const int cus = gemm_cu_count();
+  for (int m = 1; m <= M; m = (m == M ? M + 1 : std::min(M, m + 16))) {
+    if (w8_k_splits(m, N, K, mode, cus) > 1) {
+      floats = std::max(floats, (size_t)cus * kW8SplitBM * kW8SplitBN);
+      break;
+    }
+  }
+  return floats;
 }
 
 // Grid of the bf16 GEMM: work items (tile x K-split) for every row count the host cannot
@@ -985,39 +1045,59 @@ static void launch_pp(const void *A, int lda, const void *B, int ldb, int M, int
                      epi.mode == EPI_SWIGLU ? 2 * N : N, m_dev, epi);
 }
 
+// The 8-wave launch for one row-count range: the tile (and K split) every count in
+// [lo, M] picks, or -1 when they differ (the device then picks); any_split when some count
+// in the range splits K.
+struct W8Choice {
+  int choice;  // kernel index of w8_tile, 100 + splits for the split 192x128 tile, -1 mixed
+  bool any_split;
+};
+static W8Choice w8_choice(int M, int N, int K, const int32_t *m_dev, int mode,
+                          const float *part, int m_min) {
+  const int cus = gemm_cu_count();
+  auto at = [&](int m) {
+    const int sp = part ? w8_k_splits(m, N, K, mode, cus) : 1;
+    return sp > 1 ? 100 + sp : gemm_w8_tile(m, N, mode, cus);
+  };
+  W8Choice c{at(M), false};
+  c.any_split = c.choice >= 100;
+  if (m_dev) {
+    for (int m = std::max(m_min, 1); m < M; m = std::min(M, m + 16)) {
+      const int x = at(m);
+      c.any_split |= x >= 100;
+      if (x != c.choice) c.choice = -1;
+    }
+  }
+  if (c.any_split) c.choice = -1;  // the split launches go through the picking kernel
+  return c;
+}
+
 hipError_t launch_gemm(const void *A, int lda, const void *B, int ldb, int M, int N, int K,
                        const int32_t *m_dev, int dtype, const Epi &epi, hipStream_t s,
                        float *part, int m_min) {
   if (M == 0 || N == 0) return hipSuccess;
   if (dtype == AKVS_BF16) {
-    const GemmPlan p = gemm_plan(M, N, K, m_dev, epi, part, m_min);
     const size_t b_rows = epi.mode == EPI_SWIGLU ? 2 * (size_t)N : (size_t)N;
     // buffer offsets are 32-bit: larger operands stay on the 4-wave kernel
     const bool fits = (size_t)M * lda * 2 < (1u << 31) && b_rows * ldb * 2 < (1u << 31);
-    if (!p.any_split && fits) {
+    if (fits) {
       const int cus = gemm_cu_count();
-      int choice = gemm_w8_tile(M, N, epi.mode, cus);
-      if (m_dev) {
-        // a row count known only on the device: one static tile if every count the host
-        // cannot rule out picks it, else the launch that picks on the device
-        bool one = true;
-        for (int m = std::max(m_min, 1); m < M && one; m = std::min(M, m + 16))
-          one = gemm_w8_tile(m, N, epi.mode, cus) == choice;
-        if (!one) {
-          int grid = 0;
-          for (int i = 0; i < kW8Count; ++i) {
-            const W8Tile c = w8_tile(i);
-            const int bn_out = epi.mode == EPI_SWIGLU ? c.bn / 2 : c.bn;
-            grid = std::max(grid, ((M + c.bm - 1) / c.bm) * ((N + bn_out - 1) / bn_out));
-          }
-          hipLaunchKernelGGL(k_gemm_bf16_pick, dim3(grid), dim3(512), 0, s,
-                             reinterpret_cast<const bf16_t *>(A), lda,
-                             reinterpret_cast<const bf16_t *>(B), ldb, M, N, K,
-                             epi.mode == EPI_SWIGLU ? 2 * N : N, m_dev, epi, cus);
-          return hipGetLastError();
+      const W8Choice c = w8_choice(M, N, K, m_dev, epi.mode, part, m_min);
+      if (c.choice < 0) {
+        int grid = c.any_split ? cus : 0;
+        for (int i = 0; i < kW8Count; ++i) {
+          const W8Tile t = w8_tile(i);
+          const int bn_out = epi.mode == EPI_SWIGLU ? t.bn / 2 : t.bn;
+          grid = std::max(grid, ((M + t.bm - 1) / t.bm) * ((N + bn_out - 1) / bn_out));
         }
+        hipLaunchKernelGGL(k_gemm_bf16_pick, dim3(grid), dim3(512), 0, s,
+                           reinterpret_cast<const bf16_t *>(A), lda,
+                           reinterpret_cast<const bf16_t *>(B), ldb, M, N, K,
+                           epi.mode == EPI_SWIGLU ? 2 * N : N, m_dev, epi, cus,
+                           c.any_split ? part : nullptr);
+        return hipGetLastError();
       }
-      switch (choice) {
+      switch (c.choice) {
         case 0: launch_w8<256, 256, 2, 1>(A, lda, B, ldb, M, N, K, m_dev, epi, s); break;
         case 1: launch_pp<192, 256>(A, lda, B, ldb, M, N, K, m_dev, epi, s); break;
         case 2: launch_w8<256, 128, 4, 2>(A, lda, B, ldb, M, N, K, m_dev, epi, s); break;
@@ -1025,6 +1105,7 @@ hipError_t launch_gemm(const void *A, int lda, const void *B, int ldb, int M, in
       }
       return hipGetLastError();
     }
+    const GemmPlan p = gemm_plan(M, N, K, m_dev, epi, part, m_min);
     hipLaunchKernelGGL((k_gemm_bf16<128, false>), dim3(p.items), dim3(256), 0, s,
                        reinterpret_cast<const bf16_t *>(A), lda,
                        reinterpret_cast<const bf16_t *>(B), ldb, M, N, K, m_dev, epi, p.n_slots,
@@ -1039,14 +1120,25 @@ hipError_t launch_gemm(const void *A, int lda, const void *B, int ldb, int M, in
   return hipGetLastError();
 }
 
-hipError_t launch_gemm_fixup(const void *, int, const void *, int, int M, int N, int K,
+hipError_t launch_gemm_fixup(const void *, int lda, const void *, int ldb, int M, int N, int K,
                              const int32_t *m_dev, int dtype, const Epi &epi, hipStream_t s,
                              float *part, int m_min) {
   if (M == 0 || N == 0 || dtype != AKVS_BF16) return hipSuccess;
+  const size_t b_rows = epi.mode == EPI_SWIGLU ? 2 * (size_t)N : (size_t)N;
+  const bool fits = (size_t)M * lda * 2 < (1u << 31) && b_rows * ldb * 2 < (1u << 31);
+  if (fits) {
+    const W8Choice c = w8_choice(M, N, K, m_dev, epi.mode, part, m_min);
+    if (!c.any_split) return hipSuccess;
+    const int bn_out = epi.mode == EPI_SWIGLU ? kW8SplitBN / 2 : kW8SplitBN;
+    const int tiles = ((M + kW8SplitBM - 1) / kW8SplitBM) * ((N + bn_out - 1) / bn_out);
+    hipLaunchKernelGGL((k_gemm_fixup<kW8SplitBM, true>), dim3(tiles * (kW8SplitBM / G_FR)),
+                       dim3(256), 0, s, M, N, K, m_dev, epi, gemm_cu_count(), part);
+    return hipGetLastError();
+  }
   const GemmPlan p = gemm_plan(M, N, K, m_dev, epi, part, m_min);
   if (!p.any_split) return hipSuccess;
-  hipLaunchKernelGGL((k_gemm_fixup<128>), dim3(p.tiles_cap * (128 / G_FR)), dim3(256), 0, s, M,
-                     N, K, m_dev, epi, p.n_slots, part);
+  hipLaunchKernelGGL((k_gemm_fixup<128, false>), dim3(p.tiles_cap * (128 / G_FR)), dim3(256), 0, s,
+                     M, N, K, m_dev, epi, p.n_slots, part);
   return hipGetLastError();
 }
 
