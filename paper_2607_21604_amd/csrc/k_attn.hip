@@ -47,7 +47,79 @@ static inline AttnShape attn_shape(int G, int rows, int hkv) {
   return a;
 }
 
-// A block serves head group hg of KV head kvh: 32 * nrb query rows x gh query heads. Wave
+// Key split planned on the device (split launches of one-head 8-wave blocks): the host
+// knows only a bound on the row count, and how long the (row tile, key range) blocks of a
+// split count are depends on the live rows' positions. Wave 0 of every block derives the
+// same plan: the key range of tile t (rows sorted by position) ends at its last row's
+// position; each candidate count sp <= min(sp_max, 16) cuts the keys into ranges of
+// S = attn_split_keys keys, tile t taking ceil(keys_t / S) of them. Its cost, in keys: the
+// blocks in dispatch order fill rounds of `slots` blocks, each round costs its longest
+// block (keys + 512 for the block's fixed work), plus 32 per split for the merge; the
+// least cost wins, the smaller count on a tie (the model ranked the measured launch
+// sweeps of the 3B probe layers at r = 1/100 to 1/5 correctly). Items are ordered
+// tile-descending (longest first), splits ascending; item -> (tile, split, S, splits of
+// that tile) in s_plan, tile -1 past the last item. Needs tiles <= 64.
+__device__ __forceinline__ void attn_plan(int item, int R, int rb_rows, const int32_t *pos,
+                                          int pos0, int n_keys, int heads, int sp_max,
+                                          int slots, int lane, int *s_plan) {
+  const int nt = (R + rb_rows - 1) / rb_rows;
+  int keys = 0;
+  if (lane < nt) {
+    const int e = min((lane + 1) * rb_rows, R) - 1;
+    keys = min(n_keys, (pos ? pos[e] : pos0 + e) + 1);
+  }
+  const int sp = lane + 1;
+  const bool cand = sp <= min(sp_max, 16);
+  const int S = ((n_keys + sp - 1) / sp + 63) / 64 * 64;
+  // (32-bit counts: at most 64 tiles x 64 splits x heads blocks; no divisions in the loop)
+  int blk = 0, total = 0, round_end = slots;
+  int rmax = 0;  // longest block of the open round
+  for (int t = nt - 1; t >= 0; --t) {
+    const int k = __shfl(keys, t, 64);
+    if (!cand) continue;
+    for (int k0 = 0; k0 < k; k0 += S) {
+      const int d = min(S, k - k0) + 512;
+      if (blk >= round_end) {  // this item opens a new round
+        total += rmax;
+        rmax = 0;
+        round_end += slots;
+      }
+      rmax = max(rmax, d);
+      while (blk + heads - 1 >= round_end) {  // its blocks run on into the next round
+        total += rmax;
+        rmax = d;
+        round_end += slots;
+      }
+      blk += heads;
+    }
+  }
+  total += rmax;
+  long long key = 0x7fffffffffffffffLL;
+  if (cand) key = ((long long)total + 32LL * sp) * 64 + lane;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) key = min(key, __shfl_xor(key, o, 64));
+  const int best = (int)(key & 63);
+  const int Sb = __shfl(S, best, 64);
+  // lane j <-> tile nt - 1 - j: split count and inclusive prefix over the item order
+  const int kj = __shfl(keys, max(nt - 1 - lane, 0), 64);
+  const int c = lane < nt ? (kj + Sb - 1) / Sb : 0;
+  int incl = c;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int v = __shfl_up(incl, o, 64);
+    if (lane >= o) incl += v;
+  }
+  const int j = __popcll(__ballot(lane < nt && incl <= item));
+  const int cj = __shfl(c, min(j, 63), 64), ij = __shfl(incl, min(j, 63), 64);
+  if (lane == 0) {
+    s_plan[0] = j < nt ? nt - 1 - j : -1;
+    s_plan[1] = item - (ij - cj);
+    s_plan[2] = Sb;
+    s_plan[3] = cj;
+  }
+}
+
+// A block serves head group hg of KV head kvh: 32 * nrb query rows x gh query heads. Wave// A block serves head group hg of KV head kvh: 32 * nrb query rows x gh query heads. Wave
 // w owns 32 rows (row block w / gh) of query head kvh * G + hg * gh + w % gh. Waves 0-3
 // stage each 64-key K / V tile in LDS for all of them (double buffered, next tile
 // prefetched into registers during the current one). Block b serves KV head b % Hkv, so
@@ -60,7 +132,8 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
                                                    const bf16_t *__restrict__ Vc, int n_keys,
                                                    int hq, int hkv, int gh, int n_groups,
                                                    int nrb, int n_tiles, int n_splits,
-                                                   int split_keys, float scale_log2,
+                                                   int split_keys, int plan_slots,
+                                                   float scale_log2,
                                                    bf16_t *__restrict__ out,
                                                    bf16_t *__restrict__ part_o,
                                                    float *__restrict__ part_ml,
@@ -78,6 +151,7 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
   __shared__ __attribute__((aligned(16))) bf16_t Ks[2 * KBUF];
   __shared__ __attribute__((aligned(16))) bf16_t Vt[2 * VBUF];
   __shared__ int s_max[8];
+  __shared__ int s_plan[4];
   if (row_base) {  // this call's rows start at row *row_base of q, pos and out
     const int rb0 = *row_base;
     Q += (size_t)rb0 * hq * HD;
@@ -92,12 +166,24 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
   int rest = (int)(blockIdx.x / hkv);
   const int hg = rest % n_groups;
   rest /= n_groups;
-  const int split = rest % n_splits;
-  const int tile = n_tiles - 1 - rest / n_splits;
   const int head = kvh * G + hg * gh + wave % gh;
   int R = rows;
   if (rows_dev) R = min(R, *rows_dev);
   const int rb_rows = 32 * nrb;
+  int split, tile, n_part = n_splits;
+  if (plan_slots > 0) {  // key split planned here from the live rows (see attn_plan)
+    if (wave == 0)
+      attn_plan(rest, R, rb_rows, pos, pos0, n_keys, hkv * n_groups, n_splits, plan_slots, lane,
+                s_plan);
+    __syncthreads();
+    tile = s_plan[0];
+    split = s_plan[1];
+    split_keys = s_plan[2];
+    n_part = s_plan[3];
+  } else {
+    split = rest % n_splits;
+    tile = n_tiles - 1 - rest / n_splits;
+  }
   const int row0 = tile * rb_rows;
   if (tile < 0 || row0 >= R) return;
   const int hi = lane >> 5;  // which half of a row's 32 keys (and 32 dims) this lane holds
@@ -317,6 +403,11 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
     if (hi == 0) {
       part_ml[2 * prow] = m_run;
       part_ml[2 * prow + 1] = l_row;
+      if (split == n_part - 1 && n_part < n_splits) {  // end mark: no later split of this tile
+        const size_t pend = ((size_t)n_part * rows + r) * hq + head;
+        part_ml[2 * pend] = -INFINITY;
+        part_ml[2 * pend + 1] = -1.f;
+      }
     }
     return;
   }
@@ -334,7 +425,9 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
 // o_s (bf16, normalised by its own sum l_s), and (m_s, l_s); the result is
 // sum_s w_s o_s / sum_s w_s with w_s = 2^(m_s - max m) l_s, added in split order. A split
 // whose keys all lie past the row (causal mask) holds m = -inf and is skipped, never
-// multiplied in (its part_o slot holds whatever the workspace held).
+// multiplied in (its part_o slot holds whatever the workspace held). With a device-planned
+// split a tile may use fewer splits than the launch's count: l = -1 after its last one
+// ends the list (the slots past it are stale).
 // Thread = 8 consecutive head dims of one (row, head) (16-byte loads and stores). Up to 8
 // splits, all (m, l) pairs and partial outputs are requested at once; with more, the
 // maxima first, then the splits in order.
@@ -367,22 +460,31 @@ __global__ __launch_bounds__(256) void k_attn_combine(const bf16_t *__restrict__
         load8(part_o + pi * hd + e0, o[u]);
       }
     }
+    int n = n_splits;  // up to the first end mark
+#pragma unroll
+    for (int u = 7; u >= 0; --u)
+      if (u < n_splits && ml[u].y < 0.f) n = u;
 #pragma unroll
     for (int u = 0; u < 8; ++u)
-      if (u < n_splits) mx = fmaxf(mx, ml[u].x);
+      if (u < n) mx = fmaxf(mx, ml[u].x);
     const float moff = mx == -INFINITY ? 0.f : mx;
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
-      if (u >= n_splits || ml[u].x == -INFINITY) continue;
+      if (u >= n || ml[u].x == -INFINITY) continue;
       const float w = exp2f(ml[u].x - moff) * ml[u].y;
       l += w;
 #pragma unroll
       for (int i = 0; i < 8; ++i) a[i] += w * o[u][i];
     }
   } else {
-    for (int sp = 0; sp < n_splits; ++sp) mx = fmaxf(mx, part_ml[2 * (sp * stride + item)]);
+    int n = n_splits;  // up to the first end mark
+    for (int sp = 0; sp < n; ++sp) {
+      const float2 ml = *reinterpret_cast<const float2 *>(part_ml + 2 * (sp * stride + item));
+      if (ml.y < 0.f) n = sp;
+      else mx = fmaxf(mx, ml.x);
+    }
     const float moff = mx == -INFINITY ? 0.f : mx;
-    for (int sp = 0; sp < n_splits; ++sp) {
+    for (int sp = 0; sp < n; ++sp) {
       const size_t pi = sp * stride + item;
       const float2 ml = *reinterpret_cast<const float2 *>(part_ml + 2 * pi);
       if (ml.x == -INFINITY) continue;  // no visible key: its part_o was never written
@@ -493,19 +595,31 @@ hipError_t launch_attention(const void *q, const int32_t *pos, int pos0, int row
     const bf16_t *K = reinterpret_cast<const bf16_t *>(k);
     const bf16_t *V = reinterpret_cast<const bf16_t *>(v);
     bf16_t *O = reinterpret_cast<bf16_t *>(out);
-    const AttnShape a = attn_shape(hq / hkv, rows, hkv);
+    AttnShape a = attn_shape(hq / hkv, rows, hkv);
     if (a.gh == 0) return hipErrorInvalidValue;
-    const int rb = 32 * a.nrb;
-    const int n_tiles = (rows + rb - 1) / rb;
     int n_splits = part_o && part_ml ? attn_splits(rows, hq, hkv, n_keys) : 1;
     if ((long long)n_splits * rows > part_rows) n_splits = (int)std::max(1LL, part_rows / rows);
     const int split_keys = attn_split_keys(n_keys, n_splits);
+    // Split launches whose 128-row tiles alone leave CUs without a block: 8-wave blocks, the
+    // split count (<= n_splits) planned on the device. Where the 128-row tiles already
+    // give every CU one, their finer grain balances the causal ramp better (launch sweeps
+    // of the 3B probe layers: 79 against 83 us at r = 1/5; 65 against 78 us at r = 1/10
+    // and 35 against 48 us at r = 1/100 for the planned split).
+    int plan_slots = 0;
+    const int cus = gemm_cu_count();
+    if (n_splits > 1 && a.gh == 1 && (rows + 255) / 256 <= 64 &&
+        (long long)((rows + 127) / 128) * hkv * a.n_groups <= cus) {
+      a.nrb = 8;
+      plan_slots = cus;
+    }
+    const int n_tiles = (rows + 32 * a.nrb - 1) / (32 * a.nrb);
     dim3 g(n_tiles * hkv * a.n_groups * n_splits), b(64 * a.nrb * a.gh);
     const bool pref = a.nrb * a.gh <= 4;  // see PREF in the kernel
 #define AKVS_ATTN(HD_, PREF_)                                                                    \
   hipLaunchKernelGGL((k_attn_bf16<HD_, PREF_>), g, b, 0, s, Q, pos, pos0, rows, rows_dev, K, V,    \
                      n_keys, hq, hkv, a.gh, a.n_groups, a.nrb, n_tiles, n_splits, split_keys,      \
-                     scale_log2, O, reinterpret_cast<bf16_t *>(part_o), part_ml, row_base)
+                     plan_slots, scale_log2, O, reinterpret_cast<bf16_t *>(part_o), part_ml,      \
+                     row_base)
     if (hd == 128) {
       if (pref) AKVS_ATTN(128, true); else AKVS_ATTN(128, false);
     } else {

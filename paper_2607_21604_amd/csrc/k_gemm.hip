@@ -774,9 +774,9 @@ __host__ __device__ inline int gemm_w8_tile(int M, int N, int mode, int cus) {
 
 // K split of the 192x128 8-wave tile for row counts whose tiles would leave at least half of
 // the CUs idle (probe layers at small refresh ratios, the query rows of the last layer):
-// about one round of (tile, k-slice) items, slices of at least 16 k-tiles, at most 8 per
+// about one round of (tile, k-slice) items, slices of at least 8 k-tiles, at most 12 per
 // tile; k_gemm_fixup adds the slices in order. (At 810 rows of the 3B shape the output and
-// down projections make 120 such tiles for 256 CUs.)
+// down projections make 120 such tiles for 256 CUs; at 171 rows 24.)
 constexpr int kW8SplitBM = 192, kW8SplitBN = 128;
 __host__ __device__ inline int w8_k_splits(int M, int N, int K, int mode, int cus) {
   const int bn_out = mode == EPI_SWIGLU ? kW8SplitBN / 2 : kW8SplitBN;
@@ -784,8 +784,8 @@ __host__ __device__ inline int w8_k_splits(int M, int N, int K, int mode, int cu
   const int nk = K / GB_K;
   if (tiles <= 0 || 2 * tiles > cus || nk < 32) return 1;
   int sp = cus / tiles;
-  if (sp > nk / 16) sp = nk / 16;
-  if (sp > 8) sp = 8;
+  if (sp > nk / 8) sp = nk / 8;
+  if (sp > 12) sp = 12;
   return sp < 2 ? 1 : sp;
 }
 
