@@ -60,6 +60,17 @@ def test_3b_full_sequence_reuse_prefill(full3b):
     print("3b full sequence", {k: f"{v:.2e}" for k, v in errs.items()})
 
 
+@pytest.mark.parametrize("refresh", [(1, 100), (1, 10)])
+def test_3b_full_sequence_low_refresh(full3b, refresh):
+    """Small probe sets (171 and about 810 recomputed rows): the probe layer's attention
+    runs the key split planned on the device from the live rows (8-wave blocks, per-tile
+    split counts with end marks for the merge)."""
+    c = full3b
+    ref = c.oracle(refresh=refresh)
+    errs = c.compare(c.gpu(refresh=refresh, probes=(ref["probe_k"], ref["probe_v"])), ref)
+    print("3b full sequence r=%d/%d" % refresh, {k: f"{v:.2e}" for k, v in errs.items()})
+
+
 def test_3b_full_sequence_full_prefill_bf16(full3b):
     """akvs_full_prefill (the speedup's denominator) against the oracle at bf16, 3 layers,
     every layer's keys and values and the final states of every row."""
