@@ -539,7 +539,11 @@ __device__ __forceinline__ void unpack_bf8(u32x4_t w, float (&o)[8]) {
     o[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
   }
 }
-template <typename TS>
+// SIMPLE: the reuse call's own case (bf16 unit cache, per-token unit and shift tables, every
+// table present and valid, a fresh row for every recomputed position, neither
+// AKVS_F_PRE_ROPE_OFFSETS nor AKVS_F_FRESH_IF_RECOMPUTED, no fresh-row base), with those
+// checks taken out at compile time.
+template <typename TS, bool SIMPLE>
 __global__ __launch_bounds__(256) void k_correction_bf(CacheLayer cache, const float *mu_k,
                                                        const float *mu_v, const float *w_k,
                                                        const float *w_v, const uint8_t *tok_flags,
@@ -556,7 +560,7 @@ __global__ __launch_bounds__(256) void k_correction_bf(CacheLayer cache, const f
                                                        const int32_t *fresh_base) {
   const int half = hd >> 1;
   const int side_units = hkv * (half >> 3);  // threads per side and position
-  const int fresh_off = fresh_base ? *fresh_base : 0;
+  const int fresh_off = (!SIMPLE && fresh_base) ? *fresh_base : 0;
   const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
   const long long grp = gid / (2 * side_units);
   int u = (int)(gid - grp * 2 * side_units);
@@ -571,11 +575,11 @@ __global__ __launch_bounds__(256) void k_correction_bf(CacheLayer cache, const f
   // bookkeeping first, all of it at once (the row index of a recomputed position is read
   // whether or not the position is one), then only the rows this side uses: the cache row
   // of a reused token or the fresh row of a recomputed one
-  const uint8_t f = unit_tok ? (tok_flags ? tok_flags[t] : 0) : 3;
-  int fr = fresh_row ? fresh_row[t] : -1;
+  const uint8_t f = unit_tok ? ((SIMPLE || tok_flags) ? tok_flags[t] : 0) : 3;
+  int fr = (SIMPLE || fresh_row) ? fresh_row[t] : -1;
   int chunk = 0, delta = 0;
   if (unit_tok) {
-    if (tok_chunk) {
+    if (SIMPLE || tok_chunk) {
       chunk = tok_chunk[t];
       delta = tok_delta[t];
     } else if (meta) {
@@ -585,15 +589,15 @@ __global__ __launch_bounds__(256) void k_correction_bf(CacheLayer cache, const f
       delta = tok_delta[t];
     }
     if (delta < 0 || delta >= rope_rows) delta = 0;
-    if (chunk < 0 || chunk >= n_chunks) chunk = 0;
+    if (!SIMPLE && (chunk < 0 || chunk >= n_chunks)) chunk = 0;
   }
-  const bool any = f != 0 && (flags & AKVS_F_FRESH_IF_RECOMPUTED);
+  const bool any = !SIMPLE && f != 0 && (flags & AKVS_F_FRESH_IF_RECOMPUTED);
   const bool fresh = (vside ? (f & 2) : (f & 1)) || any;
-  if (fr >= 0) fr += fresh_off;
+  if (!SIMPLE && fr >= 0) fr += fresh_off;
   float lo[8], hi[8];
   if (fresh) {
-    if (fr >= 0) {
-      const TS *src = (vside ? v_fresh : k_fresh) + ((size_t)fr * hkv + h) * hd;
+    if (SIMPLE || fr >= 0) {  // (the reuse call gives every recomputed position its row)
+      const TS *src = (vside ? v_fresh : k_fresh) + ((size_t)max(fr, 0) * hkv + h) * hd;
       load8(src + e0, lo);
       load8(src + e0 + half, hi);
     } else {
@@ -601,7 +605,7 @@ __global__ __launch_bounds__(256) void k_correction_bf(CacheLayer cache, const f
       for (int i = 0; i < 8; ++i) lo[i] = hi[i] = 0.f;
     }
   } else {
-    if (cache.dtype == AKVS_BF16) {
+    if (SIMPLE || cache.dtype == AKVS_BF16) {
       const bf16_t *cb = reinterpret_cast<const bf16_t *>(vside ? cache.v : cache.k) + orow * hd;
       unpack_bf8(__builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(cb + e0)), lo);
       unpack_bf8(__builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(cb + e0 + half)),
@@ -614,16 +618,16 @@ __global__ __launch_bounds__(256) void k_correction_bf(CacheLayer cache, const f
     }
     const float *mu = vside ? mu_v : mu_k;
     const size_t mo = (size_t)chunk * hkv * hd + (size_t)h * hd;
-    const float w = mu ? (vside ? w_v[t] : w_k[t]) : 0.f;
+    const float w = (SIMPLE || mu) ? (vside ? w_v[t] : w_k[t]) : 0.f;
     if (!vside) {
-      const float2 *mu_rot = (flags & AKVS_F_PRE_ROPE_OFFSETS)
+      const float2 *mu_rot = (!SIMPLE && (flags & AKVS_F_PRE_ROPE_OFFSETS))
                                  ? rope + (size_t)min(t, rope_rows - 1) * half
                                  : nullptr;
       corr_finish(false, -1, k_fresh, hkv, h, hd, e0, rope + (size_t)delta * half,
-                  mu ? mu + mo : nullptr, w, lo, hi, mu_rot);
+                  (SIMPLE || mu) ? mu + mo : nullptr, w, lo, hi, mu_rot);
     } else {
-      corr_finish(false, -1, v_fresh, hkv, h, hd, e0, nullptr, mu ? mu + mo : nullptr, w, lo,
-                  hi);
+      corr_finish(false, -1, v_fresh, hkv, h, hd, e0, nullptr, (SIMPLE || mu) ? mu + mo : nullptr,
+                  w, lo, hi);
     }
   }
   // streaming stores: the corrected rows are written once here (0.58 -> 0.64 of the HBM
@@ -661,14 +665,23 @@ hipError_t launch_correction(CacheLayer cache, const float *mu_k, const float *m
   if (cache.dtype != AKVS_F32 && CORR_T == 1) {
     const long long thr2 = (long long)t_all * 2 * hkv * (hd / 16);
     g = dim3((unsigned)((thr2 + 255) / 256));
-    if (out_dtype == AKVS_BF16)
-      hipLaunchKernelGGL(k_correction_bf<bf16_t>, g, b, 0, s, cache, mu_k, mu_v, w_k, w_v,
+    const bool simple = cache.dtype == AKVS_BF16 && tok_flags && fresh_row && tok_chunk &&
+                        tok_delta && mu_k && mu_v && w_k && w_v && !fresh_base &&
+                        !(flags & (AKVS_F_PRE_ROPE_OFFSETS | AKVS_F_FRESH_IF_RECOMPUTED));
+    if (out_dtype == AKVS_BF16 && simple)
+      hipLaunchKernelGGL((k_correction_bf<bf16_t, true>), g, b, 0, s, cache, mu_k, mu_v, w_k, w_v,
+                         tok_flags, as<bf16_t>(k_fresh), as<bf16_t>(v_fresh), fresh_row,
+                         tok_chunk, tok_delta, m4, n_chunks, t_ctx, t_all, hkv, hd, flags, r,
+                         rope_rows, reinterpret_cast<bf16_t *>(k_corr),
+                         reinterpret_cast<bf16_t *>(v_corr), fresh_base);
+    else if (out_dtype == AKVS_BF16)
+      hipLaunchKernelGGL((k_correction_bf<bf16_t, false>), g, b, 0, s, cache, mu_k, mu_v, w_k, w_v,
                          tok_flags, as<bf16_t>(k_fresh), as<bf16_t>(v_fresh), fresh_row,
                          tok_chunk, tok_delta, m4, n_chunks, t_ctx, t_all, hkv, hd, flags, r,
                          rope_rows, reinterpret_cast<bf16_t *>(k_corr),
                          reinterpret_cast<bf16_t *>(v_corr), fresh_base);
     else
-      hipLaunchKernelGGL(k_correction_bf<float>, g, b, 0, s, cache, mu_k, mu_v, w_k, w_v,
+      hipLaunchKernelGGL((k_correction_bf<float, false>), g, b, 0, s, cache, mu_k, mu_v, w_k, w_v,
                          tok_flags, as<float>(k_fresh), as<float>(v_fresh), fresh_row, tok_chunk,
                          tok_delta, m4, n_chunks, t_ctx, t_all, hkv, hd, flags, r, rope_rows,
                          reinterpret_cast<float *>(k_corr), reinterpret_cast<float *>(v_corr),
