@@ -2,7 +2,7 @@
 //
 // bf16 path: one block = a group of the query heads that read one KV head, over a tile of
 // rows; each wave owns 32 rows of one query head. Keys stream through LDS in tiles of 64
-// (K row-major, V transposed), shared by every wave of the block. Scores are computed
+// (K and V row-major), shared by every wave of the block. Scores are computed
 // transposed, S^T = K Q^T, with MFMA 32x32x16 bf16: each lane then holds 16 scores of ONE
 // query row (the other 16 of that row's 32 keys sit in lane ^ 32), and the probabilities
 // already sit in the operand layout of the second product O^T = V^T P^T (the pairing of
@@ -15,14 +15,16 @@
 
 namespace akvs {
 
-// V^T tile: row r = head dim, 64 keys in 16 groups of 4 (8 bytes), rows padded to 72
-// elements (144 bytes, a 4-bank shift per row). Group g of row r sits at column
-// (g ^ ((r >> 3) & 1)) * 4: the one-bit swizzle separates rows r and r + 8, so 16 lanes
-// reading 16 consecutive rows at one group, or writing 16 groups of one row, touch 32
-// distinct banks; and since it only flips bit 0 of the group, a lane's reads of groups
-// 4t + c (c < 4) are one base address plus compile-time offsets.
-constexpr int VT_ST = 72;
-__device__ __forceinline__ int vt_col(int r, int g) { return (g ^ ((r >> 3) & 1)) * 4; }
+// V tile: 64 keys x hd, row-major as in memory, rows padded by 32 elements (64 bytes, a
+// 16-bank shift per row). The P.V operand wants, per lane, 8 keys of ONE head dim; gfx950's
+// transposing LDS read (ds_read_b64_tr_b16) delivers that from row-major rows: within
+// each 16-lane group, lane j receives element j % 4 of the 8-byte chunk addressed by lane
+// 4k + j / 4, for k = 0..3. So source lane s of a group points at key row +s/4, head dims
+// 4*(s%4)..+3 of the group's 16 dims, and each lane gets 4 consecutive keys of its dim per
+// read. Against the transposed V^T staging it replaced (VALU byte shuffles and 8-byte LDS
+// stores in the loading waves), same bits: 1-4 % faster on the 32B, 7B and 3B shapes
+// (standalone timing, not in the repository). A 32-lane read phase touches 4 rows x 64
+// bytes, at 16-bank offsets: no conflicts.
 
 // Block shape: one query head per block, 32-row waves. With about 200 VGPRs (250 for the
 // read-ahead variant) a compute unit holds eight waves, so blocks of 8 waves (one per unit)
@@ -141,13 +143,11 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
   constexpr int KS = HD / 16;          // contraction steps of S
   constexpr int DB = HD / 32;          // 32-wide head-dim blocks of O
   constexpr int KST = HD + 8;          // K tile row stride (bf16)
-  constexpr int VST = VT_ST;           // V^T tile row stride (bf16), swizzled by vt_col
+  constexpr int VRS = HD + 32;         // V tile row stride (bf16)
   constexpr int CPK = HD / 8;          // 16-byte chunks per key row
   constexpr int LT = 256;              // loading threads (waves 0-3)
-  constexpr int KCH = 64 * CPK / LT;   // K chunks per loading thread
-  constexpr int VKEYS = 64 * CPK / LT; // keys per loading thread in the V transpose
-  constexpr int VQ = 64 / VKEYS;       // key groups per tile in the V transpose
-  constexpr int KBUF = 64 * KST, VBUF = HD * VST;
+  constexpr int KCH = 64 * CPK / LT;   // K (and V) chunks per loading thread
+  constexpr int KBUF = 64 * KST, VBUF = 64 * VRS;
   __shared__ __attribute__((aligned(16))) bf16_t Ks[2 * KBUF];
   __shared__ __attribute__((aligned(16))) bf16_t Vt[2 * VBUF];
   __shared__ int s_max[8];
@@ -233,21 +233,15 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
 
   // One K / V tile in the loading waves' registers. Keys past kv_end are clamped to the
   // last key: finite data that the score mask gives probability 0.
-  u32x4_t kreg[KCH], vreg[VKEYS];
-  // V: keys vkg*VKEYS.., dims ve0..; the 16 (32) lanes of an LDS write phase share ve0
-  const int vkg = tid % VQ, ve0 = (tid / VQ) * 8;
+  u32x4_t kreg[KCH], vreg[KCH];
   const int klast = kv_end - 1;
-  const int vsw = (hi ^ (((lane & 31) >> 3) & 1)) * 4;  // this lane's swizzled column offset
 #define AKVS_KV_LOAD(KEY0)                                                                  \
   {                                                                                         \
     _Pragma("unroll") for (int i = 0; i < KCH; ++i) {                                       \
       const int c = tid + LT * i, kr = c / CPK, e0 = (c - kr * CPK) * 8;                    \
-      const int key = min((KEY0) + kr, klast);                                              \
-      kreg[i] = *reinterpret_cast<const u32x4_t *>(Kc + ((size_t)key * hkv + kvh) * HD + e0); \
-    }                                                                                       \
-    _Pragma("unroll") for (int j = 0; j < VKEYS; ++j) {                                     \
-      const int key = min((KEY0) + vkg * VKEYS + j, klast);                                 \
-      vreg[j] = *reinterpret_cast<const u32x4_t *>(Vc + ((size_t)key * hkv + kvh) * HD + ve0); \
+      const size_t o_ = ((size_t)min((KEY0) + kr, klast) * hkv + kvh) * HD + e0;            \
+      kreg[i] = *reinterpret_cast<const u32x4_t *>(Kc + o_);                                \
+      vreg[i] = *reinterpret_cast<const u32x4_t *>(Vc + o_);                                \
     }                                                                                       \
   }
 #define AKVS_KV_STORE(BUFI)                                                                 \
@@ -257,26 +251,7 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
     _Pragma("unroll") for (int i = 0; i < KCH; ++i) {                                       \
       const int c = tid + LT * i, kr = c / CPK, e0 = (c - kr * CPK) * 8;                    \
       *reinterpret_cast<u32x4_t *>(ks_ + kr * KST + e0) = kreg[i];                          \
-    }                                                                                       \
-    _Pragma("unroll") for (int d = 0; d < 8; ++d) {                                         \
-      const int word = d >> 1;                                                              \
-      const bool hi_ = (d & 1) != 0;                                                        \
-      if (VKEYS >= 4) {                                                                     \
-        _Pragma("unroll") for (int qd = 0; qd < VKEYS / 4; ++qd) {                         \
-          const uint32_t a0 = vreg[4 * qd][word], a1 = vreg[4 * qd + 1][word];              \
-          const uint32_t a2 = vreg[4 * qd + 2][word], a3 = vreg[4 * qd + 3][word];          \
-          uint2 v2;                                                                         \
-          v2.x = hi_ ? ((a0 >> 16) | (a1 & 0xffff0000u)) : ((a0 & 0xffffu) | (a1 << 16));  \
-          v2.y = hi_ ? ((a2 >> 16) | (a3 & 0xffff0000u)) : ((a2 & 0xffffu) | (a3 << 16));  \
-          *reinterpret_cast<uint2 *>(vt_ + (ve0 + d) * VST +                                \
-                                     vt_col(ve0 + d, vkg * (VKEYS / 4) + qd)) = v2;         \
-        }                                                                                   \
-      } else {                                                                              \
-        const uint32_t a0 = vreg[0][word], a1 = vreg[VKEYS > 1 ? 1 : 0][word];              \
-        *reinterpret_cast<uint32_t *>(vt_ + (ve0 + d) * VST + vt_col(ve0 + d, vkg >> 1) +     \
-                                      (vkg & 1) * 2) =                                      \
-            hi_ ? ((a0 >> 16) | (a1 & 0xffff0000u)) : ((a0 & 0xffffu) | (a1 << 16));        \
-      }                                                                                     \
+      *reinterpret_cast<u32x4_t *>(vt_ + kr * VRS + e0) = vreg[i];                          \
     }                                                                                       \
   }
 
@@ -306,13 +281,21 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
     for (int st = 0; st < 2; ++st) {
       const int sk0 = key0 + st * 32;
       if (sk0 <= wmax) {  // skip keys past every row of this wave
-        // V^T fragments of this block: groups kg and kg + 2 of row db*32 + lane%32, at
-        // vt_col = (st*8 + 4t (+2)) * 4 + vsw
+        // V^T operand of k-step t, head-dim block db: lane holds dim db*32 + lane%32 at the
+        // keys of its 8 slots (slots 0-3: 16t + 4*hi + 0..3 of this 32-key block, 4-7: the
+        // same + 8), two transposing reads of 4 keys each
         bf16x8_t vf[2][DB];
         auto read_v = [&](int t, int db) {
-          const bf16_t *vrow = vt_ + (db * 32 + (lane & 31)) * VST + vsw;
-          const uint2 x0 = *reinterpret_cast<const uint2 *>(vrow + (st * 8 + 4 * t) * 4);
-          const uint2 x1 = *reinterpret_cast<const uint2 *>(vrow + (st * 8 + 4 * t + 2) * 4);
+          typedef short v4s __attribute__((ext_vector_type(4)));
+          const bf16_t *vb = vt_ + (st * 32 + 16 * t + 4 * hi + ((lane & 15) >> 2)) * VRS +
+                             db * 32 + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+          const v4s r0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (__attribute__((address_space(3))) v4s *)(vb));
+          const v4s r1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (__attribute__((address_space(3))) v4s *)(vb + 8 * VRS));
+          uint2 x0, x1;
+          __builtin_memcpy(&x0, &r0, 8);
+          __builtin_memcpy(&x1, &r1, 8);
           uint32_t vw[4] = {x0.x, x0.y, x1.x, x1.y};
           __builtin_memcpy(&vf[t][db], vw, 16);
         };
