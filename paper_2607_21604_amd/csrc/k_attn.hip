@@ -147,9 +147,14 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
   constexpr int CPK = HD / 8;          // 16-byte chunks per key row
   constexpr int LT = 256;              // loading threads (waves 0-3)
   constexpr int KCH = 64 * CPK / LT;   // K (and V) chunks per loading thread
-  constexpr int KBUF = 64 * KST, VBUF = 64 * VRS;
-  __shared__ __attribute__((aligned(16))) bf16_t Ks[2 * KBUF];
-  __shared__ __attribute__((aligned(16))) bf16_t Vt[2 * VBUF];
+  // DIR: the tiles go from global memory straight into LDS (8-wave blocks, hd 128)
+  constexpr bool DIR = !PREF && HD == 128;
+  constexpr int KBUF = DIR ? 64 * HD : 64 * KST, VBUF = DIR ? 64 * HD : 64 * VRS;
+  // the two buffers of a tile pair; with DIR separate LDS objects (see the loop below)
+  __shared__ __attribute__((aligned(16))) bf16_t Ks[(DIR ? 1 : 2) * KBUF];
+  __shared__ __attribute__((aligned(16))) bf16_t Vt[(DIR ? 1 : 2) * VBUF];
+  __shared__ __attribute__((aligned(16))) bf16_t Ks1[DIR ? KBUF : 1];
+  __shared__ __attribute__((aligned(16))) bf16_t Vt1[DIR ? VBUF : 1];
   __shared__ int s_max[8];
   __shared__ int s_plan[4];
   if (row_base) {  // this call's rows start at row *row_base of q, pos and out
@@ -233,8 +238,34 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
 
   // One K / V tile in the loading waves' registers. Keys past kv_end are clamped to the
   // last key: finite data that the score mask gives probability 0.
-  u32x4_t kreg[KCH], vreg[KCH];
+  u32x4_t kreg[DIR ? 1 : KCH], vreg[DIR ? 1 : KCH];
   const int klast = kv_end - 1;
+  // DIR staging: global_load_lds, 16 bytes per lane, the 64 lanes of a loading wave filling
+  // 1 KB = 4 unpadded rows of 256 bytes (lane p: row +p/16, 16-byte chunk position p%16).
+  // Which global chunk a lane fetches sets the layout: chunk c of row r sits at position
+  // c ^ (r & 15) for K and c ^ 4 (r & 3) for V, so that the 32 K rows of a fragment read
+  // and the 4 V rows of a transposing read fall on distinct banks. No registers, no LDS
+  // stores in the loading waves: 4.7 % faster on the 32B probe layer (986 -> 940 us), same
+  // bits (standalone harness, not in the repository). On the 4-wave blocks with read-ahead
+  // it was 20-27 % slower (their first transposing read follows the DMA at once, and the
+  // compiler, unable to tell it from the DMA's LDS writes, waits there for the DMA).
+  auto dma_to = [&](int key0_, bf16_t *kbuf, bf16_t *vbuf) {
+    const int w = tid >> 6;  // loading wave 0..3
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = (i * 4 + w) * 4 + (lane >> 4);
+      const int pc = lane & 15;
+      const size_t gro = ((size_t)min(key0_ + row, klast) * hkv + kvh) * HD;
+      __builtin_amdgcn_global_load_lds((const void *)(Kc + gro + (pc ^ (row & 15)) * 8),
+                                       (__attribute__((address_space(3))) void *)(
+                                           kbuf + (i * 4 + w) * 4 * HD),
+                                       16, 0, 0);
+      __builtin_amdgcn_global_load_lds((const void *)(Vc + gro + (pc ^ (4 * (row & 3))) * 8),
+                                       (__attribute__((address_space(3))) void *)(
+                                           vbuf + (i * 4 + w) * 4 * HD),
+                                       16, 0, 0);
+    }
+  };
 #define AKVS_KV_LOAD(KEY0)                                                                  \
   {                                                                                         \
     _Pragma("unroll") for (int i = 0; i < KCH; ++i) {                                       \
@@ -244,10 +275,10 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
       vreg[i] = *reinterpret_cast<const u32x4_t *>(Vc + o_);                                \
     }                                                                                       \
   }
-#define AKVS_KV_STORE(BUFI)                                                                 \
+#define AKVS_KV_STORE(KB, VB)                                                               \
   {                                                                                         \
-    bf16_t *ks_ = Ks + (BUFI) * KBUF;                                                       \
-    bf16_t *vt_ = Vt + (BUFI) * VBUF;                                                       \
+    bf16_t *ks_ = (KB);                                                                     \
+    bf16_t *vt_ = (VB);                                                                     \
     _Pragma("unroll") for (int i = 0; i < KCH; ++i) {                                       \
       const int c = tid + LT * i, kr = c / CPK, e0 = (c - kr * CPK) * 8;                    \
       *reinterpret_cast<u32x4_t *>(ks_ + kr * KST + e0) = kreg[i];                          \
@@ -255,17 +286,25 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
     }                                                                                       \
   }
 
-  if (loader) {
+  if (DIR) {
+    if (loader) dma_to(kv_begin, Ks, Vt);
+    __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
+  } else if (loader) {
     AKVS_KV_LOAD(kv_begin);
-    AKVS_KV_STORE(0);
+    AKVS_KV_STORE(Ks, Vt);
   }
   __syncthreads();
-  for (int kt = 0; kt < nkt; ++kt) {
+  // one 64-key tile from ks_ / vt_, the next one staged into nks_ / nvt_
+  auto step = [&](int kt, const bf16_t *ks_in, const bf16_t *vt_in, bf16_t *nks_,
+                  bf16_t *nvt_) __attribute__((always_inline)) {
+    const bf16_t *ks_ = DIR ? ks_in : Ks + (kt & 1) * KBUF;
+    const bf16_t *vt_ = DIR ? vt_in : Vt + (kt & 1) * VBUF;
     const int key0 = kv_begin + kt * 64;
     const bool more = kt + 1 < nkt;
-    if (loader && more) AKVS_KV_LOAD(key0 + 64);
-    const bf16_t *ks_ = Ks + (kt & 1) * KBUF;
-    const bf16_t *vt_ = Vt + (kt & 1) * VBUF;
+    if (loader && more) {
+      if (DIR) dma_to(key0 + 64, nks_, nvt_);
+      else AKVS_KV_LOAD(key0 + 64);
+    }
     // PREF: the K fragments of a 32-key block are read ahead (the tile's first block here,
     // its second under the first block's softmax) and each block's V^T fragments are
     // requested before its score MFMAs, so no MFMA waits on its own LDS read. It needs about
@@ -276,6 +315,7 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
       const bf16_t *krow = ks_ + (lane & 31) * KST + hi * 8;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) kf[ks] = *reinterpret_cast<const bf16x8_t *>(krow + ks * 16);
+      static_assert(!DIR || !PREF, "the read-ahead reads the padded K layout");
     }
 #pragma unroll
     for (int st = 0; st < 2; ++st) {
@@ -287,12 +327,18 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
         bf16x8_t vf[2][DB];
         auto read_v = [&](int t, int db) {
           typedef short v4s __attribute__((ext_vector_type(4)));
-          const bf16_t *vb = vt_ + (st * 32 + 16 * t + 4 * hi + ((lane & 15) >> 2)) * VRS +
-                             db * 32 + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+          // DIR: the 16-byte chunk db*4 + 2*((lane>>4)&1) + (lane&3)/2 of a row whose low two
+          // bits are (lane>>2)&3 sits at db ^ ((lane>>2)&3) in place of db
+          const bf16_t *vb =
+              DIR ? vt_ + (st * 32 + 16 * t + 4 * hi + ((lane & 15) >> 2)) * HD +
+                        (4 * (db ^ ((lane >> 2) & 3)) + 2 * ((lane >> 4) & 1) + ((lane & 3) >> 1)) * 8 +
+                        (lane & 1) * 4
+                  : vt_ + (st * 32 + 16 * t + 4 * hi + ((lane & 15) >> 2)) * VRS + db * 32 +
+                        16 * ((lane >> 4) & 1) + 4 * (lane & 3);
           const v4s r0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
               (__attribute__((address_space(3))) v4s *)(vb));
           const v4s r1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              (__attribute__((address_space(3))) v4s *)(vb + 8 * VRS));
+              (__attribute__((address_space(3))) v4s *)(vb + 8 * (DIR ? HD : VRS)));
           uint2 x0, x1;
           __builtin_memcpy(&x0, &r0, 8);
           __builtin_memcpy(&x1, &r1, 8);
@@ -309,11 +355,16 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
         f32x16_t sc;
 #pragma unroll
         for (int i = 0; i < 16; ++i) sc[i] = 0.f;
-        const bf16_t *krow = ks_ + (st * 32 + (lane & 31)) * KST + hi * 8;
+        // K fragment of step ks: 16-byte chunk 2ks + hi of row st*32 + lane%32 (DIR: at its
+        // swizzled position; st*32 is a multiple of 16, so the row's low bits are lane%16)
+        const bf16_t *krow =
+            ks_ + (st * 32 + (lane & 31)) * (DIR ? HD : KST) + (DIR ? 0 : hi * 8);
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
           const bf16x8_t a =
-              PREF ? kf[ks] : *reinterpret_cast<const bf16x8_t *>(krow + ks * 16);
+              PREF ? kf[ks]
+                   : *reinterpret_cast<const bf16x8_t *>(
+                         krow + (DIR ? ((2 * ks + hi) ^ (lane & 15)) * 8 : ks * 16));
           sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ks], sc, 0, 0, 0);
         }
         if (PREF && st == 0 && sk0 + 32 <= wmax) {
@@ -366,8 +417,144 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
         }
       }
     }
-    if (loader && more) AKVS_KV_STORE((kt + 1) & 1);
+    if (DIR) __builtin_amdgcn_s_waitcnt(0x0f70);  // this wave's DMA of the next tile landed
+    else if (loader && more) AKVS_KV_STORE(Ks + ((kt + 1) & 1) * KBUF, Vt + ((kt + 1) & 1) * VBUF);
     __syncthreads();
+  };
+  if constexpr (DIR) {
+    // unrolled by two over separate LDS objects, so that the compiler can see that a
+    // step's reads and the next tile's DMA touch different memory and does not wait for
+    // the DMA before the reads
+    for (int kt = 0; kt < nkt; kt += 2) {
+      step(kt, Ks, Vt, Ks1, Vt1);
+      if (kt + 1 < nkt) step(kt + 1, Ks1, Vt1, Ks, Vt);
+    }
+  } else {
+    // (the same step written out in the loop: as a lambda it cost the read-ahead variant
+    // two spilled registers)
+    for (int kt = 0; kt < nkt; ++kt) {
+    const bf16_t *ks_ = Ks + (kt & 1) * KBUF;
+    const bf16_t *vt_ = Vt + (kt & 1) * VBUF;
+    const int key0 = kv_begin + kt * 64;
+    const bool more = kt + 1 < nkt;
+    if (loader && more) {
+      AKVS_KV_LOAD(key0 + 64);
+    }
+    // PREF: the K fragments of a 32-key block are read ahead (the tile's first block here,
+    // its second under the first block's softmax) and each block's V^T fragments are
+    // requested before its score MFMAs, so no MFMA waits on its own LDS read. It needs about
+    // 50 more registers; measured 4 % faster on the four-wave 128-row blocks (3B and 7B
+    // probe layers) and 2 % slower on the eight-wave 256-row blocks (32B probe layer).
+    bf16x8_t kf[KS];
+    if (PREF && key0 <= wmax) {
+      const bf16_t *krow = ks_ + (lane & 31) * KST + hi * 8;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) kf[ks] = *reinterpret_cast<const bf16x8_t *>(krow + ks * 16);
+      static_assert(!DIR || !PREF, "the read-ahead reads the padded K layout");
+    }
+#pragma unroll
+    for (int st = 0; st < 2; ++st) {
+      const int sk0 = key0 + st * 32;
+      if (sk0 <= wmax) {  // skip keys past every row of this wave
+        // V^T operand of k-step t, head-dim block db: lane holds dim db*32 + lane%32 at the
+        // keys of its 8 slots (slots 0-3: 16t + 4*hi + 0..3 of this 32-key block, 4-7: the
+        // same + 8), two transposing reads of 4 keys each
+        bf16x8_t vf[2][DB];
+        auto read_v = [&](int t, int db) {
+          typedef short v4s __attribute__((ext_vector_type(4)));
+          // DIR: the 16-byte chunk db*4 + 2*((lane>>4)&1) + (lane&3)/2 of a row whose low two
+          // bits are (lane>>2)&3 sits at db ^ ((lane>>2)&3) in place of db
+          const bf16_t *vb =
+              DIR ? vt_ + (st * 32 + 16 * t + 4 * hi + ((lane & 15) >> 2)) * HD +
+                        (4 * (db ^ ((lane >> 2) & 3)) + 2 * ((lane >> 4) & 1) + ((lane & 3) >> 1)) * 8 +
+                        (lane & 1) * 4
+                  : vt_ + (st * 32 + 16 * t + 4 * hi + ((lane & 15) >> 2)) * VRS + db * 32 +
+                        16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+          const v4s r0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (__attribute__((address_space(3))) v4s *)(vb));
+          const v4s r1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (__attribute__((address_space(3))) v4s *)(vb + 8 * (DIR ? HD : VRS)));
+          uint2 x0, x1;
+          __builtin_memcpy(&x0, &r0, 8);
+          __builtin_memcpy(&x1, &r1, 8);
+          uint32_t vw[4] = {x0.x, x0.y, x1.x, x1.y};
+          __builtin_memcpy(&vf[t][db], vw, 16);
+        };
+        if (PREF) {
+#pragma unroll
+          for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int db = 0; db < DB; ++db) read_v(t, db);
+        }
+        // S^T block: 32 keys x 32 rows; s[i] is key sk0 + (i/4)*8 + hi*4 + i%4 of row r
+        f32x16_t sc;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) sc[i] = 0.f;
+        // K fragment of step ks: 16-byte chunk 2ks + hi of row st*32 + lane%32 (DIR: at its
+        // swizzled position; st*32 is a multiple of 16, so the row's low bits are lane%16)
+        const bf16_t *krow =
+            ks_ + (st * 32 + (lane & 31)) * (DIR ? HD : KST) + (DIR ? 0 : hi * 8);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          const bf16x8_t a =
+              PREF ? kf[ks]
+                   : *reinterpret_cast<const bf16x8_t *>(
+                         krow + (DIR ? ((2 * ks + hi) ^ (lane & 15)) * 8 : ks * 16));
+          sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ks], sc, 0, 0, 0);
+        }
+        if (PREF && st == 0 && sk0 + 32 <= wmax) {
+          const bf16_t *knext = ks_ + (32 + (lane & 31)) * KST + hi * 8;
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks)
+            kf[ks] = *reinterpret_cast<const bf16x8_t *>(knext + ks * 16);
+        }
+        if (sk0 + 31 > wmin || sk0 + 31 >= kv_end) {  // causal / range mask needed
+#pragma unroll
+          for (int i = 0; i < 16; ++i) {
+            const int key = sk0 + (i >> 2) * 8 + hi * 4 + (i & 3);
+            if (key > rpos || key >= kv_end) sc[i] = -INFINITY;
+          }
+        }
+        float mx = sc[0];
+#pragma unroll
+        for (int i = 1; i < 16; ++i) mx = fmaxf(mx, sc[i]);
+        // raise the running maximum only when some score exceeds it by more than 2^8
+        if (__ballot(mx * scale_log2 > m_run + 8.f)) {
+          const float mp = fmaxf(mx, __shfl_xor(mx, 32, 64)) * scale_log2;
+          const float m_new = fmaxf(m_run, mp);
+          const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
+#pragma unroll
+          for (int db = 0; db < DB; ++db) o[db] *= alpha;
+          l_run *= alpha;
+          m_run = m_new;
+        }
+        // rows with no key yet keep m = -inf: offset by 0 then (every p is 0)
+        const float m_off = m_run == -INFINITY ? 0.f : m_run;
+        float pv[16];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          pv[i] = __builtin_amdgcn_exp2f(fmaf(sc[i], scale_log2, -m_off));  // v_exp_f32: arguments <= 8
+          l_run += pv[i];
+        }
+        // P^T operand of k-step t: slots hi*8 + j hold keys 16t + (j/4)*8 + hi*4 + j%4
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+          uint32_t pw[4];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) pw[j] = pack_bf2(pv[8 * t + 2 * j], pv[8 * t + 2 * j + 1]);
+          bf16x8_t pb;
+          __builtin_memcpy(&pb, pw, 16);
+#pragma unroll
+          for (int db = 0; db < DB; ++db) {
+            if (!PREF) read_v(t, db);
+            o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[t][db], pb, o[db], 0, 0, 0);
+          }
+        }
+      }
+    }
+    if (loader && more) AKVS_KV_STORE(Ks + ((kt + 1) & 1) * KBUF, Vt + ((kt + 1) & 1) * VBUF);
+    __syncthreads();
+    }
   }
 #undef AKVS_KV_LOAD
 #undef AKVS_KV_STORE
