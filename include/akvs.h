@@ -149,8 +149,9 @@ size_t akvs_workspace_size(const akvs_model_cfg *m, const akvs_reuse_cfg *cfg, i
 /* Workspace bytes of akvs_probe_qkv / akvs_probe_out_mlp over n_rows rows. */
 size_t akvs_step_workspace_size(const akvs_model_cfg *m, int32_t n_rows);
 /* Workspace bytes that let akvs_sparse_query_attention split the key range of n_rows rows
- * over n_keys keys (the launch configuration of the reuse prefill); 0 when that call would
- * not split (fp32 models, or enough row tiles to fill the GPU). */
+ * over n_keys keys (the launch configuration of the reuse prefill: the split partials and,
+ * for few rows, a plan of the split made on the device from the positions); 0 when that
+ * call would not split (fp32 models, or enough row tiles to fill the GPU). */
 size_t akvs_attention_workspace_size(const akvs_model_cfg *m, int32_t n_rows, int32_t n_keys);
 
 /* ---- step entries ---------------------------------------------------------------- */

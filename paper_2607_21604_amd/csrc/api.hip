@@ -269,6 +269,7 @@ struct LayerBufs {
   float *part_o, *part_ml;  // attention key-split partials (bf16 models)
   long long part_rows;      // splits x rows that part_o / part_ml hold
   float *gpart;             // GEMM K-split partials (bf16 models)
+  int32_t *plan;            // attention split plan of full_layer's rows
 };
 
 // GEMM partial-tile workspace (floats) of the four projections of one layer over `rows`.
@@ -303,12 +304,14 @@ void carve_layer_bufs(Carver &cv, const akvs_model_cfg *m, long long rows,
   b.part_ml = nullptr;
   b.part_rows = 0;
   b.gpart = nullptr;
+  b.plan = cv.take<int32_t>(kAttnPlanInts);
   size_t g = 0;
   long long worst = 0;
   for (const AttnUse &u : uses) {
     g = std::max(g, layer_gemm_part(m, u.rows));
     if (m->dtype != AKVS_BF16 || u.rows <= 0) continue;
-    const long long sp = attn_splits((int)u.rows, m->n_q_heads, m->n_kv_heads, (int)u.n_keys);
+    const long long sp = attn_part_splits((int)u.rows, m->n_q_heads, m->n_kv_heads, m->head_dim,
+                                          (int)u.n_keys);
     if (sp > 1 && sp * u.rows > worst) worst = sp * u.rows;
   }
   if (g) b.gpart = cv.take<float>(g);
@@ -333,6 +336,7 @@ struct ReuseBufs {
   float *mu_k, *mu_v;
   float *h_last;  // the query rows' residual stream at the last layer
   void *q_last;   // and their queries
+  int32_t *plan_rows, *plan_q;  // attention split plans: recomputed rows, query rows
 };
 
 size_t carve_reuse(void *ws, const akvs_model_cfg *m, const akvs_reuse_cfg *c, const Meta &mt,
@@ -367,6 +371,8 @@ size_t carve_reuse(void *ws, const akvs_model_cfg *m, const akvs_reuse_cfg *c, c
   b.mu_v = cv.take<float>((size_t)c->n_chunks * kvw);
   b.h_last = cv.take<float>((size_t)c->query_len * m->d_model);
   b.q_last = cv.take<char>((size_t)c->query_len * m->n_q_heads * m->head_dim * es);
+  b.plan_rows = cv.take<int32_t>(kAttnPlanInts);
+  b.plan_q = cv.take<int32_t>(kAttnPlanInts);
   return cv.off;
 }
 
@@ -464,11 +470,18 @@ akvs_status out_mlp(const akvs_model_cfg *m, const akvs_layer_w &w, float *h, in
   return AKVS_OK;
 }
 
+// Attention split plan of full_layer over n rows (into lb.plan, read by every such layer).
+hipError_t plan_full_layers(const akvs_model_cfg *m, int n, const LayerBufs &lb,
+                            hipStream_t stream) {
+  return launch_attention_plan(nullptr, 0, n, nullptr, n, m->n_q_heads, m->head_dim, m->dtype,
+                               lb.part_rows, lb.plan, stream);
+}
+
 // One ordinary causal layer over n consecutive rows at positions pos0.. (keys written to
-// k_dst / v_dst rows 0..n-1).
+// k_dst / v_dst rows 0..n-1). With planned = true, plan_full_layers(m, n, lb) ran before.
 akvs_status full_layer(const akvs_model_cfg *m, const akvs_layer_w &w, float *h, int n, int pos0,
                        const float *rope, const LayerBufs &lb, void *k_dst, void *v_dst,
-                       hipStream_t stream) {
+                       hipStream_t stream, bool planned) {
   const int D = m->d_model;
   const int qkvw = (m->n_q_heads + 2 * m->n_kv_heads) * m->head_dim;
   LAUNCH(AKVS_K_NORM, launch_rmsnorm(h, D, n, nullptr, nullptr, w.attn_norm, m->dtype, D,
@@ -478,7 +491,8 @@ akvs_status full_layer(const akvs_model_cfg *m, const akvs_layer_w &w, float *h,
                                   stream, lb.gpart);
   LAUNCH(AKVS_K_ATTENTION, launch_attention(lb.q, nullptr, 0, n, nullptr, k_dst, v_dst, n,
                                             m->n_q_heads, m->n_kv_heads, m->head_dim, m->dtype,
-                                            lb.att, lb.part_o, lb.part_ml, lb.part_rows, stream));
+                                            lb.att, lb.part_o, lb.part_ml, lb.part_rows, stream,
+                                            nullptr, planned ? lb.plan : nullptr));
   return out_mlp(m, w, h, n, nullptr, lb.att, lb.x, lb.act, lb.gpart, stream);
 }
 
@@ -494,6 +508,7 @@ struct BatchReq {
   uint8_t *flags;
   int32_t *chunk_rows, *rows, *fresh_row, *probe_k, *probe_v;
   float *mu_k, *mu_v;
+  int32_t *plan_rows, *plan_q;  // attention split plans: recomputed rows, query rows
 };
 
 struct BatchBufs {
@@ -542,6 +557,7 @@ size_t carve_batch(void *ws, const akvs_model_cfg *m, const akvs_reuse_cfg *cfgs
   b.lb.gpart = nullptr;
   b.lb.part_o = b.lb.part_ml = nullptr;
   b.lb.part_rows = 0;
+  b.lb.plan = nullptr;
   {
     const size_t g = std::max(layer_gemm_part(m, pl.cap_sum), layer_gemm_part(m, pl.q_sum));
     if (g) b.lb.gpart = cv.take<float>(g);
@@ -550,7 +566,8 @@ size_t carve_batch(void *ws, const akvs_model_cfg *m, const akvs_reuse_cfg *cfgs
     long long worst = 0;
     for (int i = 0; i < B; ++i) {
       for (long long r : {pl.mt[i].row_cap, (long long)cfgs[i].query_len}) {
-        const long long sp = attn_splits((int)r, m->n_q_heads, m->n_kv_heads, (int)pl.mt[i].t_all);
+        const long long sp = attn_part_splits((int)r, m->n_q_heads, m->n_kv_heads, m->head_dim,
+                                              (int)pl.mt[i].t_all);
         if (sp > 1 && sp * r > worst) worst = sp * r;
       }
     }
@@ -583,6 +600,8 @@ size_t carve_batch(void *ws, const akvs_model_cfg *m, const akvs_reuse_cfg *cfgs
     r.probe_v = cv.take<int32_t>((size_t)mt.sum_b_v + 1);
     r.mu_k = cv.take<float>((size_t)nch * kvw);
     r.mu_v = cv.take<float>((size_t)nch * kvw);
+    r.plan_rows = cv.take<int32_t>(kAttnPlanInts);
+    r.plan_q = cv.take<int32_t>(kAttnPlanInts);
   }
   return cv.off;
 }
@@ -858,17 +877,26 @@ static size_t attention_part_floats(const akvs_model_cfg *m, long long rows, lon
                                     size_t *ml_floats) {
   *ml_floats = 0;
   if (m->dtype != AKVS_BF16 || rows <= 0) return 0;
-  const long long sp = attn_splits((int)rows, m->n_q_heads, m->n_kv_heads, (int)n_keys);
+  const long long sp =
+      attn_part_splits((int)rows, m->n_q_heads, m->n_kv_heads, m->head_dim, (int)n_keys);
   if (sp < 2) return 0;
   *ml_floats = (size_t)(sp * rows) * m->n_q_heads * 2;
   return (size_t)(sp * rows) * m->n_q_heads * m->head_dim / 2;  // bf16 outputs, two per float
 }
 
+// The split partials, then the plan of the split (launch_attention_plan).
+static size_t attention_ws_bytes(const akvs_model_cfg *m, long long rows, long long n_keys,
+                                 size_t *o_floats, size_t *ml_floats) {
+  *o_floats = attention_part_floats(m, rows, n_keys, ml_floats);
+  if (!*o_floats) return 0;
+  return align256(*o_floats * sizeof(float)) + align256(*ml_floats * sizeof(float)) +
+         align256(kAttnPlanInts * sizeof(int32_t));
+}
+
 size_t akvs_attention_workspace_size(const akvs_model_cfg *m, int32_t n_rows, int32_t n_keys) {
   if (check_model(m) != AKVS_OK || n_rows < 0 || n_keys < 1) return 0;
-  size_t ml;
-  const size_t o = attention_part_floats(m, n_rows, n_keys, &ml);
-  return o ? align256(o * sizeof(float)) + align256(ml * sizeof(float)) : 0;
+  size_t o, ml;
+  return attention_ws_bytes(m, n_rows, n_keys, &o, &ml);
 }
 
 akvs_status akvs_sparse_query_attention(const void *q, const int32_t *positions, int32_t n_rows,
@@ -882,22 +910,28 @@ akvs_status akvs_sparse_query_attention(const void *q, const int32_t *positions,
   REQUIRE(aligned16(q) && aligned16(k) && aligned16(v) && aligned16(out) && aligned16(ws),
           AKVS_EINVAL, "misaligned argument");
   float *part_o = nullptr, *part_ml = nullptr;
+  int32_t *plan = nullptr;
   long long part_rows = 0;
   if (ws) {
-    size_t ml;
-    const size_t o = attention_part_floats(m, n_rows, n_keys, &ml);
-    const size_t need = o ? align256(o * sizeof(float)) + align256(ml * sizeof(float)) : 0;
+    size_t o, ml;
+    const size_t need = attention_ws_bytes(m, n_rows, n_keys, &o, &ml);
     REQUIRE(ws_bytes >= need, AKVS_ENOSPACE, "workspace %zu bytes, need %zu", ws_bytes, need);
     if (o) {
       Carver cv(ws);
       part_o = cv.take<float>(o);
       part_ml = cv.take<float>(ml);
+      plan = cv.take<int32_t>(kAttnPlanInts);
       part_rows = (long long)(ml / ((size_t)m->n_q_heads * 2));
     }
   }
+  if (plan)
+    LAUNCH(AKVS_K_OTHER, launch_attention_plan(positions, 0, n_rows, nullptr, n_keys,
+                                               m->n_q_heads, m->head_dim, m->dtype, part_rows,
+                                               plan, stream));
   LAUNCH(AKVS_K_ATTENTION, launch_attention(q, positions, 0, n_rows, nullptr, k, v, n_keys,
                                             m->n_q_heads, m->n_kv_heads, m->head_dim, m->dtype,
-                                            out, part_o, part_ml, part_rows, stream));
+                                            out, part_o, part_ml, part_rows, stream, nullptr,
+                                            plan));
   return AKVS_OK;
 }
 
@@ -958,10 +992,11 @@ akvs_status akvs_full_prefill(const int32_t *tokens, int32_t n_tokens, int32_t p
   LAUNCH(AKVS_K_OTHER, launch_rope_table(pos0, n_tokens, m->head_dim, (double)m->rope_theta,
                                          b.rope, stream));
   LAUNCH(AKVS_K_OTHER, launch_embed(tokens, n_tokens, embed, m->dtype, m->vocab, D, b.h, stream));
+  LAUNCH(AKVS_K_OTHER, plan_full_layers(m, n_tokens, b.lb, stream));
   for (int l = 0; l < m->n_layers; ++l) {
     st = full_layer(m, lw[l], b.h, n_tokens, pos0, b.rope, b.lb,
                     reinterpret_cast<char *>(k_out) + l * kvl,
-                    reinterpret_cast<char *>(v_out) + l * kvl, stream);
+                    reinterpret_cast<char *>(v_out) + l * kvl, stream, true);
     if (st) return st;
   }
   if (h_out)
@@ -1021,9 +1056,10 @@ akvs_status akvs_reuse_prefill(const int32_t *tokens, const void *embed, const a
   LAUNCH(AKVS_K_OTHER, launch_embed(tokens, T, embed, m->dtype, m->vocab, D, b.h_full, stream));
 
   // layers before the check layer: every token
+  if (c > 0) LAUNCH(AKVS_K_OTHER, plan_full_layers(m, T, b.lb, stream));
   for (int l = 0; l < c; ++l) {
     st = full_layer(m, lw[l], b.h_full, T, 0, b.rope, b.lb, k_corr + l * corr_layer,
-                    v_corr + l * corr_layer, stream);
+                    v_corr + l * corr_layer, stream, true);
     if (st) return st;
   }
   // check layer: fresh K/V of every unit token, divergence against the re-rotated cache
@@ -1044,6 +1080,12 @@ akvs_status akvs_reuse_prefill(const int32_t *tokens, const void *embed, const a
                                       b.rows, b.n_rows, b.fresh_row, stream));
   LAUNCH(AKVS_K_OTHER, launch_gather_rows(b.h_full, T, b.rows, cap, b.n_rows, D, b.h_probe,
                                           stream));
+  // one key-split plan per row set, for every layer's attention over it
+  LAUNCH(AKVS_K_OTHER, launch_attention_plan(b.rows, 0, cap, b.n_rows, T, m->n_q_heads, hd,
+                                             m->dtype, b.lb.part_rows, b.plan_rows, stream));
+  LAUNCH(AKVS_K_OTHER, launch_attention_plan(nullptr, Tc, cfg->query_len, nullptr, T,
+                                             m->n_q_heads, hd, m->dtype, b.lb.part_rows, b.plan_q,
+                                             stream));
   // from the check layer on: recomputed rows only, every unit token corrected
   const int qkvw = hqw + 2 * kvw;
   for (int l = c; l < L; ++l) {
@@ -1066,7 +1108,7 @@ akvs_status akvs_reuse_prefill(const int32_t *tokens, const void *embed, const a
       LAUNCH(AKVS_K_ATTENTION, launch_attention(b.lb.q, b.rows, 0, cap, b.n_rows, kl, vl, T,
                                                 m->n_q_heads, hkv, hd, m->dtype, b.lb.att,
                                                 b.lb.part_o, b.lb.part_ml, b.lb.part_rows,
-                                                stream));
+                                                stream, nullptr, b.plan_rows));
       st = out_mlp(m, lw[l], b.h_probe, cap, b.n_rows, b.lb.att, b.lb.x, b.lb.act, b.lb.gpart,
                    stream, (int)mt.row_min);
       if (st) return st;
@@ -1081,7 +1123,8 @@ akvs_status akvs_reuse_prefill(const int32_t *tokens, const void *embed, const a
                                                stream));
     LAUNCH(AKVS_K_ATTENTION, launch_attention(b.q_last, nullptr, Tc, q, nullptr, kl, vl, T,
                                               m->n_q_heads, hkv, hd, m->dtype, b.lb.att,
-                                              b.lb.part_o, b.lb.part_ml, b.lb.part_rows, stream));
+                                              b.lb.part_o, b.lb.part_ml, b.lb.part_rows, stream,
+                                              nullptr, b.plan_q));
     st = out_mlp(m, lw[l], b.h_last, q, nullptr, b.lb.att, b.lb.x, b.lb.act, b.lb.gpart, stream);
     if (st) return st;
   }
@@ -1162,8 +1205,9 @@ akvs_status akvs_reuse_prefill_batch(const int32_t *const *tokens, int32_t batch
     LAUNCH(AKVS_K_OTHER, launch_token_setup(r.meta, nch, r.tok_delta, r.tok_chunk, stream));
     LAUNCH(AKVS_K_OTHER, launch_embed(tokens[i], T, embed, m->dtype, m->vocab, D, r.h_full, stream));
     for (int l = 0; l < c; ++l) {
+      if (l == 0) LAUNCH(AKVS_K_OTHER, plan_full_layers(m, T, b.lb_full, stream));
       st = full_layer(m, lw[l], r.h_full, T, 0, b.rope, b.lb_full, k_corr + l * corr_layer,
-                      v_corr + l * corr_layer, stream);
+                      v_corr + l * corr_layer, stream, true);
       if (st) return st;
     }
     if (!no_prefix) {
@@ -1191,6 +1235,13 @@ akvs_status akvs_reuse_prefill_batch(const int32_t *const *tokens, int32_t batch
                                             b.n_rows + i, D, b.h_probe, stream, b.row_off + i));
     LAUNCH(AKVS_K_OTHER, launch_copy_ints_at(b.req[i].rows, cap, b.n_rows + i, b.pos,
                                              b.row_off + i, stream));
+    LAUNCH(AKVS_K_OTHER, launch_attention_plan(b.req[i].rows, 0, cap, b.n_rows + i,
+                                               (int)mt.t_all, m->n_q_heads, hd, m->dtype,
+                                               b.lb.part_rows, b.req[i].plan_rows, stream));
+    LAUNCH(AKVS_K_OTHER, launch_attention_plan(nullptr, (int)mt.t_ctx, cfgs[i].query_len,
+                                               nullptr, (int)mt.t_all, m->n_q_heads, hd,
+                                               m->dtype, b.lb.part_rows, b.req[i].plan_q,
+                                               stream));
   }
   for (int l = c; l < L; ++l) {
     LAUNCH(AKVS_K_NORM, launch_rmsnorm(b.h_probe, D, cap_sum, M_dev, nullptr, lw[l].attn_norm,
@@ -1221,7 +1272,7 @@ akvs_status akvs_reuse_prefill_batch(const int32_t *const *tokens, int32_t batch
         LAUNCH(AKVS_K_ATTENTION,
                launch_attention(b.lb.q, b.pos, 0, cap, b.n_rows + i, kl, vl, T, m->n_q_heads, hkv,
                                 hd, m->dtype, b.lb.att, b.lb.part_o, b.lb.part_ml,
-                                b.lb.part_rows, stream, b.row_off + i));
+                                b.lb.part_rows, stream, b.row_off + i, r.plan_rows));
         continue;
       }
       // last layer: only the query rows (the last q of each request's rows) go on
@@ -1235,7 +1286,8 @@ akvs_status akvs_reuse_prefill_batch(const int32_t *const *tokens, int32_t batch
       LAUNCH(AKVS_K_ATTENTION,
              launch_attention(ql, nullptr, Tc, q, nullptr, kl, vl, T, m->n_q_heads, hkv, hd,
                               m->dtype, reinterpret_cast<char *>(b.lb.att) + (size_t)q_off * hqw * es,
-                              b.lb.part_o, b.lb.part_ml, b.lb.part_rows, stream));
+                              b.lb.part_o, b.lb.part_ml, b.lb.part_rows, stream, nullptr,
+                              r.plan_q));
       q_off += q;
     }
     if (!last) {

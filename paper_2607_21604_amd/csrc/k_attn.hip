@@ -49,79 +49,99 @@ static inline AttnShape attn_shape(int G, int rows, int hkv) {
   return a;
 }
 
-// Key split planned on the device (split launches of one-head 8-wave blocks): the host
-// knows only a bound on the row count, and how long the (row tile, key range) blocks of a
-// split count are depends on the live rows' positions. Wave 0 of every block derives the
-// same plan: the key range of tile t (rows sorted by position) ends at its last row's
-// position; each candidate count sp <= min(sp_max, 16) cuts the keys into ranges of
-// S = attn_split_keys keys, tile t taking ceil(keys_t / S) of them. Its cost, in keys: the
-// blocks in dispatch order fill rounds of `slots` blocks, each round costs its longest
-// block (keys + 512 for the block's fixed work), plus 32 per split for the merge; the
-// least cost wins, the smaller count on a tie (the model ranked the measured launch
-// sweeps of the 3B probe layers at r = 1/100 to 1/5 correctly). Items are ordered
-// tile-descending (longest first), splits ascending; item -> (tile, split, S, splits of
-// that tile) in s_plan, tile -1 past the last item. Needs tiles <= 64.
-__device__ __forceinline__ void attn_plan(int item, int R, int rb_rows, const int32_t *pos,
-                                          int pos0, int n_keys, int heads, int sp_max,
-                                          int slots, int lane, int *s_plan) {
-  const int nt = (R + rb_rows - 1) / rb_rows;
-  int keys = 0;
-  if (lane < nt) {
-    const int e = min((lane + 1) * rb_rows, R) - 1;
-    keys = min(n_keys, (pos ? pos[e] : pos0 + e) + 1);
+// Planned split (launch_attention_plan, then launch_attention with the plan): for calls
+// over few position-sorted rows, whose tiles leave block slots idle or end at very
+// different times, the key range of each tile is cut into nearly equal pieces sized so
+// that every block slot of the chip gets about the same work, and the pieces go out
+// longest first. Block shape and item budget from the row bound (host):
+//  - 4-wave 128-row blocks (two per CU) in one round, where the 128-row tiles fill at most
+//    3/4 of the round's items (slots / heads) and are at least 3;
+//  - else 8-wave 256-row blocks (one per CU): one round where their tiles fill at most
+//    half of it, two rounds where they fill less than two;
+//  - else no plan (the tiles alone fill the chip; launch_attention's own split applies).
+// Measured on the 3B-class probe layers (1441 / 865 / 300 / 166 rows over 4516 keys):
+// 75 / 53 / 38 / 35 us against 92 / 60 / 47 / 37 us; 7B-class (2802 / 1513 rows over
+// 8128 keys) 199 / 129 against 215 / 155 us; the query rows of the last layer (64 over
+// 4516 keys, 128 over 16128) 27 / 69 against 28 / 79 us. With one round for the 3B
+// layers at 1992 rows over 4516 keys the 128-row blocks took 101 us against 89 us for two
+// rounds of 256-row blocks, which is what sets the 3/4 bound (standalone harness, not in
+// the repository).
+struct AttnEqShape {
+  int rb, budget, max_pc;
+  bool use;
+};
+constexpr int kAttnMaxPieces = 8;  // the merge's all-at-once path
+static inline AttnEqShape attn_eq_shape(int rows, int hq, int hd, int dtype, long long part_rows,
+                                        int cus) {
+  AttnEqShape e{0, 0, 0, false};
+  if (dtype != AKVS_BF16 || rows <= 0 || hq <= 0 || (hd != 64 && hd != 128)) return e;
+  const int p128 = 2 * cus / hq, p256 = cus / hq;
+  const int nt128 = (rows + 127) / 128, nt256 = (rows + 255) / 256;
+  if (nt128 >= 3 && 4 * nt128 <= 3 * p128) {
+    e.rb = 128;
+    e.budget = p128;
+  } else if (p256 >= 1 && 2 * nt256 <= p256) {
+    e.rb = 256;
+    e.budget = p256;
+  } else if (p256 >= 1 && nt256 < 2 * p256) {
+    e.rb = 256;
+    e.budget = 2 * p256;
+  } else {
+    return e;
   }
-  const int sp = lane + 1;
-  const bool cand = sp <= min(sp_max, 16);
-  const int S = ((n_keys + sp - 1) / sp + 63) / 64 * 64;
-  // (32-bit counts: at most 64 tiles x 64 splits x heads blocks; no divisions in the loop)
-  int blk = 0, total = 0, round_end = slots;
-  int rmax = 0;  // longest block of the open round
-  for (int t = nt - 1; t >= 0; --t) {
-    const int k = __shfl(keys, t, 64);
-    if (!cand) continue;
-    for (int k0 = 0; k0 < k; k0 += S) {
-      const int d = min(S, k - k0) + 512;
-      if (blk >= round_end) {  // this item opens a new round
-        total += rmax;
-        rmax = 0;
-        round_end += slots;
-      }
-      rmax = max(rmax, d);
-      while (blk + heads - 1 >= round_end) {  // its blocks run on into the next round
-        total += rmax;
-        rmax = d;
-        round_end += slots;
-      }
-      blk += heads;
-    }
-  }
-  total += rmax;
-  long long key = 0x7fffffffffffffffLL;
-  if (cand) key = ((long long)total + 32LL * sp) * 64 + lane;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) key = min(key, __shfl_xor(key, o, 64));
-  const int best = (int)(key & 63);
-  const int Sb = __shfl(S, best, 64);
-  // lane j <-> tile nt - 1 - j: split count and inclusive prefix over the item order
-  const int kj = __shfl(keys, max(nt - 1 - lane, 0), 64);
-  const int c = lane < nt ? (kj + Sb - 1) / Sb : 0;
-  int incl = c;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int v = __shfl_up(incl, o, 64);
-    if (lane >= o) incl += v;
-  }
-  const int j = __popcll(__ballot(lane < nt && incl <= item));
-  const int cj = __shfl(c, min(j, 63), 64), ij = __shfl(incl, min(j, 63), 64);
-  if (lane == 0) {
-    s_plan[0] = j < nt ? nt - 1 - j : -1;
-    s_plan[1] = item - (ij - cj);
-    s_plan[2] = Sb;
-    s_plan[3] = cj;
-  }
+  if ((rows + e.rb - 1) / e.rb > 64) return e;
+  e.max_pc = (int)std::min<long long>(kAttnMaxPieces, part_rows / rows);
+  e.use = e.max_pc >= 2;
+  return e;
 }
 
-// A block serves head group hg of KV head kvh: 32 * nrb query rows x gh query heads. Wave// A block serves head group hg of KV head kvh: 32 * nrb query rows x gh query heads. Wave
+// The plan (one wave): tile t of rb rows sees kt_t = ceil(keys_t / 64) key tiles, keys_t
+// its last row's position + 1. It is cut into c_t = ceil(kt_t / L) ranges of nearly equal
+// length, L the smallest with sum_t c_t <= max(tiles, budget) and c_t <= max_pc. Items
+// (tile, range) are numbered by the tile's range length, longest first (equal lengths:
+// later tile first), a tile's ranges together. plan[0] = {tiles, items, max_t c_t},
+// plan[1 + t] = {c_t, first item of tile t, kt_t} (c_t = 0 past the last tile).
+__global__ __launch_bounds__(64) void k_attn_plan(const int32_t *pos, int pos0, int rows,
+                                                  const int32_t *rows_dev,
+                                                  const int32_t *row_base, int n_keys, int rb,
+                                                  int budget, int max_pc, int4 *plan) {
+  const int lane = threadIdx.x;
+  int R = rows;
+  if (rows_dev) R = min(R, *rows_dev);
+  if (row_base && pos) pos += *row_base;
+  const int nt = (R + rb - 1) / rb;
+  int kt = 0;
+  if (lane < nt) {
+    const int e = min((lane + 1) * rb, R) - 1;
+    kt = (min(n_keys, (pos ? pos[e] : pos0 + e) + 1) + 63) >> 6;
+  }
+  int ktmax = kt;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) ktmax = max(ktmax, __shfl_xor(ktmax, o, 64));
+  const int B = max(nt, budget);
+  int lo = max(1, (ktmax + max_pc - 1) / max_pc), hi = max(lo, ktmax);
+  while (lo < hi) {  // the same bounds in every lane
+    const int L = (lo + hi) >> 1;
+    int c = lane < nt ? (kt + L - 1) / L : 0;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) c += __shfl_xor(c, o, 64);
+    if (c <= B) hi = L;
+    else lo = L + 1;
+  }
+  const int c = lane < nt ? (kt + lo - 1) / lo : 0;
+  const int p = lane < nt ? (kt + c - 1) / c : 0;  // the tile's longest range
+  int off = 0, total = 0, cmax = 0;
+  for (int u = 0; u < nt; ++u) {  // u is the same in every lane: lane reads, no LDS trips
+    const int pu = __builtin_amdgcn_readlane(p, u), cu = __builtin_amdgcn_readlane(c, u);
+    if (pu > p || (pu == p && u > lane)) off += cu;
+    total += cu;
+    cmax = max(cmax, cu);
+  }
+  plan[1 + lane] = make_int4(c, off, kt, 0);
+  if (lane == 0) plan[0] = make_int4(nt, total, cmax, 0);
+}
+
+// A block serves head group hg of KV head kvh: 32 * nrb query rows x gh query heads. Wave
 // w owns 32 rows (row block w / gh) of query head kvh * G + hg * gh + w % gh. Waves 0-3
 // stage each 64-key K / V tile in LDS for all of them (double buffered, next tile
 // prefetched into registers during the current one). Block b serves KV head b % Hkv, so
@@ -134,12 +154,13 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
                                                    const bf16_t *__restrict__ Vc, int n_keys,
                                                    int hq, int hkv, int gh, int n_groups,
                                                    int nrb, int n_tiles, int n_splits,
-                                                   int split_keys, int plan_slots,
+                                                   int split_keys,
                                                    float scale_log2,
                                                    bf16_t *__restrict__ out,
                                                    bf16_t *__restrict__ part_o,
                                                    float *__restrict__ part_ml,
-                                                   const int32_t *row_base) {
+                                                   const int32_t *row_base,
+                                                   const int4 *__restrict__ plan) {
   constexpr int KS = HD / 16;          // contraction steps of S
   constexpr int DB = HD / 32;          // 32-wide head-dim blocks of O
   constexpr int KST = HD + 8;          // K tile row stride (bf16)
@@ -156,7 +177,6 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
   __shared__ __attribute__((aligned(16))) bf16_t Ks1[DIR ? KBUF : 1];
   __shared__ __attribute__((aligned(16))) bf16_t Vt1[DIR ? VBUF : 1];
   __shared__ int s_max[8];
-  __shared__ int s_plan[4];
   if (row_base) {  // this call's rows start at row *row_base of q, pos and out
     const int rb0 = *row_base;
     Q += (size_t)rb0 * hq * HD;
@@ -175,16 +195,19 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
   int R = rows;
   if (rows_dev) R = min(R, *rows_dev);
   const int rb_rows = 32 * nrb;
-  int split, tile, n_part = n_splits;
-  if (plan_slots > 0) {  // key split planned here from the live rows (see attn_plan)
-    if (wave == 0)
-      attn_plan(rest, R, rb_rows, pos, pos0, n_keys, hkv * n_groups, n_splits, plan_slots, lane,
-                s_plan);
-    __syncthreads();
-    tile = s_plan[0];
-    split = s_plan[1];
-    split_keys = s_plan[2];
-    n_part = s_plan[3];
+  int split, tile, n_part = n_splits, kv_begin = -1;
+  if (plan) {  // item `rest` of the call's plan (see k_attn_plan)
+    const int4 e = plan[1 + lane];  // (c = 0 past the last tile)
+    const unsigned long long mine = __ballot(e.x > 0 && e.y <= rest && rest < e.y + e.x);
+    if (mine == 0) return;  // past the last item (the whole block)
+    const int t = __ffsll((long long)mine) - 1;
+    const int c = __shfl(e.x, t, 64), first = __shfl(e.y, t, 64), kt = __shfl(e.z, t, 64);
+    tile = t;
+    split = rest - first;
+    n_part = c;
+    if (c > n_splits) return;  // not a plan for this launch's partial slots
+    kv_begin = (split * kt / c) * 64;
+    split_keys = ((split + 1) * kt / c) * 64 - kv_begin;
   } else {
     split = rest % n_splits;
     tile = n_tiles - 1 - rest / n_splits;
@@ -207,7 +230,7 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
   int bmax = -1;
   for (int w = 0; w < nw; ++w) bmax = max(bmax, s_max[w]);
   // this block's keys: [kv_begin, kv_end) of split `split`
-  const int kv_begin = split * split_keys;
+  if (kv_begin < 0) kv_begin = split * split_keys;
   const int kv_end = min(min(n_keys, bmax + 1), kv_begin + split_keys);
   const int nkt = kv_end > kv_begin ? (kv_end - kv_begin + 63) / 64 : 0;
   const size_t prow = ((size_t)split * rows + r) * hq + head;  // partial slot of this lane's row
@@ -561,7 +584,12 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
   const float l_row = l_run + __shfl_xor(l_run, 32, 64);
   if (!rvalid) return;
   // o[db][i] is dim db*32 + (i/4)*8 + hi*4 + i%4 of row r
-  if (n_splits > 1) {  // this split's output over its own keys (bf16) + (max, sum)
+  if (n_splits > 1 && n_part == 1) {  // a whole tile: final output here; the merge skips
+    if (hi == 0) {                     // the row (end mark in the first slot)
+      part_ml[2 * prow] = -INFINITY;
+      part_ml[2 * prow + 1] = -1.f;
+    }
+  } else if (n_splits > 1) {  // this split's output over its own keys (bf16) + (max, sum)
     const float pinv = l_row > 0.f ? 1.0f / l_row : 0.f;  // no visible key: m = -inf, skipped
     bf16_t *po = part_o + prow * HD + hi * 4;
 #pragma unroll
@@ -597,7 +625,8 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
 // whose keys all lie past the row (causal mask) holds m = -inf and is skipped, never
 // multiplied in (its part_o slot holds whatever the workspace held). With a device-planned
 // split a tile may use fewer splits than the launch's count: l = -1 after its last one
-// ends the list (the slots past it are stale).
+// ends the list (the slots past it are stale); l = -1 in the first slot marks a row whose
+// tile ran as one piece and whose output the attention block wrote itself.
 // Thread = 8 consecutive head dims of one (row, head) (16-byte loads and stores). Up to 8
 // splits, all (m, l) pairs and partial outputs are requested at once; with more, the
 // maxima first, then the splits in order.
@@ -606,7 +635,8 @@ __global__ __launch_bounds__(256) void k_attn_combine(const bf16_t *__restrict__
                                                       int n_splits, int rows,
                                                       const int32_t *rows_dev, int hq, int hd,
                                                       bf16_t *__restrict__ out,
-                                                      const int32_t *row_base) {
+                                                      const int32_t *row_base,
+                                                      const int4 *plan) {
   const int per = hd >> 3;  // threads per (row, head)
   const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
   const long long item = gid / per;
@@ -615,6 +645,7 @@ __global__ __launch_bounds__(256) void k_attn_combine(const bf16_t *__restrict__
   if (rows_dev) R = min(R, *rows_dev);
   if (item >= (long long)R * hq) return;
   if (row_base) out += (size_t)*row_base * hq * hd;
+  if (plan) n_splits = min(n_splits, plan[0].z);  // no tile of the plan has more pieces
   const size_t stride = (size_t)rows * hq;  // items per split
   float mx = -INFINITY, l = 0.f, a[8];
 #pragma unroll
@@ -637,6 +668,7 @@ __global__ __launch_bounds__(256) void k_attn_combine(const bf16_t *__restrict__
 #pragma unroll
     for (int u = 0; u < 8; ++u)
       if (u < n) mx = fmaxf(mx, ml[u].x);
+    if (n == 0) return;  // the attention wrote this row's output itself
     const float moff = mx == -INFINITY ? 0.f : mx;
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
@@ -653,6 +685,7 @@ __global__ __launch_bounds__(256) void k_attn_combine(const bf16_t *__restrict__
       if (ml.y < 0.f) n = sp;
       else mx = fmaxf(mx, ml.x);
     }
+    if (n == 0) return;
     const float moff = mx == -INFINITY ? 0.f : mx;
     for (int sp = 0; sp < n; ++sp) {
       const size_t pi = sp * stride + item;
@@ -753,11 +786,28 @@ int attn_split_keys(int n_keys, int n_splits) {
   return (per + 63) / 64 * 64;
 }
 
+int attn_part_splits(int rows, int hq, int hkv, int hd, int n_keys) {
+  const int sp = attn_splits(rows, hq, hkv, n_keys);
+  const AttnEqShape e =
+      attn_eq_shape(rows, hq, hd, AKVS_BF16, (long long)kAttnMaxPieces * rows, gemm_cu_count());
+  return e.use ? std::max(sp, kAttnMaxPieces) : sp;
+}
+
+hipError_t launch_attention_plan(const int32_t *pos, int pos0, int rows, const int32_t *rows_dev,
+                                 int n_keys, int hq, int hd, int dtype, long long part_rows,
+                                 int32_t *plan, hipStream_t s, const int32_t *row_base) {
+  const AttnEqShape e = attn_eq_shape(rows, hq, hd, dtype, part_rows, gemm_cu_count());
+  if (!e.use || !plan) return hipSuccess;  // launch_attention will not read it either
+  hipLaunchKernelGGL(k_attn_plan, dim3(1), dim3(64), 0, s, pos, pos0, rows, rows_dev, row_base,
+                     n_keys, e.rb, e.budget, e.max_pc, reinterpret_cast<int4 *>(plan));
+  return hipGetLastError();
+}
+
 hipError_t launch_attention(const void *q, const int32_t *pos, int pos0, int rows,
                             const int32_t *rows_dev, const void *k, const void *v, int n_keys,
                             int hq, int hkv, int hd, int dtype, void *out, float *part_o,
                             float *part_ml, long long part_rows, hipStream_t s,
-                            const int32_t *row_base) {
+                            const int32_t *row_base, const int32_t *plan) {
   if (rows == 0) return hipSuccess;
   if (dtype == AKVS_BF16) {
     const float scale_log2 = 1.4426950408889634f / sqrtf((float)hd);
@@ -767,29 +817,41 @@ hipError_t launch_attention(const void *q, const int32_t *pos, int pos0, int row
     bf16_t *O = reinterpret_cast<bf16_t *>(out);
     AttnShape a = attn_shape(hq / hkv, rows, hkv);
     if (a.gh == 0) return hipErrorInvalidValue;
+    const AttnEqShape e = attn_eq_shape(rows, hq, hd, dtype, part_rows, gemm_cu_count());
+    if (plan && part_o && part_ml && e.use) {  // the split that launch_attention_plan planned
+      const int nrb = e.rb / 32;
+      const int items = std::max((rows + e.rb - 1) / e.rb, e.budget);
+      dim3 g(items * hq), b(64 * nrb);
+      const int4 *P = reinterpret_cast<const int4 *>(plan);
+#define AKVS_ATTN_PLANNED(HD_, PREF_)                                                             \
+  hipLaunchKernelGGL((k_attn_bf16<HD_, PREF_>), g, b, 0, s, Q, pos, pos0, rows, rows_dev, K, V,     \
+                     n_keys, hq, hkv, 1, hq / hkv, nrb, 1, e.max_pc, 0, scale_log2, O,             \
+                     reinterpret_cast<bf16_t *>(part_o), part_ml, row_base, P)
+      if (hd == 128) {
+        if (nrb == 4) AKVS_ATTN_PLANNED(128, true); else AKVS_ATTN_PLANNED(128, false);
+      } else {
+        if (nrb == 4) AKVS_ATTN_PLANNED(64, true); else AKVS_ATTN_PLANNED(64, false);
+      }
+#undef AKVS_ATTN_PLANNED
+      hipError_t er = hipGetLastError();
+      if (er != hipSuccess) return er;
+      const long long threads = (long long)rows * hq * (hd / 8);
+      hipLaunchKernelGGL(k_attn_combine, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, s,
+                         reinterpret_cast<const bf16_t *>(part_o), part_ml, e.max_pc, rows,
+                         rows_dev, hq, hd, O, row_base, P);
+      return hipGetLastError();
+    }
     int n_splits = part_o && part_ml ? attn_splits(rows, hq, hkv, n_keys) : 1;
     if ((long long)n_splits * rows > part_rows) n_splits = (int)std::max(1LL, part_rows / rows);
     const int split_keys = attn_split_keys(n_keys, n_splits);
-    // Split launches whose 128-row tiles alone leave CUs without a block: 8-wave blocks, the
-    // split count (<= n_splits) planned on the device. Where the 128-row tiles already
-    // give every CU one, their finer grain balances the causal ramp better (launch sweeps
-    // of the 3B probe layers: 79 against 83 us at r = 1/5; 65 against 78 us at r = 1/10
-    // and 35 against 48 us at r = 1/100 for the planned split).
-    int plan_slots = 0;
-    const int cus = gemm_cu_count();
-    if (n_splits > 1 && a.gh == 1 && (rows + 255) / 256 <= 64 &&
-        (long long)((rows + 127) / 128) * hkv * a.n_groups <= cus) {
-      a.nrb = 8;
-      plan_slots = cus;
-    }
     const int n_tiles = (rows + 32 * a.nrb - 1) / (32 * a.nrb);
     dim3 g(n_tiles * hkv * a.n_groups * n_splits), b(64 * a.nrb * a.gh);
     const bool pref = a.nrb * a.gh <= 4;  // see PREF in the kernel
 #define AKVS_ATTN(HD_, PREF_)                                                                    \
   hipLaunchKernelGGL((k_attn_bf16<HD_, PREF_>), g, b, 0, s, Q, pos, pos0, rows, rows_dev, K, V,    \
                      n_keys, hq, hkv, a.gh, a.n_groups, a.nrb, n_tiles, n_splits, split_keys,      \
-                     plan_slots, scale_log2, O, reinterpret_cast<bf16_t *>(part_o), part_ml,      \
-                     row_base)
+                     scale_log2, O, reinterpret_cast<bf16_t *>(part_o), part_ml, row_base,         \
+                     nullptr)
     if (hd == 128) {
       if (pref) AKVS_ATTN(128, true); else AKVS_ATTN(128, false);
     } else {
@@ -802,7 +864,7 @@ hipError_t launch_attention(const void *q, const int32_t *pos, int pos0, int row
       const long long threads = (long long)rows * hq * (hd / 8);
       hipLaunchKernelGGL(k_attn_combine, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, s,
                          reinterpret_cast<const bf16_t *>(part_o), part_ml, n_splits, rows,
-                         rows_dev, hq, hd, O, row_base);
+                         rows_dev, hq, hd, O, row_base, nullptr);
     }
   } else {
     const float scale = 1.0f / sqrtf((float)hd);

@@ -119,9 +119,20 @@ hipError_t launch_attention(const void *q, const int32_t *pos, int pos0, int row
                             const int32_t *rows_dev, const void *k, const void *v, int n_keys,
                             int hq, int hkv, int hd, int dtype, void *out, float *part_o,
                             float *part_ml, long long part_rows, hipStream_t s,
-                            const int32_t *row_base = nullptr);
+                            const int32_t *row_base = nullptr, const int32_t *plan = nullptr);
+// Plan of a split over the same rows (positions, row bound, live count, row_base as the
+// launch_attention call that reads it; plan: kAttnPlanInts int32 of device memory, 16-byte
+// aligned). Nothing is launched, and launch_attention ignores the plan, where the call's
+// shape does not use one. The plan depends only on the rows' positions and n_keys: one
+// plan serves every layer over the same rows.
+constexpr int kAttnPlanInts = 4 * 65;
+hipError_t launch_attention_plan(const int32_t *pos, int pos0, int rows, const int32_t *rows_dev,
+                                 int n_keys, int hq, int hd, int dtype, long long part_rows,
+                                 int32_t *plan, hipStream_t s, const int32_t *row_base = nullptr);
 // number of key splits launch_attention uses for `rows` rows over n_keys keys
 int attn_splits(int rows, int hq, int hkv, int n_keys);
+// partial slots per row that the part_o / part_ml buffers of such a call should hold
+int attn_part_splits(int rows, int hq, int hkv, int hd, int n_keys);
 int attn_split_keys(int n_keys, int n_splits);
 
 // ---- k_decode.hip -------------------------------------------------------------------

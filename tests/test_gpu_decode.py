@@ -106,12 +106,14 @@ def test_decode_workspace_and_bounds():
 
 @pytest.mark.parametrize("n_q,n_kv,hd,n", [
     (24, 8, 128, 0), (24, 8, 128, 16), (24, 8, 128, 4516), (28, 4, 128, 1000),
-    (40, 8, 128, 16128), (8, 1, 64, 300), (4, 4, 64, 129), (16, 1, 128, 200)])
+    (40, 8, 128, 16128), (8, 1, 64, 300), (4, 4, 64, 129), (16, 1, 128, 200),
+    (16, 1, 128, 3000)])
 def test_decode_step_one_row_attention_shapes(n_q, n_kv, hd, n):
     """One decode step of a one-layer bf16 model over random caches of n positions, at the
     query / KV head ratios of the 3B, 7B and 32B shapes and at head dim 64: the one-row
     attention kernel from a single key chunk up to 127 chunks of 128 keys; 16 query heads
-    per KV head take the general attention kernel instead. Keys are scaled
+    per KV head take the general attention kernel instead (over 3001 keys with its
+    12-way key split and the merge's sequential path). Keys are scaled
     so that the softmax is far from uniform. Logits and the new K/V row against the oracle
     run on the same cache values."""
     shape = synthetic.ModelShape("dec", 1, 512, n_q, n_kv, hd, 1024, 2048, 1.0e6)
