@@ -865,27 +865,22 @@ __global__ __launch_bounds__(256) void k_gemm_fixup(int M, int N, int K, const i
   const int splits = W8 ? w8_k_splits(M_eff, N, K, epi.mode, n_slots)
                         : gemm_k_splits(tiles, K / GB_K, n_slots);
   constexpr int SLICES = BM / G_FR;
-  if (splits < 2) return;  // nothing was split at this row count
-  // (tile, slice) items, grid-strided: the grid stays small, so that a launch whose GEMM
-  // did not split costs little more than its dispatch
-  for (int it = blockIdx.x; it < tiles * SLICES; it += gridDim.x) {
-    const int tile = it / SLICES, slice = it - tile * SLICES;
-    const int m0 = (tile / n_tiles) * BM + slice * G_FR;
-    if (m0 >= M_eff) continue;  // the same in every thread of the block
-    const int n0 = (tile - (tile / n_tiles) * n_tiles) * bn_out;
-    const float *src = part + (size_t)tile * splits * BM * GB_N + (size_t)slice * G_FR * GB_N;
-    constexpr int PER = G_FR * GB_N / 4 / 256;  // float4 per thread
+  const int tile = blockIdx.x / SLICES, slice = blockIdx.x - tile * SLICES;
+  if (splits < 2 || tile >= tiles) return;
+  const int m0 = (tile / n_tiles) * BM + slice * G_FR;
+  if (m0 >= M_eff) return;
+  const int n0 = (tile - (tile / n_tiles) * n_tiles) * bn_out;
+  const float *src = part + (size_t)tile * splits * BM * GB_N + (size_t)slice * G_FR * GB_N;
+  constexpr int PER = G_FR * GB_N / 4 / 256;  // float4 per thread
 #pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      const int e4 = threadIdx.x + 256 * i;
-      const int row = e4 / (GB_N / 4), c4 = (e4 - row * (GB_N / 4)) * 4;
-      const float4 acc = sum_pieces(src + row * GB_N + c4, (size_t)BM * GB_N, splits);
-      *reinterpret_cast<float4 *>(Cs + row * G_CLD + c4) = acc;
-    }
-    __syncthreads();
-    epilogue_tile<G_FR, GB_N, 256>(Cs, G_CLD, m0, n0, M_eff, N, epi);
-    __syncthreads();  // Cs is reused by the next item
+  for (int i = 0; i < PER; ++i) {
+    const int e4 = threadIdx.x + 256 * i;
+    const int row = e4 / (GB_N / 4), c4 = (e4 - row * (GB_N / 4)) * 4;
+    const float4 acc = sum_pieces(src + row * GB_N + c4, (size_t)BM * GB_N, splits);
+    *reinterpret_cast<float4 *>(Cs + row * G_CLD + c4) = acc;
   }
+  __syncthreads();
+  epilogue_tile<G_FR, GB_N, 256>(Cs, G_CLD, m0, n0, M_eff, N, epi);
 }
 
 // ------------------------------------------------------------------------------------------
@@ -1136,17 +1131,14 @@ hipError_t launch_gemm_fixup(const void *, int lda, const void *, int ldb, int M
     if (!c.any_split) return hipSuccess;
     const int bn_out = epi.mode == EPI_SWIGLU ? kW8SplitBN / 2 : kW8SplitBN;
     const int tiles = ((M + kW8SplitBM - 1) / kW8SplitBM) * ((N + bn_out - 1) / bn_out);
-    const int items = tiles * (kW8SplitBM / G_FR);
-    hipLaunchKernelGGL((k_gemm_fixup<kW8SplitBM, true>),
-                       dim3(std::min(items, 4 * gemm_cu_count())), dim3(256), 0, s, M, N, K,
-                       m_dev, epi, gemm_cu_count(), part);
+    hipLaunchKernelGGL((k_gemm_fixup<kW8SplitBM, true>), dim3(tiles * (kW8SplitBM / G_FR)),
+                       dim3(256), 0, s, M, N, K, m_dev, epi, gemm_cu_count(), part);
     return hipGetLastError();
   }
   const GemmPlan p = gemm_plan(M, N, K, m_dev, epi, part, m_min);
   if (!p.any_split) return hipSuccess;
-  hipLaunchKernelGGL((k_gemm_fixup<128, false>),
-                     dim3(std::min(p.tiles_cap * (128 / G_FR), 4 * gemm_cu_count())), dim3(256), 0,
-                     s, M, N, K, m_dev, epi, p.n_slots, part);
+  hipLaunchKernelGGL((k_gemm_fixup<128, false>), dim3(p.tiles_cap * (128 / G_FR)), dim3(256), 0, s,
+                     M, N, K, m_dev, epi, p.n_slots, part);
   return hipGetLastError();
 }
 
