@@ -16,7 +16,10 @@ namespace akvs {
 
 namespace {
 
-__device__ __forceinline__ float silu_dec(float g) { return g / (1.0f + __expf(-g)); }
+// the prefill GEMMs' SiLU (hardware reciprocal in place of an IEEE division)
+__device__ __forceinline__ float silu_dec(float g) {
+  return g * __builtin_amdgcn_rcpf(1.0f + __expf(-g));
+}
 
 // v rounded to the storage type T and widened back to fp32.
 template <typename T>

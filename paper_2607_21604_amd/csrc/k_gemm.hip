@@ -22,7 +22,11 @@
 
 namespace akvs {
 
-__device__ __forceinline__ float silu(float g) { return g / (1.0f + __expf(-g)); }
+// g * sigmoid(g) with the hardware reciprocal (v_rcp_f32, 1 ulp) in place of an IEEE
+// division, which cost about twice the instructions of the rest of the SwiGLU epilogue
+__device__ __forceinline__ float silu(float g) {
+  return g * __builtin_amdgcn_rcpf(1.0f + __expf(-g));
+}
 
 // Epilogue over an LDS tile Cs[BM][ldc] holding C[m0.., n0..] (SWIGLU: gate cols [0,BN/2),
 // up cols [BN/2,BN) of output columns n0..n0+BN/2).
