@@ -117,7 +117,7 @@ def traffic_summary(fetch_csv, write_csv, workload, refresh):
     lines = [
         f"# k_gemm_bf16 HBM traffic, {workload}-class reuse prefill (r={refresh}), bench.py "
         "counter runs",
-        "# commands (from the repository root, on the GPU box):",
+        "# commands (from the repository root):",
         f"#   rocprofv3 --pmc FETCH_SIZE -f csv -d OUT/fetch -o run -- {run}",
         f"#   rocprofv3 --pmc WRITE_SIZE -f csv -d OUT/write -o run -- {run}",
         f"#   python3 bench.py --workload {workload} --refresh {refresh} --traffic-summary "
