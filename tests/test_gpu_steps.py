@@ -346,13 +346,15 @@ def test_constant_residual_is_recovered_on_gpu():
     ("bf16", 6, 2, 128, 77, 300), ("bf16", 28, 4, 128, 130, 1000), ("bf16", 4, 4, 64, 64, 64),
     ("bf16", 24, 8, 128, 600, 2400), ("bf16", 6, 2, 128, 5, 2000), ("bf16", 24, 8, 128, 3, 4096),
     ("bf16", 28, 4, 128, 1700, 2600), ("bf16", 16, 2, 64, 700, 3000),
+    ("bf16", 64, 8, 128, 900, 3000), ("bf16", 2, 1, 128, 5000, 6000),
     ("f32", 4, 4, 64, 50, 288), ("f32", 6, 3, 128, 9, 70)])
 def test_sparse_query_attention(dtype, hq, hkv, hd, n_rows, n_keys):
     """Against the oracle with and without the key-split workspace. With it, the bf16 calls
     run the planned split: one round of 128-row blocks (600 rows over 2400 keys; hd 64 at
     700 over 3000), one round of 256-row blocks (the few-row cases, up to 8 pieces per tile)
-    and two rounds of them (1700 rows over 2600 keys at 28 query heads), tiles in one piece
-    writing their rows directly."""
+    and two rounds of them (1700 rows over 2600 keys at 28 query heads; 900 over 3000 at 64),
+    tiles in one piece writing their rows directly; at 2 query heads one round of forty
+    128-row tiles in up to 8 pieces each."""
     tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
     rng = np.random.default_rng(n_rows)
     pos = np.sort(rng.choice(n_keys, size=n_rows, replace=False)).astype(np.int32)
