@@ -26,9 +26,9 @@ namespace akvs {
 // (standalone timing, not in the repository). A 32-lane read phase touches 4 rows x 64
 // bytes, at 16-bank offsets: no conflicts.
 
-// Block shape: one query head per block, 32-row waves. With about 200 VGPRs (250 for the
-// read-ahead variant) a compute unit holds eight waves, so blocks of 8 waves (one per unit)
-// or 4 (two per unit) use every SIMD evenly; the first four waves stage the K / V tiles.
+// Block shape: one query head per block, 32-row waves. With about 250 VGPRs a compute unit
+// holds eight waves, so blocks of 8 waves (one per unit) or 4 (two per unit) use every SIMD
+// evenly; the first four waves stage the K / V tiles.
 //  - 256 rows (8 waves sharing each K / V tile) when that still makes 512 blocks (32B probe
 //    layer, 5527 rows over 16128 keys: 1094 us against 1383 us for blocks that grouped the
 //    five query heads of a KV head over 32 rows, whose 5 waves leave SIMDs unevenly loaded);
@@ -143,9 +143,10 @@ __global__ __launch_bounds__(64) void k_attn_plan(const int32_t *pos, int pos0, 
 
 // A block serves head group hg of KV head kvh: 32 * nrb query rows x gh query heads. Wave
 // w owns 32 rows (row block w / gh) of query head kvh * G + hg * gh + w % gh. Waves 0-3
-// stage each 64-key K / V tile in LDS for all of them (double buffered, next tile
-// prefetched into registers during the current one). Block b serves KV head b % Hkv, so
-// the blocks streaming one head's keys run on the same XCD and share its L2.
+// stage each 64-key K / V tile in LDS for all of them (double buffered, the next tile in
+// flight during the current one: hd 128 straight from global memory into LDS, hd 64 through
+// registers). Block b serves KV head b % Hkv, so the blocks streaming one head's keys run on
+// the same XCD and share its L2.
 template <int HD, bool PREF>
 __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
                                                    const int32_t *pos, int pos0, int rows,
@@ -168,7 +169,7 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
   constexpr int CPK = HD / 8;          // 16-byte chunks per key row
   constexpr int LT = 256;              // loading threads (waves 0-3)
   constexpr int KCH = 64 * CPK / LT;   // K (and V) chunks per loading thread
-  // DIR: the tiles go from global memory straight into LDS (8-wave blocks, hd 128)
+  // DIR: the tiles go from global memory straight into LDS (hd 128; PREF: hd 64, 4 waves)
   constexpr bool DIR = !PREF && HD == 128;
   constexpr int KBUF = DIR ? 64 * HD : 64 * KST, VBUF = DIR ? 64 * HD : 64 * VRS;
   // the two buffers of a tile pair; with DIR separate LDS objects (see the loop below)
@@ -269,9 +270,12 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
   // c ^ (r & 15) for K and c ^ 4 (r & 3) for V, so that the 32 K rows of a fragment read
   // and the 4 V rows of a transposing read fall on distinct banks. No registers, no LDS
   // stores in the loading waves: 4.7 % faster on the 32B probe layer (986 -> 940 us), same
-  // bits (standalone harness, not in the repository). On the 4-wave blocks with read-ahead
-  // it was 20-27 % slower (their first transposing read follows the DMA at once, and the
-  // compiler, unable to tell it from the DMA's LDS writes, waits there for the DMA).
+  // bits. The transposing V reads are inline assembly: through the builtin, the compiler
+  // cannot tell them from the DMA's LDS writes and waits for the next tile's DMA before the
+  // first of them, which cost the 4-wave blocks 20-27 % against register staging with
+  // read-ahead; without that wait the 4-wave blocks are 3-8 % faster than the register
+  // staging on the 3B probe layers (1/100 to 3/10 of the context), the 8-wave blocks about
+  // 1 % (standalone harness, not in the repository).
   auto dma_to = [&](int key0_, bf16_t *kbuf, bf16_t *vbuf) {
     const int w = tid >> 6;  // loading wave 0..3
 #pragma unroll
@@ -328,11 +332,10 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
       if (DIR) dma_to(key0 + 64, nks_, nvt_);
       else AKVS_KV_LOAD(key0 + 64);
     }
-    // PREF: the K fragments of a 32-key block are read ahead (the tile's first block here,
-    // its second under the first block's softmax) and each block's V^T fragments are
-    // requested before its score MFMAs, so no MFMA waits on its own LDS read. It needs about
-    // 50 more registers; measured 4 % faster on the four-wave 128-row blocks (3B and 7B
-    // probe layers) and 2 % slower on the eight-wave 256-row blocks (32B probe layer).
+    // PREF (register-staged hd 64 blocks): the K fragments of a 32-key block are read ahead
+    // (the tile's first block here, its second under the first block's softmax) and each
+    // block's V^T fragments are requested before its score MFMAs, so no MFMA waits on its own
+    // LDS read. It needs about 50 more registers.
     bf16x8_t kf[KS];
     if (PREF && key0 <= wmax) {
       const bf16_t *krow = ks_ + (lane & 31) * KST + hi * 8;
@@ -358,17 +361,31 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
                         (lane & 1) * 4
                   : vt_ + (st * 32 + 16 * t + 4 * hi + ((lane & 15) >> 2)) * VRS + db * 32 +
                         16 * ((lane >> 4) & 1) + 4 * (lane & 3);
-          const v4s r0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              (__attribute__((address_space(3))) v4s *)(vb));
-          const v4s r1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              (__attribute__((address_space(3))) v4s *)(vb + 8 * (DIR ? HD : VRS)));
-          uint2 x0, x1;
-          __builtin_memcpy(&x0, &r0, 8);
-          __builtin_memcpy(&x1, &r1, 8);
-          uint32_t vw[4] = {x0.x, x0.y, x1.x, x1.y};
+          uint32_t vw[4];
+          if constexpr (DIR) {
+            // as assembly: the builtin carries no alias information, so the compiler would
+            // wait for the next tile's DMA (vmcnt(0)) before it; the fragments are complete
+            // at the explicit lgkmcnt(0) before the P.V MFMAs (below)
+            typedef unsigned int u2_t __attribute__((ext_vector_type(2)));
+            u2_t x0, x1;
+            const uint32_t a0 =
+                (uint32_t)(size_t)(__attribute__((address_space(3))) const bf16_t *)(vb);
+            asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(x0) : "v"(a0));
+            asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(x1) : "v"(a0), "i"(8 * HD * 2));
+            vw[0] = x0.x; vw[1] = x0.y; vw[2] = x1.x; vw[3] = x1.y;
+          } else {
+            const v4s r0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (__attribute__((address_space(3))) v4s *)(vb));
+            const v4s r1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (__attribute__((address_space(3))) v4s *)(vb + 8 * VRS));
+            uint2 x0, x1;
+            __builtin_memcpy(&x0, &r0, 8);
+            __builtin_memcpy(&x1, &r1, 8);
+            vw[0] = x0.x; vw[1] = x0.y; vw[2] = x1.x; vw[3] = x1.y;
+          }
           __builtin_memcpy(&vf[t][db], vw, 16);
         };
-        if (PREF) {
+        if (PREF || DIR) {  // every V^T fragment of the block requested up front
 #pragma unroll
           for (int t = 0; t < 2; ++t)
 #pragma unroll
@@ -397,11 +414,11 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
             kf[ks] = *reinterpret_cast<const bf16x8_t *>(knext + ks * 16);
         }
         if (sk0 + 31 > wmin || sk0 + 31 >= kv_end) {  // causal / range mask needed
+          // score i is key sk0 + hi*4 + (i/4)*8 + i%4: masked past min(row position, last key)
+          const int lim = min(rpos, kv_end - 1) - (sk0 + hi * 4);
 #pragma unroll
-          for (int i = 0; i < 16; ++i) {
-            const int key = sk0 + (i >> 2) * 8 + hi * 4 + (i & 3);
-            if (key > rpos || key >= kv_end) sc[i] = -INFINITY;
-          }
+          for (int i = 0; i < 16; ++i)
+            if ((i >> 2) * 8 + (i & 3) > lim) sc[i] = -INFINITY;
         }
         float mx = sc[0];
 #pragma unroll
@@ -424,6 +441,12 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
           pv[i] = __builtin_amdgcn_exp2f(fmaf(sc[i], scale_log2, -m_off));  // v_exp_f32: arguments <= 8
           l_run += pv[i];
         }
+        if constexpr (DIR) {  // the assembly reads above: results complete here
+          static_assert(DB == 4, "hd 128");
+          asm volatile("s_waitcnt lgkmcnt(0)"
+                       : "+v"(vf[0][0]), "+v"(vf[0][1]), "+v"(vf[0][2]), "+v"(vf[0][3]),
+                         "+v"(vf[1][0]), "+v"(vf[1][1]), "+v"(vf[1][2]), "+v"(vf[1][3]));
+        }
         // P^T operand of k-step t: slots hi*8 + j hold keys 16t + (j/4)*8 + hi*4 + j%4
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
@@ -434,7 +457,7 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
           __builtin_memcpy(&pb, pw, 16);
 #pragma unroll
           for (int db = 0; db < DB; ++db) {
-            if (!PREF) read_v(t, db);
+            if (!PREF && !DIR) read_v(t, db);
             o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[t][db], pb, o[db], 0, 0, 0);
           }
         }
@@ -463,11 +486,10 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
     if (loader && more) {
       AKVS_KV_LOAD(key0 + 64);
     }
-    // PREF: the K fragments of a 32-key block are read ahead (the tile's first block here,
-    // its second under the first block's softmax) and each block's V^T fragments are
-    // requested before its score MFMAs, so no MFMA waits on its own LDS read. It needs about
-    // 50 more registers; measured 4 % faster on the four-wave 128-row blocks (3B and 7B
-    // probe layers) and 2 % slower on the eight-wave 256-row blocks (32B probe layer).
+    // PREF (register-staged hd 64 blocks): the K fragments of a 32-key block are read ahead
+    // (the tile's first block here, its second under the first block's softmax) and each
+    // block's V^T fragments are requested before its score MFMAs, so no MFMA waits on its own
+    // LDS read. It needs about 50 more registers.
     bf16x8_t kf[KS];
     if (PREF && key0 <= wmax) {
       const bf16_t *krow = ks_ + (lane & 31) * KST + hi * 8;
@@ -532,11 +554,11 @@ __global__ __launch_bounds__(512) void k_attn_bf16(const bf16_t *__restrict__ Q,
             kf[ks] = *reinterpret_cast<const bf16x8_t *>(knext + ks * 16);
         }
         if (sk0 + 31 > wmin || sk0 + 31 >= kv_end) {  // causal / range mask needed
+          // score i is key sk0 + hi*4 + (i/4)*8 + i%4: masked past min(row position, last key)
+          const int lim = min(rpos, kv_end - 1) - (sk0 + hi * 4);
 #pragma unroll
-          for (int i = 0; i < 16; ++i) {
-            const int key = sk0 + (i >> 2) * 8 + hi * 4 + (i & 3);
-            if (key > rpos || key >= kv_end) sc[i] = -INFINITY;
-          }
+          for (int i = 0; i < 16; ++i)
+            if ((i >> 2) * 8 + (i & 3) > lim) sc[i] = -INFINITY;
         }
         float mx = sc[0];
 #pragma unroll
@@ -828,7 +850,7 @@ hipError_t launch_attention(const void *q, const int32_t *pos, int pos0, int row
                      n_keys, hq, hkv, 1, hq / hkv, nrb, 1, e.max_pc, 0, scale_log2, O,             \
                      reinterpret_cast<bf16_t *>(part_o), part_ml, row_base, P)
       if (hd == 128) {
-        if (nrb == 4) AKVS_ATTN_PLANNED(128, true); else AKVS_ATTN_PLANNED(128, false);
+        AKVS_ATTN_PLANNED(128, false);
       } else {
         if (nrb == 4) AKVS_ATTN_PLANNED(64, true); else AKVS_ATTN_PLANNED(64, false);
       }
@@ -846,14 +868,14 @@ hipError_t launch_attention(const void *q, const int32_t *pos, int pos0, int row
     const int split_keys = attn_split_keys(n_keys, n_splits);
     const int n_tiles = (rows + 32 * a.nrb - 1) / (32 * a.nrb);
     dim3 g(n_tiles * hkv * a.n_groups * n_splits), b(64 * a.nrb * a.gh);
-    const bool pref = a.nrb * a.gh <= 4;  // see PREF in the kernel
+    const bool pref = a.nrb * a.gh <= 4;  // hd 64 (see PREF in the kernel)
 #define AKVS_ATTN(HD_, PREF_)                                                                    \
   hipLaunchKernelGGL((k_attn_bf16<HD_, PREF_>), g, b, 0, s, Q, pos, pos0, rows, rows_dev, K, V,    \
                      n_keys, hq, hkv, a.gh, a.n_groups, a.nrb, n_tiles, n_splits, split_keys,      \
                      scale_log2, O, reinterpret_cast<bf16_t *>(part_o), part_ml, row_base,         \
                      nullptr)
     if (hd == 128) {
-      if (pref) AKVS_ATTN(128, true); else AKVS_ATTN(128, false);
+      AKVS_ATTN(128, false);  // the direct-to-LDS staging, 4- and 8-wave blocks alike
     } else {
       if (pref) AKVS_ATTN(64, true); else AKVS_ATTN(64, false);
     }
