@@ -29,97 +29,163 @@ __device__ __forceinline__ float silu(float g) {
 }
 
 // Epilogue over an LDS tile Cs[BM][ldc] holding C[m0.., n0..] (SWIGLU: gate cols [0,BN/2),
-// up cols [BN/2,BN) of output columns n0..n0+BN/2).
+// up cols [BN/2,BN) of output columns n0..n0+BN/2). Thread tid takes items tid + it * NT.
+// The items go in groups whose loads (residual rows, row positions, rotary rows, LDS) are
+// all issued before the group's first result is formed: one memory round trip per group
+// instead of one per item (a loop over single items waits for every residual load, since
+// the compiler cannot move it above the previous item's store to the same buffer).
 template <int BM, int BN, int NT>
 __device__ void epilogue_tile(const float *Cs, int ldc, int m0, int n0, int M_eff, int N,
                               const Epi &e) {
-  const int tid = threadIdx.x;
+  // (loads go to clamped, in-bounds addresses whether or not their item is live, so that no
+  // load sits in a branch whose join would wait for it; only the stores are conditional.
+  // The thread index passes through an opaque move so that the item indices are formed
+  // afresh in each call, not kept live from one half tile's epilogue to the next.)
+  int tid;
+  asm volatile("v_mov_b32 %0, %1" : "=v"(tid) : "v"((int)threadIdx.x));
   if (e.mode == EPI_STORE || e.mode == EPI_RESID) {
-    constexpr int U = BN / 4;
-    for (int idx = tid; idx < BM * U; idx += NT) {
-      const int r = idx / U, c4 = (idx - (idx / U) * U) * 4;
-      const int gm = m0 + r, gn = n0 + c4;
-      if (gm >= M_eff || gn >= N) continue;
-      const float *src = Cs + r * ldc + c4;
-      if (e.mode == EPI_RESID) {
-        float *hp = reinterpret_cast<float *>(e.out) + (size_t)gm * e.ldo + gn;
-        float4 v = *reinterpret_cast<float4 *>(hp);
-        v.x += src[0]; v.y += src[1]; v.z += src[2]; v.w += src[3];
-        *reinterpret_cast<float4 *>(hp) = v;
-      } else if (e.out_dtype == AKVS_BF16) {
-        store4(reinterpret_cast<bf16_t *>(e.out) + (size_t)gm * e.ldo + gn, src[0], src[1], src[2], src[3]);
-      } else {
-        store4(reinterpret_cast<float *>(e.out) + (size_t)gm * e.ldo + gn, src[0], src[1], src[2], src[3]);
+    constexpr int U = BN / 4, ITEMS = BM * U, IT = (ITEMS + NT - 1) / NT;
+    constexpr int EG = IT < 8 ? IT : 8;
+    const bool resid = e.mode == EPI_RESID;
+    for (int it0 = 0; it0 < IT; it0 += EG) {
+      __builtin_amdgcn_sched_barrier(0);  // one group's registers at a time
+      float4 c[EG], h[EG];
+#pragma unroll
+      for (int j = 0; j < EG; ++j) {
+        const int idx = min(tid + (it0 + j) * NT, ITEMS - 1);
+        const int r = idx / U, c4 = (idx - r * U) * 4;
+        c[j] = *reinterpret_cast<const float4 *>(Cs + r * ldc + c4);
+        if (resid)  // N (the model width) is a multiple of 4 here
+          h[j] = *reinterpret_cast<const float4 *>(
+              reinterpret_cast<const float *>(e.out) +
+              (size_t)min(m0 + r, M_eff - 1) * e.ldo + min(n0 + c4, N - 4));
+      }
+#pragma unroll
+      for (int j = 0; j < EG; ++j) {
+        const int idx = tid + (it0 + j) * NT;
+        const int r = idx / U, c4 = (idx - r * U) * 4;
+        const int gm = m0 + r, gn = n0 + c4;
+        if (!(it0 + j < IT && idx < ITEMS && gm < M_eff && gn < N)) continue;
+        const size_t off = (size_t)gm * e.ldo + gn;
+        if (resid) {
+          float4 v = h[j];
+          v.x += c[j].x; v.y += c[j].y; v.z += c[j].z; v.w += c[j].w;
+          *reinterpret_cast<float4 *>(reinterpret_cast<float *>(e.out) + off) = v;
+        } else if (e.out_dtype == AKVS_BF16) {
+          store4(reinterpret_cast<bf16_t *>(e.out) + off, c[j].x, c[j].y, c[j].z, c[j].w);
+        } else {
+          store4(reinterpret_cast<float *>(e.out) + off, c[j].x, c[j].y, c[j].z, c[j].w);
+        }
       }
     }
   } else if (e.mode == EPI_SWIGLU) {
-    constexpr int HALF = BN / 2, U = HALF / 4;
-    for (int idx = tid; idx < BM * U; idx += NT) {
-      const int r = idx / U, c4 = (idx - (idx / U) * U) * 4;
-      const int gm = m0 + r, gn = n0 + c4;
-      if (gm >= M_eff || gn >= N) continue;
-      const float *g = Cs + r * ldc + c4;
-      const float *u = g + HALF;
-      const float a0 = silu(g[0]) * u[0], a1 = silu(g[1]) * u[1];
-      const float a2 = silu(g[2]) * u[2], a3 = silu(g[3]) * u[3];
-      if (e.out_dtype == AKVS_BF16)
-        store4(reinterpret_cast<bf16_t *>(e.out) + (size_t)gm * e.ldo + gn, a0, a1, a2, a3);
-      else
-        store4(reinterpret_cast<float *>(e.out) + (size_t)gm * e.ldo + gn, a0, a1, a2, a3);
+    constexpr int HALF = BN / 2, U = HALF / 4, ITEMS = BM * U, IT = (ITEMS + NT - 1) / NT;
+    constexpr int EG = IT < 4 ? IT : 4;
+    for (int it0 = 0; it0 < IT; it0 += EG) {
+      __builtin_amdgcn_sched_barrier(0);  // one group's registers at a time
+      float4 g[EG], u[EG];
+#pragma unroll
+      for (int j = 0; j < EG; ++j) {
+        const int idx = min(tid + (it0 + j) * NT, ITEMS - 1);
+        const int r = idx / U, c4 = (idx - r * U) * 4;
+        g[j] = *reinterpret_cast<const float4 *>(Cs + r * ldc + c4);
+        u[j] = *reinterpret_cast<const float4 *>(Cs + r * ldc + c4 + HALF);
+      }
+#pragma unroll
+      for (int j = 0; j < EG; ++j) {
+        const int idx = tid + (it0 + j) * NT;
+        const int r = idx / U, c4 = (idx - r * U) * 4;
+        const int gm = m0 + r, gn = n0 + c4;
+        if (!(it0 + j < IT && idx < ITEMS && gm < M_eff && gn < N)) continue;
+        const float a0 = silu(g[j].x) * u[j].x, a1 = silu(g[j].y) * u[j].y;
+        const float a2 = silu(g[j].z) * u[j].z, a3 = silu(g[j].w) * u[j].w;
+        if (e.out_dtype == AKVS_BF16)
+          store4(reinterpret_cast<bf16_t *>(e.out) + (size_t)gm * e.ldo + gn, a0, a1, a2, a3);
+        else
+          store4(reinterpret_cast<float *>(e.out) + (size_t)gm * e.ldo + gn, a0, a1, a2, a3);
+      }
     }
   } else {  // EPI_QKV: every tile holds whole heads of one section
+    // hd (64 or 128) divides BN: a row holds BN / hd heads of hd / 8 items (4 columns of
+    // each rotary half)
     const int hd = e.hd, half = hd >> 1;
-    const int lo_units = half >> 2;
-    const int items = (BN / hd) * lo_units;  // per row
+    const int lu_shift = hd == 128 ? 4 : 3;  // log2 of the items per head (hd / 8)
+    constexpr int items = BN / 8;
+    constexpr int IT = (BM * items + NT - 1) / NT, EG = IT < 4 ? IT : 4;
     const float2 *rope = reinterpret_cast<const float2 *>(e.rope);
-    for (int idx = tid; idx < BM * items; idx += NT) {
-      const int r = idx / items, it = idx - (idx / items) * items;
-      const int hs = it / lo_units, u = it - hs * lo_units;
-      const int gm = m0 + r;
-      if (gm >= M_eff || n0 + hs * hd >= N) continue;
-      const int col = e.n_off + n0 + hs * hd + u * 4;  // logical q|k|v column of the lo half
-      const int pos = e.pos ? e.pos[gm] : e.pos0 + gm;
-      const float *src = Cs + r * ldc + hs * hd + u * 4;
-      float lo[4], hi[4];
+    int rpos[IT];  // row positions of this thread's items, all requested first
+    if (e.pos) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        lo[i] = src[i];
-        hi[i] = src[half + i];
-      }
-      if (col < e.hq_w + e.kv_w) {
-        const int p = min(max(pos - e.rope_base, 0), e.rope_rows - 1);
-        const float2 *rr = rope + (size_t)p * half + u * 4;
+      for (int it = 0; it < IT; ++it)
+        rpos[it] = e.pos[min(m0 + min((tid + it * NT) / items, BM - 1), M_eff - 1)];
+    } else {
+#pragma unroll
+      for (int it = 0; it < IT; ++it) rpos[it] = e.pos0 + m0 + (tid + it * NT) / items;
+    }
+#pragma unroll
+    for (int it0 = 0; it0 < IT; it0 += EG) {
+      __builtin_amdgcn_sched_barrier(0);  // one group's registers at a time
+      float lo[EG][4], hi[EG][4];
+      float2 cs[EG][4];
+#pragma unroll
+      for (int j = 0; j < EG; ++j) {
+        const int idx = min(tid + (it0 + j) * NT, BM * items - 1);
+        const int r = idx / items, it_ = idx - r * items;
+        const int hs = it_ >> lu_shift, u = it_ - (hs << lu_shift);
+        const float *src = Cs + r * ldc + hs * hd + u * 4;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const float2 cs = rr[i];
-          const float a = lo[i], b = hi[i];
-          lo[i] = a * cs.x - b * cs.y;
-          hi[i] = b * cs.x + a * cs.y;
+          lo[j][i] = src[i];
+          hi[j][i] = src[half + i];
+        }
+        if (rope) {
+          const int p = min(max(rpos[it0 + j] - e.rope_base, 0), e.rope_rows - 1);
+          const float2 *rr = rope + (size_t)p * half + u * 4;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) cs[j][i] = rr[i];
         }
       }
-      size_t off;
-      void *base;
-      if (col < e.hq_w) {
-        base = e.q_out;
-        off = (size_t)gm * e.hq_w + col;
-      } else {
-        const int drow = e.kv_by_pos ? pos : gm;
+#pragma unroll
+      for (int j = 0; j < EG; ++j) {
+        const int it = it0 + j;
+        const int idx = tid + it * NT;
+        const int r = idx / items, it_ = idx - r * items;
+        const int hs = it_ >> lu_shift, u = it_ - (hs << lu_shift);
+        const int gm = m0 + r;
+        if (!(it < IT && idx < BM * items && gm < M_eff && n0 + hs * hd < N)) continue;
+        const int col = e.n_off + n0 + hs * hd + u * 4;  // logical q|k|v column of the lo half
         if (col < e.hq_w + e.kv_w) {
-          base = e.k_out;
-          off = (size_t)drow * e.kv_w + (col - e.hq_w);
-        } else {
-          base = e.v_out;
-          off = (size_t)drow * e.kv_w + (col - e.hq_w - e.kv_w);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const float a = lo[j][i], b = hi[j][i];
+            lo[j][i] = a * cs[j][i].x - b * cs[j][i].y;
+            hi[j][i] = b * cs[j][i].x + a * cs[j][i].y;
+          }
         }
-      }
-      if (e.out_dtype == AKVS_BF16) {
-        bf16_t *d = reinterpret_cast<bf16_t *>(base) + off;
-        store4(d, lo[0], lo[1], lo[2], lo[3]);
-        store4(d + half, hi[0], hi[1], hi[2], hi[3]);
-      } else {
-        float *d = reinterpret_cast<float *>(base) + off;
-        store4(d, lo[0], lo[1], lo[2], lo[3]);
-        store4(d + half, hi[0], hi[1], hi[2], hi[3]);
+        size_t off;
+        void *base;
+        if (col < e.hq_w) {
+          base = e.q_out;
+          off = (size_t)gm * e.hq_w + col;
+        } else {
+          const int drow = e.kv_by_pos ? rpos[it] : gm;
+          if (col < e.hq_w + e.kv_w) {
+            base = e.k_out;
+            off = (size_t)drow * e.kv_w + (col - e.hq_w);
+          } else {
+            base = e.v_out;
+            off = (size_t)drow * e.kv_w + (col - e.hq_w - e.kv_w);
+          }
+        }
+        if (e.out_dtype == AKVS_BF16) {
+          bf16_t *d = reinterpret_cast<bf16_t *>(base) + off;
+          store4(d, lo[j][0], lo[j][1], lo[j][2], lo[j][3]);
+          store4(d + half, hi[j][0], hi[j][1], hi[j][2], hi[j][3]);
+        } else {
+          float *d = reinterpret_cast<float *>(base) + off;
+          store4(d, lo[j][0], lo[j][1], lo[j][2], lo[j][3]);
+          store4(d + half, hi[j][0], hi[j][1], hi[j][2], hi[j][3]);
+        }
       }
     }
   }
