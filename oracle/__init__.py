@@ -7,8 +7,8 @@ group-64 cache quantisers: 2/4-bit integer and FP8 E4M3). Only the tests, the sm
 CPU-baseline leg may import it; the library path never does, and it shares no
 code with the HIP kernels.
 
-Every function cites the passage of the paper it follows. Readings of passages
-the paper leaves open are listed in the design notes of the repository.
+Every function cites the passage of the paper it follows; where the paper leaves a
+step open, the function's docstring states the reading it takes.
 """
 from .model import (ModelDims, dims_from, rms_norm, rope_cos_sin, rotate, attention,
                     decoder_layer, full_prefill, cache_units, split_layer, lm_logits,

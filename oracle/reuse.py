@@ -83,8 +83,9 @@ def probe_offset(fresh_probes: np.ndarray, reuse_probes: np.ndarray) -> np.ndarr
 def probe_offset_pre_rope(fresh_probes: np.ndarray, reuse_probes: np.ndarray, positions,
                           theta: float) -> np.ndarray:
     """Key offset taken before the rotary map (the pre-RoPE variant of "Mean estimation",
-    Sec. 3.3; the survey's NEXT variant of reading R2): every probe's fresh-minus-reused
-    difference is rotated back by its own position, then averaged. An empty set gives 0."""
+    Sec. 3.3, whose default form averages the differences after the rotary map): every
+    probe's fresh-minus-reused difference is rotated back by its own position, then
+    averaged. An empty set gives 0."""
     if fresh_probes.shape[0] == 0:
         return np.zeros(fresh_probes.shape[1:], dtype=np.float64)
     diff = fresh_probes - reuse_probes

@@ -21,7 +21,8 @@ with the wrong side's offset or sign all break the equality.
 At the check layer itself the same construction with ||mu_i^c|| < 1 gives a closed form
 for that layer alone (the weights are w = ||mu_i^c||): a non-probe token holds
 K_full - (1 - ||mu_i^c||) mu_i^c, which pins that the check layer corrects its non-probe
-tokens rather than taking the fresh states it computed for every token (reading R8).
+tokens rather than taking the fresh states it computed for every token (Alg. 1 keeps the
+fresh states of the probes only).
 """
 import numpy as np
 import pytest

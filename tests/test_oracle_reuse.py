@@ -204,7 +204,8 @@ def test_first_unit_has_no_residual(small):
 
 def test_check_layer_zero_has_no_value_divergence(small):
     """At the first layer a token's value depends on the token alone, so d_V is 0 up
-    to rounding: the literal layer-1 check cannot rank values (design note R1)."""
+    to rounding: a check at the very first layer cannot rank values, which is why the
+    check layer defaults to the second."""
     dims, w, V, toks, kc, vc = small
     out = oracle.reuse_prefill(toks, w, dims, LENS, Q, kc, vc, refresh=(1, 3), check_layer=0)
     assert np.abs(out["d_v"]).max() < 1e-12
