@@ -386,8 +386,14 @@ def gemm_case(shape, n_rows, seed):
     return w, dims, lw, h
 
 
-@pytest.mark.parametrize("name,n_rows", [("3b", 200), ("7b", 129), ("32b", 300), ("tiny", 70)])
+@pytest.mark.parametrize("name,n_rows", [("3b", 200), ("7b", 129), ("32b", 300), ("tiny", 70),
+                                         ("3b", 1), ("3b", 257), ("7b", 700), ("tiny", 1),
+                                         ("tiny", 33)])
 def test_probe_qkv_and_out_mlp(name, n_rows):
+    """Probe-row projections (QKV with the rotary map, output projection and MLP with the
+    residual adds) against the oracle. Row counts from 1 to 700 cross the 16-, 32-, 192- and
+    256-row tile edges and take both the K-split and the unsplit launches; tiny is the fp32
+    path with 64-wide heads."""
     shape = synthetic.SHAPES[name]
     w, dims, lw, h = gemm_case(shape, n_rows, seed=3)
     tdt = synthetic.torch_dtype(shape)
